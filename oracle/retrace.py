@@ -1,0 +1,192 @@
+"""Float64 reference of the ReTrace round (Section 4, Eq.3-9, Algorithm 1).
+
+Round t, for one sequence whose committed context ends with the anchor at
+position P (target KV and drafter context KV hold rows 0..P-1):
+
+1. Conditioning (Eq.5-9).  If the previous round left a rejected suffix, its
+   retained drafter states h^D and target states h^T are aligned to the new
+   block (m_j = h^D_{r+j}, u_j = h^T_{r+j-1}, 1 <= j <= B-r, with r the previous
+   first rejected position), corrected (c_j = W_c[m_j; u_j], r_j = m_j + beta c_j)
+   and admitted into the mask inputs through the gated residual
+   e~_j = e_j + (W_v r_j) * sigmoid(W_g[e_j; r_j]).  The anchor row and rows
+   without an aligned state keep e_j.
+2. Drafter forward on e~_{0:B} -> h^D_{0:B}, draft tokens y^_j = argmax of the
+   LM head at row j, j = 1..B.
+3. Verify: target forward of [anchor, y^_1..y^_B] at positions P..P+B ->
+   h^T_{0:B}; the target's token for block position i is y^T_i = argmax of row i-1.
+4. Accept: A = longest prefix with y^_i = y^T_i.  Commit y^_1..y^_A and the
+   correction (bonus when A = B) y^T_{A+1}, clipped to the generation budget;
+   the target keeps KV rows up to P+A (rollback), the drafter's context pathway
+   appends rows 0..A, the new anchor is y^T_{A+1} at P+A+1.
+5. Carry: if A < B-1, keep h^D and h^T (rounded to the retained format) with
+   r = A+1 and B-r conditioned rows for the next round; otherwise nothing is
+   carried (full acceptance, or rejection at the last position) -- the signal
+   lives for exactly one round.
+
+Ties in every argmax go to the lowest token id.  Losslessness: the committed
+stream equals target-only greedy decoding (ar_decode).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .model import DraftOut, OracleModel, SeqState, VerifyOut, sigmoid
+
+
+def align_rejected(hD_prev: np.ndarray, hT_prev: np.ndarray, r: int, B: int):
+    """Eq.5 and Eq.6.  Inputs are the previous round's retained states indexed by
+    block row (0..B); returns (m, u), each [B+1][d] indexed by the next block's
+    row j, zero for j = 0 and for j > B - r."""
+    d = hD_prev.shape[1]
+    m = np.zeros((B + 1, d))
+    u = np.zeros((B + 1, d))
+    for j in range(1, B - r + 1):
+        m[j] = hD_prev[r + j]
+        u[j] = hT_prev[r + j - 1]
+    return m, u
+
+
+def condition_inputs(e: np.ndarray, m: np.ndarray, u: np.ndarray, cond_len: int,
+                     w_c: np.ndarray, w_v: np.ndarray, w_g: np.ndarray,
+                     beta: float) -> np.ndarray:
+    """Eq.7 (correction), Eq.8 (corrected signal), Eq.9 (gated residual) for rows
+    j = 1..cond_len.  Weight matrices are [out][in]; W_c's first d input columns
+    act on m and W_g's first d on e."""
+    e_t = e.copy()
+    for j in range(1, cond_len + 1):
+        c = w_c @ np.concatenate([m[j], u[j]])
+        rj = m[j] + beta * c
+        gate = sigmoid(w_g @ np.concatenate([e[j], rj]))
+        e_t[j] = e[j] + (w_v @ rj) * gate
+    return e_t
+
+
+def accept_length(draft: Sequence[int], target: Sequence[int]) -> int:
+    """Number of leading block positions whose draft token equals the target's."""
+    A = 0
+    for a, b in zip(draft, target):
+        if a != b:
+            break
+        A += 1
+    return A
+
+
+def argmax_rows(logits: np.ndarray) -> np.ndarray:
+    """Per-row argmax; np.argmax returns the first maximum, i.e. the lowest id on ties."""
+    return np.argmax(logits, axis=-1)
+
+
+@dataclass
+class RoundRecord:
+    draft: DraftOut
+    verify: VerifyOut
+    y_hat: np.ndarray            # [B] draft tokens for block positions 1..B
+    y_t: np.ndarray              # [B+1] target tokens for block positions 1..B+1
+    A: int
+    committed: List[int]
+    cond_len: int                # rows conditioned in this round
+    P: int                       # anchor position of this round
+
+
+class OracleRunner:
+    """Drives OracleModel through prefill, rounds and the target-only greedy decode."""
+
+    def __init__(self, model: OracleModel):
+        self.m = model
+        self.wl = model.wl
+        self.B = model.wl.B
+
+    # -- prefill: prompt rows through the target, first token, drafter context
+    def prefill(self, prompt, budget: int) -> SeqState:
+        m = self.m
+        st = m.new_state(prompt, budget)
+        out = m.target_forward(st, prompt, 0)
+        first = int(argmax_rows(out.logits[-1]))
+        m.context_append(st, out.g, 0)
+        d = self.wl.target.hidden
+        st.P, st.anchor, st.generated = len(prompt), first, [first]
+        st.hD_prev = np.zeros((self.B + 1, d))
+        st.hT_prev = np.zeros((self.B + 1, d))
+        st.r, st.cond_len = 0, 0
+        return st
+
+    # -- steps of one round, separately callable so a caller can override decisions
+    def draft(self, st: SeqState) -> DraftOut:
+        m, W = self.m, self.m.W
+        e = m.block_inputs(st.anchor)
+        if st.cond_len > 0:
+            mm, uu = align_rejected(st.hD_prev, st.hT_prev, st.r, self.B)
+            e_t = condition_inputs(e, mm, uu, st.cond_len, W["retrace.w_c"], W["retrace.w_v"],
+                                   W["retrace.w_g"], self.wl.beta)
+        else:
+            e_t = e.copy()
+        e_t = m.prec.r(e_t)
+        h, logits = m.drafter_forward(st, e_t)
+        return DraftOut(e=e, e_tilde=e_t, h=h, logits=logits)
+
+    def verify(self, st: SeqState, y_hat: Sequence[int]) -> VerifyOut:
+        return self.m.target_forward(st, [st.anchor] + [int(t) for t in y_hat], st.P)
+
+    def commit(self, st: SeqState, y_hat, y_t, d: DraftOut, v: VerifyOut) -> Tuple[int, List[int]]:
+        B = self.B
+        A = accept_length(y_hat, y_t[:B])
+        new = [int(t) for t in y_hat[:A]] + [int(y_t[A])]
+        new = new[: max(0, st.budget - len(st.generated))]
+        st.generated.extend(new)
+        # rollback: target rows P+A+1..P+B were computed for rejected tokens
+        st.tgt_k[:, st.P + A + 1: st.P + B + 1] = 0.0
+        st.tgt_v[:, st.P + A + 1: st.P + B + 1] = 0.0
+        self.m.context_append(st, v.g[: A + 1], st.P)
+        st.P += A + 1
+        st.anchor = int(y_t[A])
+        if A < B - 1:
+            st.r = A + 1
+            st.cond_len = B - st.r
+            st.hD_prev = self.m.prec.k(d.h)
+            st.hT_prev = self.m.prec.k(v.h)
+        else:
+            st.r, st.cond_len = 0, 0
+            st.hD_prev = np.zeros_like(st.hD_prev)
+            st.hT_prev = np.zeros_like(st.hT_prev)
+        return A, new
+
+    def round(self, st: SeqState, forced_draft: Optional[Sequence[int]] = None) -> RoundRecord:
+        P, cond_len = st.P, st.cond_len
+        d = self.draft(st)
+        y_hat = (np.asarray(forced_draft, dtype=np.int64) if forced_draft is not None
+                 else argmax_rows(d.logits[1:]))
+        v = self.verify(st, y_hat)
+        y_t = argmax_rows(v.logits)
+        A, new = self.commit(st, y_hat, y_t, d, v)
+        return RoundRecord(draft=d, verify=v, y_hat=y_hat, y_t=y_t, A=A, committed=new,
+                           cond_len=cond_len, P=P)
+
+    def spec_decode(self, prompt, budget: int, max_rounds: Optional[int] = None):
+        st = self.prefill(prompt, budget)
+        recs = []
+        while not st.done and (max_rounds is None or len(recs) < max_rounds):
+            recs.append(self.round(st))
+        return st.generated, recs, st
+
+    # -- references
+    def ar_decode(self, prompt, n_new: int) -> List[int]:
+        """Target-only greedy decoding: one row per step, n_new tokens."""
+        m = self.m
+        st = m.new_state(prompt, n_new)
+        out = m.target_forward(st, prompt, 0)
+        tok = int(argmax_rows(out.logits[-1]))
+        toks, pos = [tok], len(prompt)
+        while len(toks) < n_new:
+            out = m.target_forward(st, [tok], pos)
+            tok = int(argmax_rows(out.logits[-1]))
+            toks.append(tok)
+            pos += 1
+        return toks
+
+    def logits_nocache(self, tokens) -> np.ndarray:
+        """Target logits of every row of `tokens`, recomputed from an empty cache."""
+        st = self.m.new_state(tokens, 0)
+        return self.m.target_forward(st, tokens, 0).logits

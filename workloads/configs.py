@@ -1,0 +1,124 @@
+"""Workload presets: model shapes, block size, batch, prompt mix and seeds.
+
+The five named workloads follow the synthetic configurations the method is
+measured on (a tiny fp32 model and Qwen3-0.6B/4B/8B/14B-shaped bf16 models);
+the small extra presets exist only to keep CPU tests fast.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, replace
+from typing import Tuple
+
+
+@dataclass(frozen=True)
+class ModelShape:
+    vocab: int
+    hidden: int
+    n_layers: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn: int
+
+
+def cond_layer_ids(n_layers: int, n_cond: int) -> Tuple[int, ...]:
+    """Evenly spaced target layers whose outputs feed the drafter's context path.
+
+    floor(linspace(1, L-2, n)): reproduces the given {1, 13, 26} for a 28-layer
+    target and gives {1, 9, 17, 25, 34} for 36 layers, {1, 10, 19, 28, 38} for 40.
+    """
+    if n_cond == 1:
+        return (1,)
+    lo, hi = 1, n_layers - 2
+    return tuple(math.floor(lo + (hi - lo) * i / (n_cond - 1)) for i in range(n_cond))
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str                      # "f32" or "bf16": weight / activation storage type
+    target: ModelShape
+    draft_layers: int
+    cond_layers: Tuple[int, ...]
+    block_size: int                 # rows per draft block incl. the anchor; B = block_size-1
+    batch: int
+    prompt_len: Tuple[int, int]     # inclusive range; equal ends = fixed length
+    new_tokens: int                 # generation budget per sequence, first token included
+    seed: int
+    rope_theta: float = 1.0e6
+    rms_eps: float = 1.0e-6
+    page_size: int = 16
+    beta: float = 1.0
+    init_std: float = 0.02
+    norm_init: str = "ones"         # "ones" or "perturbed" (1 + 0.1 N(0,1)); tests use both
+
+    @property
+    def B(self) -> int:
+        return self.block_size - 1
+
+    @property
+    def mask_token_id(self) -> int:
+        return self.target.vocab - 1
+
+    @property
+    def max_prompt(self) -> int:
+        return self.prompt_len[1]
+
+    @property
+    def max_seq_len(self) -> int:
+        # prompt + budget + one full block of scratch rows for the last verify
+        return self.prompt_len[1] + self.new_tokens + self.block_size
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+def _qwen(vocab, hidden, layers, hq, hkv, ffn):
+    return ModelShape(vocab=vocab, hidden=hidden, n_layers=layers, n_q_heads=hq,
+                      n_kv_heads=hkv, head_dim=128, ffn=ffn)
+
+
+PRESETS = {
+    # Tiny fp32 model: 2 target layers, 1 drafter layer conditioned on layers {0,1}.
+    "tiny-f32": Workload(
+        name="tiny-f32", dtype="f32",
+        target=ModelShape(vocab=1024, hidden=256, n_layers=2, n_q_heads=4, n_kv_heads=2,
+                          head_dim=64, ffn=688),
+        draft_layers=1, cond_layers=(0, 1), block_size=8, batch=1, prompt_len=(64, 64),
+        new_tokens=128, seed=0),
+    "qwen3-0.6b-shape": Workload(
+        name="qwen3-0.6b-shape", dtype="bf16", target=_qwen(151936, 1024, 28, 16, 8, 3072),
+        draft_layers=3, cond_layers=(1, 13, 26), block_size=16, batch=1,
+        prompt_len=(512, 512), new_tokens=256, seed=1),
+    "qwen3-4b-shape": Workload(
+        name="qwen3-4b-shape", dtype="bf16", target=_qwen(151936, 2560, 36, 32, 8, 9728),
+        draft_layers=5, cond_layers=cond_layer_ids(36, 5), block_size=16, batch=1,
+        prompt_len=(4096, 4096), new_tokens=512, seed=2),
+    "qwen3-8b-shape-b8": Workload(
+        name="qwen3-8b-shape-b8", dtype="bf16", target=_qwen(151936, 4096, 36, 32, 8, 12288),
+        draft_layers=5, cond_layers=cond_layer_ids(36, 5), block_size=16, batch=8,
+        prompt_len=(1024, 8192), new_tokens=256, seed=3),
+    "qwen3-14b-shape-b16": Workload(
+        name="qwen3-14b-shape-b16", dtype="bf16", target=_qwen(151936, 5120, 40, 40, 8, 17408),
+        draft_layers=5, cond_layers=cond_layer_ids(40, 5), block_size=16, batch=16,
+        prompt_len=(8192, 16384), new_tokens=128, seed=4),
+    # Small bf16 models for fast CPU/GPU tests (not measured workloads).
+    "mini-bf16": Workload(
+        name="mini-bf16", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=256, n_layers=3, n_q_heads=4, n_kv_heads=2,
+                          head_dim=64, ffn=512),
+        draft_layers=2, cond_layers=(0, 1, 2), block_size=16, batch=1, prompt_len=(40, 40),
+        new_tokens=48, seed=7),
+    "mini-bf16-ragged": Workload(
+        name="mini-bf16-ragged", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=256, n_layers=3, n_q_heads=8, n_kv_heads=2,
+                          head_dim=64, ffn=512),
+        draft_layers=2, cond_layers=(0, 2), block_size=16, batch=3, prompt_len=(17, 70),
+        new_tokens=40, seed=8),
+}
+
+
+def get(name: str, **overrides) -> Workload:
+    wl = PRESETS[name]
+    return wl.with_(**overrides) if overrides else wl
