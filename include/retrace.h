@@ -1,0 +1,161 @@
+/*
+ * retrace.h -- C ABI of one ReTrace speculative-decoding round on an MI355X (gfx950).
+ *
+ * The library runs the round of Algorithm 1 of the ReTrace paper for a batch of
+ * independent sequences, every step on the GPU:
+ *   1. rejected-trajectory conditioning: alignment (Eq.5, Eq.6), target-aware
+ *      correction (Eq.7, Eq.8) and gated residual fusion (Eq.9) of the previous
+ *      round's rejected suffix into the next draft block's inputs;
+ *   2. the block drafter (DFlash-style: one pass over the anchor and B mask rows,
+ *      reading a context KV cache fed by captured target states);
+ *   3. the target's block verification (Qwen3-style decoder over a paged KV cache);
+ *   4. greedy prefix acceptance, commit of the accepted drafts plus the target's
+ *      correction token, KV rollback, and the one-round carry / reset rule.
+ * Under greedy verification the committed stream equals the target's own greedy
+ * decoding (Section 4, "Optimization and Inference": verification is unchanged).
+ *
+ * Conventions for every call:
+ *  - Return value: RT_OK (0) or a negative RT_ERR_* code; rt_last_error() then
+ *    returns a thread-local message.  No C++ exception crosses this boundary.
+ *  - Host pointers are owned by the caller and only accessed during the call.
+ *  - The device workspace and the HIP stream are owned by the caller and must stay
+ *    alive until rt_destroy.  The library owns the layout inside the workspace.
+ *  - Calls on one handle must not overlap; separate handles are independent.
+ */
+#ifndef RETRACE_H
+#define RETRACE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  RT_OK = 0,
+  RT_ERR_INVALID = -1,    /* malformed argument or configuration */
+  RT_ERR_STATE = -2,      /* call out of order (e.g. rt_spec_round before rt_prefill) */
+  RT_ERR_CAPACITY = -3,   /* batch, sequence length or budget beyond the configured maxima */
+  RT_ERR_WORKSPACE = -4,  /* workspace smaller than rt_workspace_bytes() or misaligned */
+  RT_ERR_HIP = -5,        /* a HIP runtime call failed */
+  RT_ERR_TOKEN = -6       /* a token id outside [0, vocab) */
+};
+
+enum { RT_F32 = 0, RT_BF16 = 1 };                   /* weight / activation storage type */
+enum { RT_COND_OFF = 0, RT_COND_RETRACE = 1 };     /* OFF: plain block drafting (no carry) */
+
+#define RT_MAX_COND_LAYERS 8
+
+typedef struct rt_config {
+  /* Target (Qwen3-style): vocab, hidden d, layers, query / KV heads, head dim, FFN. */
+  int32_t vocab, hidden, n_layers, n_q_heads, n_kv_heads, head_dim, ffn;
+  float rope_theta;        /* RoPE base (1e6 for Qwen3) */
+  float rms_eps;           /* RMSNorm epsilon (1e-6) */
+  /* Drafter: layers of the target's width; its context pathway reads the target's
+   * residual stream after each listed layer (0-based). */
+  int32_t draft_layers, n_cond_layers, cond_layer_ids[RT_MAX_COND_LAYERS];
+  int32_t block_size;      /* rows per draft block, anchor included: B = block_size - 1 proposals */
+  int32_t mask_token_id;   /* token whose embedding fills the B proposal rows */
+  float beta;              /* correction strength of Eq.8 (1.0 at inference) */
+  int32_t cond_mode;       /* RT_COND_RETRACE or RT_COND_OFF */
+  int32_t dtype;           /* RT_BF16 (fp16 retained states) or RT_F32 (fp32 everywhere) */
+  int32_t max_batch;       /* sequences per batch */
+  int32_t max_seq_len;     /* per sequence: prompt + generation budget + block_size */
+  int32_t page_size;       /* KV page size in tokens; must be 16 */
+} rt_config;
+
+typedef struct rt_model rt_model;   /* opaque handle */
+
+/* Bytes of device workspace the configuration needs (packed weights, paged target
+ * and drafter KV caches, activations, round state).  Returns 0 for an invalid
+ * configuration (see rt_last_error). */
+size_t rt_workspace_bytes(const rt_config* cfg);
+
+/* Number of weight tensors rt_init_models expects for cfg:
+ * 1 + 11*n_layers + 4 + 11*draft_layers + 1 + 3. */
+int32_t rt_weight_count(const rt_config* cfg);
+
+/* Builds a model in `d_workspace` (device memory, >= rt_workspace_bytes, 256-byte
+ * aligned) on `hip_stream` (a hipStream_t; NULL = default stream).
+ *
+ * `weights` holds rt_weight_count() DEVICE pointers, each a row-major [out][in]
+ * tensor of the storage type (bf16 bit patterns or float), in this order:
+ *   embed [V][d];
+ *   per target layer: input_norm [d], q_proj [Hq*hd][d], k_proj [Hkv*hd][d],
+ *     v_proj [Hkv*hd][d], q_norm [hd], k_norm [hd], o_proj [d][Hq*hd],
+ *     post_norm [d], gate_proj [F][d], up_proj [F][d], down_proj [d][F];
+ *   target final_norm [d]; lm_head [V][d] (shared by the drafter);
+ *   drafter fc [d][n_cond*d]; drafter hidden_norm [d];
+ *   per drafter layer: the same eleven tensors as a target layer;
+ *   drafter final_norm [d];
+ *   W_c [d][2d] (Eq.7: first d inputs act on m, last d on u);
+ *   W_v [d][d] (Eq.9); W_g [d][2d] (Eq.9: first d inputs act on e, last d on r).
+ * The weights are copied (re-laid out) into the workspace; the caller may free
+ * them once the call returns.  The call synchronises the stream. */
+int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_weights,
+                   void* d_workspace, size_t ws_bytes, void* hip_stream, rt_model** out);
+
+/* Runs the target over each prompt (concatenated host token ids, lengths in
+ * prompt_lens[n_seqs]), fills the paged target KV cache and the drafter's context
+ * KV cache, and returns each sequence's first generated token (greedy) in
+ * first_tokens[n_seqs] (host).  gen_budget counts new tokens per sequence, the
+ * first one included; prompt_len + gen_budget + block_size must not exceed
+ * max_seq_len.  Resets all round state (nothing is carried into round 1). */
+int rt_prefill(rt_model* m, int32_t n_seqs, const int32_t* prompt_lens, const int32_t* prompt_ids,
+               int32_t gen_budget, int32_t* first_tokens);
+
+/* One ReTrace round for every prefilled sequence.  Outputs (host):
+ *   tokens[n_seqs][block_size]: committed tokens of this round, the first
+ *     n_committed[s] entries valid (accepted drafts, then the target's correction
+ *     or bonus token), -1 elsewhere;
+ *   n_committed[n_seqs]: A+1 clipped to the remaining budget; 0 once finished;
+ *   accept_len[n_seqs]: A, the number of accepted draft tokens.
+ * The rejected-suffix state (retained final drafter / target states, first
+ * rejected position, conditioned-row count) stays in the workspace for the next
+ * round.  Blocks until the outputs are on the host. */
+int rt_spec_round(rt_model* m, int32_t* tokens, int32_t* n_committed, int32_t* accept_len);
+
+/* Releases the handle (the workspace stays the caller's). */
+int rt_destroy(rt_model* m);
+
+/* Message for the last non-zero status returned on this thread. */
+const char* rt_last_error(void);
+
+/* ---- test hooks -------------------------------------------------------------- */
+
+/* Debug flags: 1 = store fp32 logits of both LM heads; 2 = run rounds without
+ * HIP-graph replay. */
+int rt_set_debug(rt_model* m, int32_t flags);
+
+/* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)
+ * instead of the drafter's argmax (the drafter still runs and its states are
+ * still carried). */
+int rt_spec_round_forced(rt_model* m, const int32_t* drafts, int32_t* tokens, int32_t* n_committed,
+                         int32_t* accept_len);
+
+enum {
+  RT_T_DRAFT_LOGITS = 0,   /* [block][V] f32 (needs debug flag 1) */
+  RT_T_VERIFY_LOGITS = 1,  /* [block][V] f32 (needs debug flag 1) */
+  RT_T_HD = 2,             /* [block][d] retained drafter final states (fp16 or f32) */
+  RT_T_HT = 3,             /* [block][d] retained target final states (fp16 or f32) */
+  RT_T_ETILDE = 4,         /* [block][d] f32 conditioned drafter inputs */
+  RT_T_DRAFT_TOKENS = 5,   /* [block] int32: anchor, then the B draft tokens */
+  RT_T_TARGET_TOKENS = 6,  /* [block] int32: target argmax of verify rows 0..B */
+  RT_T_STATE = 7,          /* [8] int32: seq_len, anchor, r, cond_len, budget, round_pos, append, A */
+  RT_T_G = 8,              /* [block][n_cond*d] captured conditioning-layer states (storage type) */
+  RT_T_TARGET_K = 100,     /* + layer: [pos][Hkv][hd] storage type, positions 0.. */
+  RT_T_TARGET_V = 200,     /* + layer */
+  RT_T_DRAFT_K = 300,      /* + drafter layer: context keys */
+  RT_T_DRAFT_V = 400       /* + drafter layer */
+};
+/* Copies `bytes` of tensor `tensor_id` for sequence `seq` to host memory. */
+int rt_debug_read(rt_model* m, int32_t tensor_id, int32_t seq, void* host_dst, size_t bytes);
+/* Overwrites RT_T_HD, RT_T_HT or RT_T_STATE of sequence `seq` from host memory
+ * (state injection for tests). */
+int rt_debug_write(rt_model* m, int32_t tensor_id, int32_t seq, const void* host_src, size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RETRACE_H */

@@ -1,0 +1,170 @@
+"""ctypes binding of libretrace.so: the C ABI of include/retrace.h under the same names.
+
+Argument marshalling only; every step of the round runs in the library's HIP kernels.
+Importing this module loads the in-tree library and fails loudly if it is missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Sequence, Tuple
+
+import numpy as np
+# torch first: its bundled HIP runtime (soname libamdhip64.so.7) is then the one the
+# library binds to, so the process holds a single HIP / HSA runtime.
+import torch  # noqa: F401
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libretrace.so")
+
+RT_OK, RT_ERR_INVALID, RT_ERR_STATE, RT_ERR_CAPACITY, RT_ERR_WORKSPACE, RT_ERR_HIP, RT_ERR_TOKEN = \
+    0, -1, -2, -3, -4, -5, -6
+RT_F32, RT_BF16 = 0, 1
+RT_COND_OFF, RT_COND_RETRACE = 0, 1
+RT_MAX_COND_LAYERS = 8
+(RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
+ RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G) = range(9)
+RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
+
+EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
+           "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
+           "rt_debug_write"]
+
+
+class RetraceError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class rt_config(C.Structure):
+    _fields_ = [("vocab", C.c_int32), ("hidden", C.c_int32), ("n_layers", C.c_int32),
+                ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("ffn", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float),
+                ("draft_layers", C.c_int32), ("n_cond_layers", C.c_int32),
+                ("cond_layer_ids", C.c_int32 * RT_MAX_COND_LAYERS), ("block_size", C.c_int32),
+                ("mask_token_id", C.c_int32), ("beta", C.c_float), ("cond_mode", C.c_int32),
+                ("dtype", C.c_int32), ("max_batch", C.c_int32), ("max_seq_len", C.c_int32),
+                ("page_size", C.c_int32)]
+
+
+def load_library(path: str = LIB_PATH) -> C.CDLL:
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python paper_2608_29748_amd/build.py` "
+                           "(there is no fallback path)")
+    lib = C.CDLL(path)
+    P = C.c_void_p
+    i32p = C.POINTER(C.c_int32)
+    lib.rt_workspace_bytes.argtypes = [C.POINTER(rt_config)]
+    lib.rt_workspace_bytes.restype = C.c_size_t
+    lib.rt_weight_count.argtypes = [C.POINTER(rt_config)]
+    lib.rt_weight_count.restype = C.c_int32
+    lib.rt_init_models.argtypes = [C.POINTER(rt_config), C.POINTER(P), C.c_int32, P, C.c_size_t, P,
+                                   C.POINTER(P)]
+    lib.rt_prefill.argtypes = [P, C.c_int32, i32p, i32p, C.c_int32, i32p]
+    lib.rt_spec_round.argtypes = [P, i32p, i32p, i32p]
+    lib.rt_spec_round_forced.argtypes = [P, i32p, i32p, i32p, i32p]
+    lib.rt_destroy.argtypes = [P]
+    lib.rt_last_error.argtypes = []
+    lib.rt_last_error.restype = C.c_char_p
+    lib.rt_set_debug.argtypes = [P, C.c_int32]
+    lib.rt_debug_read.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
+    lib.rt_debug_write.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
+    for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
+                 "rt_set_debug", "rt_debug_read", "rt_debug_write"):
+        getattr(lib, name).restype = C.c_int
+    return lib
+
+
+_lib = load_library()
+
+
+def _check(status: int) -> None:
+    if status != RT_OK:
+        raise RetraceError(status, rt_last_error())
+
+
+def _i32(a) -> Tuple[np.ndarray, C.POINTER(C.c_int32)]:
+    arr = np.ascontiguousarray(a, dtype=np.int32)
+    return arr, arr.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def make_config(**kw) -> rt_config:
+    """rt_config from keyword fields (cond_layer_ids given as a sequence)."""
+    ids = list(kw.pop("cond_layer_ids"))
+    cfg = rt_config(**kw)
+    cfg.n_cond_layers = len(ids)
+    for i, v in enumerate(ids):
+        cfg.cond_layer_ids[i] = v
+    return cfg
+
+
+def rt_last_error() -> str:
+    m = _lib.rt_last_error()
+    return m.decode() if m else ""
+
+
+def rt_workspace_bytes(cfg: rt_config) -> int:
+    return int(_lib.rt_workspace_bytes(C.byref(cfg)))
+
+
+def rt_weight_count(cfg: rt_config) -> int:
+    return int(_lib.rt_weight_count(C.byref(cfg)))
+
+
+def rt_init_models(cfg: rt_config, weight_ptrs: Sequence[int], ws_ptr: int, ws_bytes: int,
+                   stream_ptr: int = 0) -> int:
+    arr = (C.c_void_p * len(weight_ptrs))(*[C.c_void_p(p) for p in weight_ptrs])
+    h = C.c_void_p()
+    _check(_lib.rt_init_models(C.byref(cfg), arr, len(weight_ptrs), C.c_void_p(ws_ptr), ws_bytes,
+                               C.c_void_p(stream_ptr), C.byref(h)))
+    return h.value
+
+
+def rt_prefill(h: int, prompts: Sequence[np.ndarray], gen_budget: int) -> np.ndarray:
+    lens, lp = _i32([len(p) for p in prompts])
+    ids, ip = _i32(np.concatenate([np.asarray(p) for p in prompts]) if len(prompts) else [])
+    first = np.zeros(len(prompts), np.int32)
+    _check(_lib.rt_prefill(C.c_void_p(h), len(prompts), lp, ip, gen_budget,
+                           first.ctypes.data_as(C.POINTER(C.c_int32))))
+    return first
+
+
+def rt_spec_round(h: int, n_seqs: int, block_size: int):
+    tok = np.full((n_seqs, block_size), -1, np.int32)
+    n = np.zeros(n_seqs, np.int32)
+    a = np.zeros(n_seqs, np.int32)
+    _check(_lib.rt_spec_round(C.c_void_p(h), tok.ctypes.data_as(C.POINTER(C.c_int32)),
+                              n.ctypes.data_as(C.POINTER(C.c_int32)), a.ctypes.data_as(C.POINTER(C.c_int32))))
+    return tok, n, a
+
+
+def rt_spec_round_forced(h: int, drafts: np.ndarray, block_size: int):
+    d, dp = _i32(drafts)
+    n_seqs = d.shape[0]
+    tok = np.full((n_seqs, block_size), -1, np.int32)
+    n = np.zeros(n_seqs, np.int32)
+    a = np.zeros(n_seqs, np.int32)
+    _check(_lib.rt_spec_round_forced(C.c_void_p(h), dp, tok.ctypes.data_as(C.POINTER(C.c_int32)),
+                                     n.ctypes.data_as(C.POINTER(C.c_int32)),
+                                     a.ctypes.data_as(C.POINTER(C.c_int32))))
+    return tok, n, a
+
+
+def rt_set_debug(h: int, flags: int) -> None:
+    _check(_lib.rt_set_debug(C.c_void_p(h), flags))
+
+
+def rt_debug_read(h: int, tensor_id: int, seq: int, nbytes: int) -> bytes:
+    buf = C.create_string_buffer(nbytes)
+    _check(_lib.rt_debug_read(C.c_void_p(h), tensor_id, seq, buf, nbytes))
+    return buf.raw
+
+
+def rt_debug_write(h: int, tensor_id: int, seq: int, data: bytes) -> None:
+    buf = C.create_string_buffer(data, len(data))
+    _check(_lib.rt_debug_write(C.c_void_p(h), tensor_id, seq, buf, len(data)))
+
+
+def rt_destroy(h: int) -> None:
+    _check(_lib.rt_destroy(C.c_void_p(h)))

@@ -1,0 +1,33 @@
+// Paged grouped-query attention for blocks of query rows (verify, draft, prefill).
+#pragma once
+#include "common.h"
+
+namespace rt {
+
+struct AttnArgs {
+  const void* q;                 // [row][n_q_heads * head_dim], row = seq * rows_per_seq + token
+  const void* kcache;            // this layer: K pages [page][kv head][token][hd]
+  const void* vcache;            // this layer: V pages [page][kv head][hd][token]
+  const int32_t* page_table; int max_pages;
+  const int32_t* pos0;           // [seq * seq_stride] position of query token 0
+  const int32_t* nq;             // [seq * seq_stride] valid query tokens (null: rows_per_seq)
+  int seq_stride;
+  int rows_per_seq;
+  int n_seqs;
+  int causal;                    // 1: key position <= query position; 0: every key below pos0+nq
+  int n_q_heads, n_kv_heads, head_dim;
+  int splits;                    // key-range splits per (seq, kv head, row block)
+  int row_blocks;                // row blocks of 64 (token, head) rows per sequence
+  float* opart; float* mlpart;   // split partials
+  void* out; int ldo;            // [row][n_q_heads * head_dim]
+  float scale;                   // 1/sqrt(head_dim)
+};
+
+// Number of query (token, head) rows handled by one workgroup.
+constexpr int kAttnRows = 64;
+
+template <typename T>
+hipError_t attention(const AttnArgs& a, hipStream_t s);
+size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim);
+
+}  // namespace rt

@@ -1,0 +1,111 @@
+// Device-side helpers shared by the ReTrace round kernels (gfx950, wave64).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rt {
+
+typedef uint16_t bf16_t;                                   // bfloat16 bit pattern
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kWave = 64;
+constexpr int kTileK = 32;        // k extent of one packed weight tile
+constexpr int kTileN = 16;        // n extent of one packed weight tile
+constexpr int kPage = 16;         // tokens per KV page
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (bf16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+  _Float16 v; __builtin_memcpy(&v, &h, 2); return (float)v;
+}
+__device__ __forceinline__ uint16_t f32_to_f16(float f) {
+  _Float16 v = (_Float16)f; uint16_t h; __builtin_memcpy(&h, &v, 2); return h;
+}
+
+// Storage-type traits: T is the weight / activation element type (bf16 bit pattern or float).
+template <typename T> struct Elem;
+template <> struct Elem<bf16_t> {
+  static constexpr int kBytes = 2;
+  __device__ static __forceinline__ float to_f32(bf16_t v) { return bf16_to_f32(v); }
+  __device__ static __forceinline__ bf16_t from_f32(float v) { return f32_to_bf16(v); }
+};
+template <> struct Elem<float> {
+  static constexpr int kBytes = 4;
+  __device__ static __forceinline__ float to_f32(float v) { return v; }
+  __device__ static __forceinline__ float from_f32(float v) { return v; }
+};
+
+// Eight consecutive k-values of one operand row, as held by one lane for one
+// 16x16 MFMA tile step over 32 k (the lane's k-group is (lane/16)*8..+8).
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> {
+  bf16x8 v;
+  __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const bf16x8*>(p); }
+  __device__ __forceinline__ void zero() { for (int i = 0; i < 8; ++i) v[i] = 0; }
+  __device__ __forceinline__ float get(int i) const { return bf16_to_f32((bf16_t)v[i]); }
+  __device__ __forceinline__ void set(int i, float f) { v[i] = (short)f32_to_bf16(f); }
+};
+template <> struct Frag<float> {
+  float4 lo, hi;
+  __device__ __forceinline__ void load(const float* p) {
+    lo = *reinterpret_cast<const float4*>(p); hi = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void zero() { lo = make_float4(0, 0, 0, 0); hi = lo; }
+  __device__ __forceinline__ float get(int i) const {
+    switch (i) { case 0: return lo.x; case 1: return lo.y; case 2: return lo.z; case 3: return lo.w;
+                 case 4: return hi.x; case 5: return hi.y; case 6: return hi.z; default: return hi.w; }
+  }
+  __device__ __forceinline__ void set(int i, float f) {
+    switch (i) { case 0: lo.x = f; break; case 1: lo.y = f; break; case 2: lo.z = f; break;
+                 case 3: lo.w = f; break; case 4: hi.x = f; break; case 5: hi.y = f; break;
+                 case 6: hi.z = f; break; default: hi.w = f; }
+  }
+};
+
+// acc[16x16] += A[16 x 32] * B[32 x 16]; lane l holds A row l%16 / B column l%16,
+// k-values (l/16)*8..+8 (any k permutation shared by A and B is valid).
+// Output: lane l, register i -> row 4*(l/16)+i, column l%16.
+__device__ __forceinline__ void mma(f32x4& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x4& acc, const Frag<float>& a, const Frag<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.x, b.lo.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.y, b.lo.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.z, b.lo.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.w, b.lo.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.x, b.hi.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.y, b.hi.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.z, b.hi.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ float warp_sum(float v, int width = 64) {
+  for (int o = width / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float warp_max(float v, int width = 64) {
+  for (int o = width / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Monotone map float -> uint32 (larger float -> larger key).
+__device__ __forceinline__ uint32_t orderable(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+// 64-bit argmax key: value in the high word, (0xffffffff - index) in the low word, so
+// an unsigned max picks the larger value and, among equal values, the lower index.
+__device__ __forceinline__ uint64_t argmax_key(float v, uint32_t idx) {
+  return ((uint64_t)orderable(v) << 32) | (uint64_t)(0xffffffffu - idx);
+}
+__device__ __forceinline__ int32_t key_index(uint64_t key) {
+  return (int32_t)(0xffffffffu - (uint32_t)(key & 0xffffffffu));
+}
+
+}  // namespace rt

@@ -1,0 +1,609 @@
+// Host runtime of the ReTrace round: workspace carving, weight packing, prefill,
+// the round's kernel sequence (captured once into a HIP graph), and the C ABI.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "attn.h"
+#include "gemm.h"
+#include "host.h"
+#include "misc.h"
+
+namespace rt {
+const char* last_error();
+
+#define HIPCHK(x)                                                                          \
+  do {                                                                                     \
+    hipError_t e_ = (x);                                                                   \
+    if (e_ != hipSuccess) return fail(RT_ERR_HIP, "%s: %s", #x, hipGetErrorString(e_));    \
+  } while (0)
+#define CHK(x)                 \
+  do {                         \
+    int s_ = (x);              \
+    if (s_ != RT_OK) return s_; \
+  } while (0)
+
+struct EngineBase {
+  rt_config cfg{};
+  Plan p{};
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  int n_seqs = 0;
+  bool prefilled = false;
+  int flags = 0;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  int32_t* h_out = nullptr;      // pinned: tokens [R], n [bmax], a [bmax], first [bmax]
+  virtual ~EngineBase() {
+    drop_graph();
+    if (h_out) (void)hipHostFree(h_out);
+    if (own_stream && stream) (void)hipStreamDestroy(stream);
+  }
+  void drop_graph() {
+    if (gexec) (void)hipGraphExecDestroy(gexec);
+    if (graph) (void)hipGraphDestroy(graph);
+    gexec = nullptr;
+    graph = nullptr;
+  }
+  template <class X> X* at(size_t off) const { return reinterpret_cast<X*>(ws + off); }
+  virtual int init(const void* const* w) = 0;
+  virtual int prefill(int ns, const int32_t* lens, const int32_t* ids, int budget, int32_t* first) = 0;
+  virtual int run_round(bool forced) = 0;
+  int round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc);
+  int debug_read(int id, int seq, void* dst, size_t bytes);
+  int debug_write(int id, int seq, const void* src, size_t bytes);
+};
+
+template <typename T, typename K>
+struct Engine : EngineBase {
+  const char* tlayer(int l) const { return ws + p.t_layers + (size_t)l * p.layer_bytes; }
+  const char* dlayer(int l) const { return ws + p.d_layers + (size_t)l * p.layer_bytes; }
+
+  int gemm_call(const void* A, int lda, int a_rows, bool af32, const void* B, int N, int Kp, int M,
+                EpiArgs e) {
+    if (M <= 0) return RT_OK;
+    e.M = M;
+    e.N = N;
+    const int shape = M > 64 ? SHAPE_WIDE : SHAPE_SKINNY;
+    const int rows = gemm_tile_rows(shape);
+    const int tiles = ((N + 127) / 128) * ((M + rows - 1) / rows);
+    const int KT = Kp / 32;
+    int ks = 1;
+    if (tiles < 512) {
+      ks = (640 + tiles - 1) / tiles;
+      int maxk = KT / (shape == SHAPE_SKINNY ? 8 : 4);
+      if (maxk < 1) maxk = 1;
+      if (ks > maxk) ks = maxk;
+    }
+    while (ks > 1 && (size_t)tiles * ks * rows * 128 > kPartialFloats) --ks;
+    if (tiles > kMaxTiles) ks = 1;
+    GemmArgs a;
+    a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
+    a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
+    HIPCHK(gemm<T>(a, shape, af32, stream));
+    return RT_OK;
+  }
+
+  struct LayerCtx {
+    int M, rows_per_seq, n_seqs, stride, causal, splits, rb;
+    const int32_t* pos0;
+    const int32_t* nq;
+    const int32_t* pt;
+    T* kc;
+    T* vc;
+    T* cap;
+  };
+
+  int layer(const char* lw, const LayerCtx& c) {
+    const Plan& q = p;
+    float* x = at<float>(q.x);
+    T* xa = at<T>(q.xa);
+    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_in), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr, 0,
+                  stream);
+    EpiArgs e{};
+    e.kind = EPI_QKV; e.out_act = at<T>(q.qbuf); e.ldo = q.qN;
+    e.rows_per_seq = c.rows_per_seq; e.seq_stride = c.stride; e.pos0 = c.pos0; e.nrows = nullptr;
+    e.q_cols = q.qN; e.kv_cols = q.kvN; e.head_dim = q.hd; e.n_kv_heads = q.Hkv; e.layer_cols = q.qkvN;
+    e.q_norm = lw + q.lo_qn; e.k_norm = lw + q.lo_kn; e.norm_layer_stride = 0;
+    e.kcache = c.kc; e.vcache = c.vc; e.cache_layer_stride = 0;
+    e.page_table = c.pt; e.max_pages = q.pages_per_seq;
+    e.rope = at<float>(q.rope); e.rope_max_pos = q.T; e.eps = cfg.rms_eps;
+    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e));
+    AttnArgs a{};
+    a.q = at<T>(q.qbuf); a.kcache = c.kc; a.vcache = c.vc; a.page_table = c.pt; a.max_pages = q.pages_per_seq;
+    a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
+    a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
+    a.splits = c.splits; a.row_blocks = c.rb; a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
+    a.out = at<T>(q.attn); a.ldo = q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
+    HIPCHK(attention<T>(a, stream));
+    e = EpiArgs{};
+    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d;
+    CHK(gemm_call(at<T>(q.attn), q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e));
+    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr,
+                  0, stream);
+    e = EpiArgs{};
+    e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = q.Kp_F;
+    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e));
+    e = EpiArgs{};
+    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = q.Kp_nc;
+    CHK(gemm_call(at<T>(q.mlp), q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e));
+    return RT_OK;
+  }
+
+  int cond_slot(int l) const {
+    for (int i = 0; i < cfg.n_cond_layers; ++i)
+      if (cfg.cond_layer_ids[i] == l) return i;
+    return -1;
+  }
+
+  // Drafter context pathway for M rows: fc -> RMSNorm -> per-layer K (k-norm, RoPE) / V.
+  int context_append(int M, int rows_per_seq, const int32_t* pos0, const int32_t* nrows, int stride,
+                     const int32_t* pt) {
+    const Plan& q = p;
+    EpiArgs e{};
+    e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.fcout); e.ldo = q.d;
+    CHK(gemm_call(at<T>(q.g), q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e));
+    rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), q.Kp_d,
+                  nullptr, 0, nullptr, 0, stream);
+    e = EpiArgs{};
+    e.kind = EPI_QKV; e.rows_per_seq = rows_per_seq; e.seq_stride = stride; e.pos0 = pos0; e.nrows = nrows;
+    e.q_cols = 0; e.kv_cols = q.kvN; e.head_dim = q.hd; e.n_kv_heads = q.Hkv; e.layer_cols = 2 * q.kvN;
+    e.k_norm = at<T>(q.ctx_knorm); e.norm_layer_stride = q.hd;
+    e.kcache = at<T>(q.dkc); e.vcache = at<T>(q.dvc); e.cache_layer_stride = q.cache_layer_elems;
+    e.page_table = pt; e.max_pages = q.pages_per_seq;
+    e.rope = at<float>(q.rope); e.rope_max_pos = q.T; e.eps = cfg.rms_eps;
+    CHK(gemm_call(at<T>(q.fa), q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e));
+    return RT_OK;
+  }
+
+  int init(const void* const* w) override {
+    const Plan& q = p;
+    const size_t E = sizeof(T);
+    auto W = [&](int i) { return (const T*)w[i]; };
+    auto copy = [&](size_t off, int i, size_t n) {
+      return hipMemcpyAsync(ws + off, w[i], n * E, hipMemcpyDeviceToDevice, stream);
+    };
+    fill_zero(ws + q.zero_from, q.total - q.zero_from, stream);
+    HIPCHK(hipGetLastError());
+    HIPCHK(copy(q.embed, 0, (size_t)q.V * q.d));
+    auto pack_layer = [&](char* base, int widx) -> int {
+      T* qkv = (T*)(base + q.lo_qkv);
+      pack_weights<T>(W(widx + 1), q.qN, q.d, q.Kp_d, qkv, stream);
+      pack_weights<T>(W(widx + 2), q.kvN, q.d, q.Kp_d, qkv + (size_t)q.qN * q.Kp_d, stream);
+      pack_weights<T>(W(widx + 3), q.kvN, q.d, q.Kp_d, qkv + (size_t)(q.qN + q.kvN) * q.Kp_d, stream);
+      pack_weights<T>(W(widx + 6), q.d, q.qN, q.Kp_q, (T*)(base + q.lo_o), stream);
+      pack_interleaved<T>(W(widx + 8), W(widx + 9), q.F, q.d, q.Kp_d, (T*)(base + q.lo_gu), stream);
+      pack_weights<T>(W(widx + 10), q.d, q.F, q.Kp_F, (T*)(base + q.lo_down), stream);
+      HIPCHK(hipMemcpyAsync(base + q.lo_in, w[widx + 0], q.d * E, hipMemcpyDeviceToDevice, stream));
+      HIPCHK(hipMemcpyAsync(base + q.lo_post, w[widx + 7], q.d * E, hipMemcpyDeviceToDevice, stream));
+      HIPCHK(hipMemcpyAsync(base + q.lo_qn, w[widx + 4], q.hd * E, hipMemcpyDeviceToDevice, stream));
+      HIPCHK(hipMemcpyAsync(base + q.lo_kn, w[widx + 5], q.hd * E, hipMemcpyDeviceToDevice, stream));
+      HIPCHK(hipGetLastError());
+      return RT_OK;
+    };
+    for (int l = 0; l < q.L; ++l) CHK(pack_layer(ws + q.t_layers + (size_t)l * q.layer_bytes, 1 + 11 * l));
+    const int b2 = 1 + 11 * q.L;
+    HIPCHK(copy(q.t_final_norm, b2, q.d));
+    pack_weights<T>(W(b2 + 1), q.V, q.d, q.Kp_d, at<T>(q.lm_head), stream);
+    pack_weights<T>(W(b2 + 2), q.d, q.nc * q.d, q.Kp_nc, at<T>(q.fc), stream);
+    HIPCHK(copy(q.hidden_norm, b2 + 3, q.d));
+    for (int l = 0; l < q.LD; ++l) {
+      const int widx = b2 + 4 + 11 * l;
+      CHK(pack_layer(ws + q.d_layers + (size_t)l * q.layer_bytes, widx));
+      T* ck = at<T>(q.ctxkv) + (size_t)2 * l * q.kvN * q.Kp_d;
+      pack_weights<T>(W(widx + 2), q.kvN, q.d, q.Kp_d, ck, stream);
+      pack_weights<T>(W(widx + 3), q.kvN, q.d, q.Kp_d, ck + (size_t)q.kvN * q.Kp_d, stream);
+      HIPCHK(hipMemcpyAsync(at<T>(q.ctx_knorm) + (size_t)l * q.hd, w[widx + 5], q.hd * E,
+                            hipMemcpyDeviceToDevice, stream));
+    }
+    const int b3 = b2 + 4 + 11 * q.LD;
+    HIPCHK(copy(q.d_final_norm, b3, q.d));
+    pack_weights<T>(W(b3 + 1), q.d, 2 * q.d, q.Kp_2d, at<T>(q.wc), stream);
+    pack_weights<T>(W(b3 + 2), q.d, q.d, q.Kp_d, at<T>(q.wv), stream);
+    pack_weights<T>(W(b3 + 3), q.d, 2 * q.d, q.Kp_2d, at<T>(q.wg), stream);
+    HIPCHK(hipGetLastError());
+    // page table: page j of sequence s is pool page j * max_batch + s
+    std::vector<int32_t> pt((size_t)q.n_pages);
+    for (int s = 0; s < q.bmax; ++s)
+      for (int j = 0; j < q.pages_per_seq; ++j) pt[(size_t)s * q.pages_per_seq + j] = j * q.bmax + s;
+    HIPCHK(hipMemcpyAsync(ws + q.page_table, pt.data(), pt.size() * 4, hipMemcpyHostToDevice, stream));
+    // RoPE table: angle = fp32(pos * fp32(theta^(-2i/hd))); cos and sin rounded to fp32
+    const int half = q.hd / 2;
+    std::vector<float> rope((size_t)q.T * half * 2);
+    for (int i = 0; i < half; ++i) {
+      const float inv = (float)pow((double)cfg.rope_theta, -2.0 * i / q.hd);
+      for (int pos = 0; pos < q.T; ++pos) {
+        const float ang = (float)pos * inv;
+        rope[(size_t)pos * half + i] = (float)cos((double)ang);
+        rope[(size_t)q.T * half + (size_t)pos * half + i] = (float)sin((double)ang);
+      }
+    }
+    HIPCHK(hipMemcpyAsync(ws + q.rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice, stream));
+    HIPCHK(hipStreamSynchronize(stream));
+    return RT_OK;
+  }
+
+  int prefill(int ns, const int32_t* lens, const int32_t* ids, int budget, int32_t* first) override {
+    const Plan& q = p;
+    drop_graph();
+    prefilled = false;
+    size_t off = 0;
+    int32_t* pf = at<int32_t>(q.pf_ints);
+    int32_t* tok = at<int32_t>(q.tokbuf);
+    for (int s = 0; s < ns; ++s) {
+      const int len = lens[s];
+      HIPCHK(hipMemcpyAsync(tok, ids + off, (size_t)len * 4, hipMemcpyHostToDevice, stream));
+      const int32_t* pt = at<int32_t>(q.page_table) + (size_t)s * q.pages_per_seq;
+      for (int c0 = 0; c0 < len; c0 += q.PF) {
+        const int n = len - c0 < q.PF ? len - c0 : q.PF;
+        set_ints(pf, 2, c0, n, 0, 0, stream);
+        embed_rows<T>(at<T>(q.embed), q.d, tok + c0, n, at<float>(q.x), q.d, stream);
+        for (int l = 0; l < q.L; ++l) {
+          const int slot = cond_slot(l);
+          LayerCtx c{n, q.PF, 1, 0, 1, 1, (n * q.G + 63) / 64, pf, pf + 1, pt,
+                     at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
+                     slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr};
+          CHK(layer(tlayer(l), c));
+        }
+        CHK(context_append(n, q.PF, pf, nullptr, 0, pt));
+        if (c0 + n == len) {
+          rmsnorm<T, K>(at<float>(q.x) + (size_t)(n - 1) * q.d, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, 1,
+                        at<T>(q.xa), q.Kp_d, nullptr, 0, at<uint64_t>(q.tkeys), 1, stream);
+          EpiArgs e{};
+          e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.tkeys);
+          CHK(gemm_call(at<T>(q.xa), q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, 1, e));
+          first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), len, budget, at<int32_t>(q.first_tok), stream);
+        }
+        HIPCHK(hipGetLastError());
+      }
+      HIPCHK(hipStreamSynchronize(stream));   // the token buffer is reused by the next sequence
+      off += (size_t)len;
+    }
+    fill_zero(ws + q.hd_keep, (size_t)q.R * q.d * q.ksz, stream);
+    fill_zero(ws + q.ht_keep, (size_t)q.R * q.d * q.ksz, stream);
+    HIPCHK(hipMemcpyAsync(h_out, ws + q.first_tok, (size_t)ns * 4, hipMemcpyDeviceToHost, stream));
+    HIPCHK(hipStreamSynchronize(stream));
+    memcpy(first, h_out, (size_t)ns * 4);
+    n_seqs = ns;
+    prefilled = true;
+    return RT_OK;
+  }
+
+  int run_round(bool forced) override {
+    const Plan& q = p;
+    const int R = n_seqs * q.bk;
+    int32_t* st = at<int32_t>(q.state);
+    float* x = at<float>(q.x);
+    T* xa = at<T>(q.xa);
+    const int32_t* pt = at<int32_t>(q.page_table);
+    // (1) rejected-trajectory conditioning (Eq.5-9)
+    if (cfg.cond_mode == RT_COND_RETRACE) {
+      cond_prep<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, at<K>(q.hd_keep), at<K>(q.ht_keep), n_seqs, q.bk,
+                      at<float>(q.mu), at<float>(q.er), stream);
+      EpiArgs e{};
+      e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er) + q.d; e.ldo = 2 * q.d;
+      e.cond_m = at<float>(q.mu); e.ld_cond_m = 2 * q.d; e.beta = cfg.beta;
+      CHK(gemm_call(at<float>(q.mu), 2 * q.d, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e));
+      e = EpiArgs{};
+      e.kind = EPI_COND_GATE; e.out_f32 = at<float>(q.gate); e.ldo = q.d;
+      CHK(gemm_call(at<float>(q.er), 2 * q.d, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e));
+      e = EpiArgs{};
+      e.kind = EPI_COND_OUT; e.resid = x; e.ldr = q.d; e.etilde = at<float>(q.etilde);
+      e.gate = at<float>(q.gate); e.ld_gate = q.d; e.embed = at<T>(q.embed); e.mask_token = cfg.mask_token_id;
+      e.anchor = st + ST_ANCHOR; e.cond_len = st + ST_COND_LEN; e.seq_stride = kStateFields;
+      e.rows_per_seq = q.bk;
+      CHK(gemm_call(at<float>(q.er) + q.d, 2 * q.d, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e));
+    } else {
+      embed_block<T>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), q.d, stream);
+    }
+    // (2) drafter: B+1 rows at P..P+B over its context cache (no causal mask in the block)
+    for (int l = 0; l < q.LD; ++l) {
+      LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
+                 at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
+                 nullptr};
+      CHK(layer(dlayer(l), c));
+    }
+    rmsnorm<T, K>(x, q.d, at<T>(q.d_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.hd_keep), q.d,
+                  at<uint64_t>(q.dkeys), R, stream);
+    EpiArgs e{};
+    e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.dkeys);
+    e.out_f32 = (flags & 1) ? at<float>(q.dlogits) : nullptr; e.ldo = q.V;
+    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, R, e));
+    // (3) verify: [anchor, drafts] at P..P+B, causal over the target cache
+    embed_verify<T>(at<T>(q.embed), q.d, st, at<uint64_t>(q.dkeys), forced ? 1 : 0, at<int32_t>(q.dtok), n_seqs,
+                    q.bk, x, q.d, stream);
+    for (int l = 0; l < q.L; ++l) {
+      const int slot = cond_slot(l);
+      LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
+                 at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
+                 slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr};
+      CHK(layer(tlayer(l), c));
+    }
+    rmsnorm<T, K>(x, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.ht_keep), q.d,
+                  at<uint64_t>(q.tkeys), R, stream);
+    e = EpiArgs{};
+    e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.tkeys);
+    e.out_f32 = (flags & 1) ? at<float>(q.vlogits) : nullptr; e.ldo = q.V;
+    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, R, e));
+    // (4) acceptance, commit, rollback, carry / reset
+    accept(st, at<int32_t>(q.dtok), at<uint64_t>(q.tkeys), at<int32_t>(q.ttok), n_seqs, q.bk, at<int32_t>(q.out_tok),
+           at<int32_t>(q.out_n), at<int32_t>(q.out_a), stream);
+    // drafter context pathway for the committed rows 0..A at P..P+A
+    CHK(context_append(R, q.bk, st + ST_ROUND_POS, st + ST_APPEND, kStateFields, pt));
+    HIPCHK(hipGetLastError());
+    return RT_OK;
+  }
+};
+
+int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc) {
+  if (!prefilled) return fail(RT_ERR_STATE, "rt_spec_round called before rt_prefill");
+  if (!tokens || !n_comm || !acc) return fail(RT_ERR_INVALID, "null output pointer");
+  const Plan& q = p;
+  if (forced) {
+    std::vector<int32_t> h((size_t)n_seqs * q.bk, 0);
+    for (int s = 0; s < n_seqs; ++s)
+      for (int i = 1; i < q.bk; ++i) {
+        const int32_t t = forced[(size_t)s * q.B + i - 1];
+        if (t < 0 || t >= q.V) return fail(RT_ERR_TOKEN, "forced draft token %d out of range", t);
+        h[(size_t)s * q.bk + i] = t;
+      }
+    HIPCHK(hipMemcpyAsync(ws + q.dtok, h.data(), h.size() * 4, hipMemcpyHostToDevice, stream));
+    CHK(run_round(true));
+  } else if (flags & 2) {
+    CHK(run_round(false));
+  } else {
+    if (!gexec) {
+      HIPCHK(hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal));
+      int st = run_round(false);
+      hipGraph_t g = nullptr;
+      hipError_t ce = hipStreamEndCapture(stream, &g);
+      if (st != RT_OK) { if (g) (void)hipGraphDestroy(g); return st; }
+      if (ce != hipSuccess) return fail(RT_ERR_HIP, "graph capture: %s", hipGetErrorString(ce));
+      graph = g;
+      HIPCHK(hipGraphInstantiate(&gexec, graph, nullptr, nullptr, 0));
+    }
+    HIPCHK(hipGraphLaunch(gexec, stream));
+  }
+  const size_t R = (size_t)n_seqs * q.bk;
+  HIPCHK(hipMemcpyAsync(h_out, ws + q.out_tok, R * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipMemcpyAsync(h_out + q.R, ws + q.out_n, (size_t)n_seqs * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipMemcpyAsync(h_out + q.R + q.bmax, ws + q.out_a, (size_t)n_seqs * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  memcpy(tokens, h_out, R * 4);
+  memcpy(n_comm, h_out + q.R, (size_t)n_seqs * 4);
+  memcpy(acc, h_out + q.R + q.bmax, (size_t)n_seqs * 4);
+  return RT_OK;
+}
+
+static int copy_pages(const EngineBase& m, size_t cache_off, int layer, int seq, bool vlayout, void* dst,
+                      size_t bytes) {
+  const Plan& q = m.p;
+  const size_t E = q.esz, hd = q.hd, H = q.Hkv;
+  const size_t per_pos = H * hd * E;
+  const size_t npos = bytes / per_pos;
+  if (npos > (size_t)q.T) return fail(RT_ERR_INVALID, "read past max_seq_len");
+  std::vector<int32_t> pt((size_t)q.pages_per_seq);
+  HIPCHK(hipMemcpy(pt.data(), m.ws + q.page_table + (size_t)seq * q.pages_per_seq * 4, pt.size() * 4,
+                   hipMemcpyDeviceToHost));
+  const size_t page_bytes = H * 16 * hd * E;
+  std::vector<char> buf(page_bytes);
+  char* out = (char*)dst;
+  for (size_t pg = 0; pg * 16 < npos; ++pg) {
+    const char* src = m.ws + cache_off + ((size_t)layer * q.cache_layer_elems) * E + (size_t)pt[pg] * page_bytes;
+    HIPCHK(hipMemcpy(buf.data(), src, page_bytes, hipMemcpyDeviceToHost));
+    for (size_t t = 0; t < 16 && pg * 16 + t < npos; ++t)
+      for (size_t h = 0; h < H; ++h)
+        for (size_t e = 0; e < hd; ++e) {
+          const size_t si = vlayout ? ((h * hd + e) * 16 + t) : ((h * 16 + t) * hd + e);
+          memcpy(out + ((pg * 16 + t) * H * hd + h * hd + e) * E, buf.data() + si * E, E);
+        }
+  }
+  return RT_OK;
+}
+
+int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
+  const Plan& q = p;
+  if (!dst) return fail(RT_ERR_INVALID, "null destination");
+  if (seq < 0 || seq >= q.bmax) return fail(RT_ERR_INVALID, "sequence index out of range");
+  size_t off = 0, cap = 0;
+  const size_t bk = q.bk;
+  switch (id) {
+    case RT_T_DRAFT_LOGITS: off = q.dlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
+    case RT_T_VERIFY_LOGITS: off = q.vlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
+    case RT_T_HD: off = q.hd_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
+    case RT_T_HT: off = q.ht_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
+    case RT_T_ETILDE: off = q.etilde + seq * bk * q.d * 4; cap = bk * q.d * 4; break;
+    case RT_T_DRAFT_TOKENS: off = q.dtok + seq * bk * 4; cap = bk * 4; break;
+    case RT_T_TARGET_TOKENS: off = q.ttok + seq * bk * 4; cap = bk * 4; break;
+    case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
+    case RT_T_G: {
+      const size_t row = (size_t)q.nc * q.d * q.esz;
+      if (bytes > bk * row) return fail(RT_ERR_INVALID, "read too large");
+      HIPCHK(hipStreamSynchronize(stream));
+      HIPCHK(hipMemcpy2D(dst, row, ws + q.g + seq * bk * q.Kp_nc * q.esz, (size_t)q.Kp_nc * q.esz, row,
+                         bytes / row, hipMemcpyDeviceToHost));
+      return RT_OK;
+    }
+    default: {
+      HIPCHK(hipStreamSynchronize(stream));
+      if (id >= RT_T_TARGET_K && id < RT_T_TARGET_K + q.L) return copy_pages(*this, q.kc, id - RT_T_TARGET_K, seq, false, dst, bytes);
+      if (id >= RT_T_TARGET_V && id < RT_T_TARGET_V + q.L) return copy_pages(*this, q.vc, id - RT_T_TARGET_V, seq, true, dst, bytes);
+      if (id >= RT_T_DRAFT_K && id < RT_T_DRAFT_K + q.LD) return copy_pages(*this, q.dkc, id - RT_T_DRAFT_K, seq, false, dst, bytes);
+      if (id >= RT_T_DRAFT_V && id < RT_T_DRAFT_V + q.LD) return copy_pages(*this, q.dvc, id - RT_T_DRAFT_V, seq, true, dst, bytes);
+      return fail(RT_ERR_INVALID, "unknown tensor id %d", id);
+    }
+  }
+  if (bytes > cap) return fail(RT_ERR_INVALID, "read of %zu bytes exceeds %zu", bytes, cap);
+  HIPCHK(hipStreamSynchronize(stream));
+  HIPCHK(hipMemcpy(dst, ws + off, bytes, hipMemcpyDeviceToHost));
+  return RT_OK;
+}
+
+int EngineBase::debug_write(int id, int seq, const void* src, size_t bytes) {
+  const Plan& q = p;
+  if (!src) return fail(RT_ERR_INVALID, "null source");
+  if (seq < 0 || seq >= q.bmax) return fail(RT_ERR_INVALID, "sequence index out of range");
+  size_t off = 0, cap = 0;
+  const size_t bk = q.bk;
+  switch (id) {
+    case RT_T_HD: off = q.hd_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
+    case RT_T_HT: off = q.ht_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
+    case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
+    default: return fail(RT_ERR_INVALID, "tensor id %d is not writable", id);
+  }
+  if (bytes > cap) return fail(RT_ERR_INVALID, "write of %zu bytes exceeds %zu", bytes, cap);
+  HIPCHK(hipStreamSynchronize(stream));
+  HIPCHK(hipMemcpy(ws + off, src, bytes, hipMemcpyHostToDevice));
+  return RT_OK;
+}
+
+}  // namespace rt
+
+struct rt_model {
+  rt::EngineBase* e;
+};
+
+using namespace rt;
+
+extern "C" {
+
+size_t rt_workspace_bytes(const rt_config* cfg) {
+  Plan p;
+  if (make_plan(cfg, &p) != RT_OK) return 0;
+  return p.total;
+}
+
+int32_t rt_weight_count(const rt_config* cfg) {
+  if (validate_config(cfg) != RT_OK) return 0;
+  return weight_count(cfg);
+}
+
+int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_weights, void* d_workspace,
+                   size_t ws_bytes, void* hip_stream, rt_model** out) {
+  try {
+    if (!out) return fail(RT_ERR_INVALID, "out handle pointer is null");
+    *out = nullptr;
+    Plan p;
+    int st = make_plan(cfg, &p);
+    if (st) return st;
+    if (!weights) return fail(RT_ERR_INVALID, "weights is null");
+    if (n_weights != weight_count(cfg))
+      return fail(RT_ERR_INVALID, "expected %d weight tensors, got %d", weight_count(cfg), n_weights);
+    for (int i = 0; i < n_weights; ++i)
+      if (!weights[i]) return fail(RT_ERR_INVALID, "weight %d is null", i);
+    if (!d_workspace) return fail(RT_ERR_WORKSPACE, "workspace is null");
+    if ((uintptr_t)d_workspace % 256) return fail(RT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (ws_bytes < p.total) return fail(RT_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
+    EngineBase* e = nullptr;
+    if (cfg->dtype == RT_BF16) e = new (std::nothrow) Engine<bf16_t, uint16_t>();
+    else e = new (std::nothrow) Engine<float, float>();
+    if (!e) return fail(RT_ERR_INVALID, "out of host memory");
+    e->cfg = *cfg;
+    e->p = p;
+    e->ws = (char*)d_workspace;
+    if (hip_stream) {
+      e->stream = (hipStream_t)hip_stream;
+    } else {
+      hipError_t he = hipStreamCreateWithFlags(&e->stream, hipStreamNonBlocking);
+      if (he != hipSuccess) { delete e; return fail(RT_ERR_HIP, "hipStreamCreate: %s", hipGetErrorString(he)); }
+      e->own_stream = true;
+    }
+    hipError_t he = hipHostMalloc((void**)&e->h_out, ((size_t)p.R + 3 * (size_t)p.bmax) * 4, hipHostMallocDefault);
+    if (he != hipSuccess) { delete e; return fail(RT_ERR_HIP, "hipHostMalloc: %s", hipGetErrorString(he)); }
+    st = e->init(weights);
+    if (st) { delete e; return st; }
+    rt_model* m = new (std::nothrow) rt_model{e};
+    if (!m) { delete e; return fail(RT_ERR_INVALID, "out of host memory"); }
+    *out = m;
+    return RT_OK;
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_init_models");
+  }
+}
+
+int rt_prefill(rt_model* m, int32_t n_seqs, const int32_t* prompt_lens, const int32_t* prompt_ids,
+               int32_t gen_budget, int32_t* first_tokens) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    EngineBase& e = *m->e;
+    if (!prompt_lens || !prompt_ids || !first_tokens) return fail(RT_ERR_INVALID, "null pointer argument");
+    if (n_seqs < 1 || n_seqs > e.p.bmax) return fail(RT_ERR_CAPACITY, "n_seqs %d outside [1, %d]", n_seqs, e.p.bmax);
+    if (gen_budget < 1) return fail(RT_ERR_INVALID, "gen_budget must be >= 1");
+    size_t total = 0;
+    for (int s = 0; s < n_seqs; ++s) {
+      const int len = prompt_lens[s];
+      if (len < 1) return fail(RT_ERR_INVALID, "prompt %d is empty", s);
+      if ((long long)len + gen_budget + e.p.bk > e.p.T)
+        return fail(RT_ERR_CAPACITY, "prompt %d: length %d + budget %d + block %d exceeds max_seq_len %d", s, len,
+                    gen_budget, e.p.bk, e.p.T);
+      total += (size_t)len;
+    }
+    for (size_t i = 0; i < total; ++i)
+      if (prompt_ids[i] < 0 || prompt_ids[i] >= e.p.V) return fail(RT_ERR_TOKEN, "prompt token %d out of range", prompt_ids[i]);
+    return e.prefill(n_seqs, prompt_lens, prompt_ids, gen_budget, first_tokens);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_prefill");
+  }
+}
+
+int rt_spec_round(rt_model* m, int32_t* tokens, int32_t* n_committed, int32_t* accept_len) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    return m->e->round(nullptr, tokens, n_committed, accept_len);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_spec_round");
+  }
+}
+
+int rt_spec_round_forced(rt_model* m, const int32_t* drafts, int32_t* tokens, int32_t* n_committed,
+                         int32_t* accept_len) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    if (!drafts) return fail(RT_ERR_INVALID, "null drafts");
+    return m->e->round(drafts, tokens, n_committed, accept_len);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_spec_round_forced");
+  }
+}
+
+int rt_set_debug(rt_model* m, int32_t flags) {
+  if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+  if (flags < 0 || flags > 3) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  m->e->flags = flags;
+  m->e->drop_graph();
+  return RT_OK;
+}
+
+int rt_debug_read(rt_model* m, int32_t tensor_id, int32_t seq, void* host_dst, size_t bytes) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    return m->e->debug_read(tensor_id, seq, host_dst, bytes);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_debug_read");
+  }
+}
+
+int rt_debug_write(rt_model* m, int32_t tensor_id, int32_t seq, const void* host_src, size_t bytes) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    return m->e->debug_write(tensor_id, seq, host_src, bytes);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_debug_write");
+  }
+}
+
+int rt_destroy(rt_model* m) {
+  if (!m) return fail(RT_ERR_INVALID, "null model");
+  if (m->e) (void)hipStreamSynchronize(m->e->stream);
+  delete m->e;
+  delete m;
+  return RT_OK;
+}
+
+const char* rt_last_error(void) { return rt::last_error(); }
+
+}  // extern "C"

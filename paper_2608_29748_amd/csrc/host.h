@@ -1,0 +1,51 @@
+// Host-side planning shared by the C ABI: configuration checks, derived sizes and the
+// workspace layout.  Nothing here touches the GPU, so the checks can be exercised
+// without one.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "../../include/retrace.h"
+
+namespace rt {
+
+void set_error(const char* fmt, ...);
+int fail(int code, const char* fmt, ...);   // sets the message, returns code
+
+int validate_config(const rt_config* c);
+int weight_count(const rt_config* c);
+
+inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+constexpr int kPrefillChunk = 512;     // prompt rows per prefill pass
+constexpr int kMaxTiles = 1 << 16;     // split-K arrival counters
+constexpr size_t kPartialFloats = (size_t)8 << 20;   // split-K partial capacity (32 MiB)
+
+struct Plan {
+  // dimensions
+  int V, d, L, Hq, Hkv, hd, F, LD, nc, bk, B, bmax, T, G;
+  int qN, kvN, qkvN;                     // q columns, k (= v) columns, fused q|k|v columns
+  int Kp_d, Kp_q, Kp_F, Kp_nc, Kp_2d;    // padded reduction lengths
+  int esz, ksz;                          // storage / retained element bytes
+  int pages_per_seq, n_pages;
+  int R, PF, Mrows;                      // round rows, prefill rows, allocated activation rows
+  int attn_rb, attn_splits;              // round attention row blocks / key splits
+  int pf_rb;
+  size_t cache_layer_elems;
+  // byte offsets into the workspace
+  size_t embed, lm_head, t_final_norm, d_final_norm, fc, hidden_norm, ctxkv, ctx_knorm, wc, wg, wv;
+  size_t t_layers, d_layers, layer_bytes;               // per-layer blocks
+  size_t lo_qkv, lo_o, lo_gu, lo_down, lo_in, lo_post, lo_qn, lo_kn;   // offsets within a layer block
+  size_t kc, vc, dkc, dvc;
+  size_t page_table, rope, state, pf_ints, first_tok, counters, partial, opart, mlpart;
+  size_t x, xa, qbuf, attn, mlp, g, fcout, fa, etilde, mu, er, gate;
+  size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
+  size_t zero_from;                      // everything from here on is zero-filled at init
+  size_t total;
+};
+
+int make_plan(const rt_config* c, Plan* p);
+
+}  // namespace rt

@@ -1,0 +1,46 @@
+// Small kernels of the round: RMSNorm, embedding gathers, conditioning gather,
+// acceptance / rollback, and state set-up.
+#pragma once
+#include "common.h"
+
+namespace rt {
+
+// Per-sequence round state, one int32 array of kStateFields per sequence.
+enum StateField : int {
+  ST_SEQ_LEN = 0,    // anchor position P = number of valid target KV rows
+  ST_ANCHOR,         // last committed token (block row 0 of the next draft)
+  ST_R,              // first rejected block position of the last round (A + 1)
+  ST_COND_LEN,       // rows conditioned in the next draft (B - r, or 0)
+  ST_BUDGET,         // tokens still to generate
+  ST_ROUND_POS,      // P of the round just verified (context-append base)
+  ST_APPEND,         // rows of that round to append to the drafter context (A + 1, or 0)
+  ST_ACCEPT,         // A of the last round
+  kStateFields
+};
+
+template <typename T, typename K>
+void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldo,
+             K* keep, int ldk, uint64_t* zero_keys, int nzero, hipStream_t s);
+template <typename T>
+void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s);
+// Drafter input without conditioning: row (s, 0) = E[anchor], rows (s, j>0) = E[mask].
+template <typename T>
+void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk,
+                 float* x, float* etilde, int ldx, hipStream_t s);
+// Verify input: row (s, 0) = E[anchor], row (s, i) = E[draft token i]; also records the
+// draft tokens (decoded from the drafter's argmax keys unless `forced`).
+template <typename T>
+void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* dkeys, int forced,
+                  int32_t* dtok, int n_seqs, int bk, float* x, int ldx, hipStream_t s);
+// Conditioning gather (Eq.5/6): mu = [m | u] rows, er[:, :d] = e rows.
+template <typename T, typename K>
+void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
+               int n_seqs, int bk, float* mu, float* er, hipStream_t s);
+void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs,
+            int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
+void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s);
+void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
+                 int32_t* first_out, hipStream_t s);
+void fill_zero(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace rt

@@ -1,0 +1,235 @@
+#include "misc.h"
+
+namespace rt {
+
+// ------------------------------------------------------------------ RMSNorm
+template <typename K> struct KeepT;
+template <> struct KeepT<uint16_t> { __device__ static uint16_t of(float v) { return f32_to_f16(v); } };
+template <> struct KeepT<float> { __device__ static float of(float v) { return v; } };
+
+template <typename T, typename K>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
+                                                      const T* __restrict__ w, int d, float eps,
+                                                      T* __restrict__ out, int ldo, K* keep, int ldk,
+                                                      uint64_t* zero_keys, int nzero) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const float* xr = x + (size_t)row * ldx;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) { const float v = xr[i]; ss += v * v; }
+  ss = warp_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = xr[i] * inv * Elem<T>::to_f32(w[i]);
+    out[(size_t)row * ldo + i] = Elem<T>::from_f32(v);
+    if (keep) keep[(size_t)row * ldk + i] = KeepT<K>::of(v);
+  }
+  if (zero_keys && row == 0)
+    for (int i = threadIdx.x; i < nzero; i += 256) zero_keys[i] = 0ull;
+}
+
+template <typename T, typename K>
+void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldo,
+             K* keep, int ldk, uint64_t* zero_keys, int nzero, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldo,
+                     keep, ldk, zero_keys, nzero);
+}
+template void rmsnorm<bf16_t, uint16_t>(const float*, int, const bf16_t*, int, float, int, bf16_t*, int,
+                                        uint16_t*, int, uint64_t*, int, hipStream_t);
+template void rmsnorm<float, float>(const float*, int, const float*, int, float, int, float*, int,
+                                    float*, int, uint64_t*, int, hipStream_t);
+
+// ------------------------------------------------------------------ embeddings
+template <typename T>
+__global__ void embed_rows_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ tok,
+                                  float* __restrict__ x, int ldx) {
+  const int row = blockIdx.x;
+  const T* er = E + (size_t)tok[row] * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)row * ldx + i] = Elem<T>::to_f32(er[i]);
+}
+template <typename T>
+void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL((embed_rows_kernel<T>), dim3(rows), dim3(256), 0, s, embed, d, tokens, x, ldx);
+}
+
+template <typename T>
+__global__ void embed_block_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st,
+                                   int mask, int bk, float* x, float* et, int ldx) {
+  const int row = blockIdx.x, sq = row / bk, j = row % bk;
+  const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
+  const T* er = E + (size_t)tok * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = Elem<T>::to_f32(er[i]);
+    x[(size_t)row * ldx + i] = v;
+    et[(size_t)row * ldx + i] = v;
+  }
+}
+template <typename T>
+void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk,
+                 float* x, float* etilde, int ldx, hipStream_t s) {
+  hipLaunchKernelGGL((embed_block_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
+                     mask_token, bk, x, etilde, ldx);
+}
+
+template <typename T>
+__global__ void embed_verify_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st,
+                                    const uint64_t* __restrict__ dkeys, int forced, int32_t* dtok, int bk,
+                                    float* x, int ldx) {
+  const int row = blockIdx.x, sq = row / bk, j = row % bk;
+  int tok;
+  if (j == 0) tok = st[sq * kStateFields + ST_ANCHOR];
+  else tok = forced ? dtok[row] : key_index(dkeys[row]);
+  __syncthreads();
+  if (threadIdx.x == 0) dtok[row] = tok;
+  const T* er = E + (size_t)tok * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)row * ldx + i] = Elem<T>::to_f32(er[i]);
+}
+template <typename T>
+void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* dkeys, int forced,
+                  int32_t* dtok, int n_seqs, int bk, float* x, int ldx, hipStream_t s) {
+  hipLaunchKernelGGL((embed_verify_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state, dkeys,
+                     forced, dtok, bk, x, ldx);
+}
+
+// ------------------------------------------------------------------ conditioning gather
+template <typename K> struct KeepRead;
+template <> struct KeepRead<uint16_t> { __device__ static float of(uint16_t v) { return f16_to_f32(v); } };
+template <> struct KeepRead<float> { __device__ static float of(float v) { return v; } };
+
+// row (s, j): m_j = hD[s][r + j], u_j = hT[s][r + j - 1] for 1 <= j <= cond_len, else 0.
+template <typename T, typename K>
+__global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st, int mask,
+                                 const K* __restrict__ hD, const K* __restrict__ hT, int bk,
+                                 float* __restrict__ mu, float* __restrict__ er) {
+  const int row = blockIdx.x, sq = row / bk, j = row % bk;
+  const int r = st[sq * kStateFields + ST_R], cl = st[sq * kStateFields + ST_COND_LEN];
+  const bool cond = j >= 1 && j <= cl;
+  const K* pm = hD + ((size_t)sq * bk + (cond ? r + j : 0)) * d;
+  const K* pu = hT + ((size_t)sq * bk + (cond ? r + j - 1 : 0)) * d;
+  const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
+  const T* pe = E + (size_t)tok * d;
+  float* mrow = mu + (size_t)row * 2 * d;
+  float* erow = er + (size_t)row * 2 * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    mrow[i] = cond ? KeepRead<K>::of(pm[i]) : 0.f;
+    mrow[d + i] = cond ? KeepRead<K>::of(pu[i]) : 0.f;
+    erow[i] = Elem<T>::to_f32(pe[i]);
+  }
+}
+template <typename T, typename K>
+void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
+               int n_seqs, int bk, float* mu, float* er, hipStream_t s) {
+  hipLaunchKernelGGL((cond_prep_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
+                     mask_token, hD, hT, bk, mu, er);
+}
+
+// ------------------------------------------------------------------ acceptance / rollback
+// One wave per sequence.  Draft tokens y^_i (i = 1..B) sit in dtok[s][i]; the target's
+// token for block position i is the argmax of verify row i-1.
+__global__ void accept_kernel(int32_t* st_all, const int32_t* __restrict__ dtok,
+                              const uint64_t* __restrict__ tkeys, int32_t* ttok, int bk,
+                              int32_t* out_tok, int32_t* out_n, int32_t* out_a) {
+  const int sq = blockIdx.x, lane = threadIdx.x;
+  const int B = bk - 1;
+  int32_t* st = st_all + sq * kStateFields;
+  const int yt = lane < bk ? key_index(tkeys[(size_t)sq * bk + lane]) : -1;   // y^T_{lane+1}
+  if (lane < bk) ttok[(size_t)sq * bk + lane] = yt;
+  // mismatch at block position i = lane + 1 (1..B)
+  const bool mis = (lane < B) && (dtok[(size_t)sq * bk + lane + 1] != yt);
+  const unsigned long long ball = __ballot(mis);
+  const int A = ball ? __ffsll((long long)ball) - 1 : B;
+  const int budget = st[ST_BUDGET];
+  const int n_new = budget > 0 ? min(A + 1, budget) : 0;
+  const int corr = __shfl(yt, A, 64);                               // y^T_{A+1}
+  if (lane < bk) {
+    int v = -1;
+    if (lane < n_new) v = (lane < A) ? dtok[(size_t)sq * bk + lane + 1] : corr;
+    out_tok[(size_t)sq * bk + lane] = v;
+  }
+  if (lane == 0) {
+    out_n[sq] = n_new;
+    out_a[sq] = n_new > 0 ? A : 0;
+    if (budget > 0) {
+      const int P = st[ST_SEQ_LEN];
+      st[ST_ROUND_POS] = P;
+      st[ST_APPEND] = A + 1;
+      st[ST_ACCEPT] = A;
+      st[ST_SEQ_LEN] = P + A + 1;        // rows P+A+1.. of the target KV are rolled back
+      st[ST_ANCHOR] = corr;
+      st[ST_BUDGET] = budget - n_new;
+      if (A < B - 1) { st[ST_R] = A + 1; st[ST_COND_LEN] = B - (A + 1); }
+      else { st[ST_R] = 0; st[ST_COND_LEN] = 0; }
+    } else {
+      st[ST_APPEND] = 0;
+      st[ST_ROUND_POS] = st[ST_SEQ_LEN];
+    }
+  }
+}
+void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs, int bk,
+            int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s) {
+  hipLaunchKernelGGL(accept_kernel, dim3(n_seqs), dim3(64), 0, s, state, dtok, tkeys, ttok, bk, out_tokens,
+                     out_n, out_a);
+}
+
+__global__ void set_ints_kernel(int32_t* dst, int n, int v0, int v1, int v2, int v3) {
+  const int v[4] = {v0, v1, v2, v3};
+  if (threadIdx.x < n && threadIdx.x < 4) dst[threadIdx.x] = v[threadIdx.x];
+}
+void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s) {
+  hipLaunchKernelGGL(set_ints_kernel, dim3(1), dim3(64), 0, s, dst, n, v0, v1, v2, v3);
+}
+
+__global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys, int plen, int budget,
+                                   int32_t* first_out) {
+  if (threadIdx.x != 0) return;
+  int32_t* st = st_all + sq * kStateFields;
+  const int tok = key_index(keys[0]);
+  st[ST_SEQ_LEN] = plen;
+  st[ST_ANCHOR] = tok;
+  st[ST_R] = 0;
+  st[ST_COND_LEN] = 0;
+  st[ST_BUDGET] = budget - 1;
+  st[ST_ROUND_POS] = plen;
+  st[ST_APPEND] = 0;
+  st[ST_ACCEPT] = 0;
+  first_out[sq] = tok;
+}
+void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
+                 int32_t* first_out, hipStream_t s) {
+  hipLaunchKernelGGL(first_token_kernel, dim3(1), dim3(64), 0, s, state, seq, keys, prompt_len, budget,
+                     first_out);
+}
+
+__global__ void fill_zero_kernel(uint4* p, size_t n16) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0, 0, 0, 0);
+}
+void fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return;
+  size_t g = (n16 + 255) / 256;
+  if (g > 8192) g = 8192;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)g), dim3(256), 0, s, (uint4*)p, n16);
+}
+
+template void embed_rows<bf16_t>(const bf16_t*, int, const int32_t*, int, float*, int, hipStream_t);
+template void embed_rows<float>(const float*, int, const int32_t*, int, float*, int, hipStream_t);
+template void embed_block<bf16_t>(const bf16_t*, int, const int32_t*, int, int, int, float*, float*, int,
+                                  hipStream_t);
+template void embed_block<float>(const float*, int, const int32_t*, int, int, int, float*, float*, int,
+                                 hipStream_t);
+template void embed_verify<bf16_t>(const bf16_t*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
+                                   int, float*, int, hipStream_t);
+template void embed_verify<float>(const float*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
+                                  int, float*, int, hipStream_t);
+template void cond_prep<bf16_t, uint16_t>(const bf16_t*, int, const int32_t*, int, const uint16_t*,
+                                          const uint16_t*, int, int, float*, float*, hipStream_t);
+template void cond_prep<float, float>(const float*, int, const int32_t*, int, const float*, const float*, int,
+                                      int, float*, float*, hipStream_t);
+
+}  // namespace rt

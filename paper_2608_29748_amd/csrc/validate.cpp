@@ -1,0 +1,174 @@
+// Configuration checks and workspace layout (host only).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "host.h"
+
+namespace rt {
+
+static thread_local std::string g_err;
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+}
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+const char* last_error() { return g_err.c_str(); }
+
+int validate_config(const rt_config* c) {
+  if (!c) return fail(RT_ERR_INVALID, "config is null");
+  if (c->dtype != RT_F32 && c->dtype != RT_BF16) return fail(RT_ERR_INVALID, "dtype must be RT_F32 or RT_BF16");
+  if (c->vocab < 16 || c->vocab % 16) return fail(RT_ERR_INVALID, "vocab must be a positive multiple of 16");
+  if (c->hidden < 32 || c->hidden % 32) return fail(RT_ERR_INVALID, "hidden must be a positive multiple of 32");
+  if (c->n_layers < 1) return fail(RT_ERR_INVALID, "n_layers must be >= 1");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(RT_ERR_INVALID, "head_dim must be 64 or 128");
+  if (c->n_kv_heads < 1 || c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
+    return fail(RT_ERR_INVALID, "n_q_heads must be a positive multiple of n_kv_heads");
+  if ((c->n_q_heads * c->head_dim) % 128 || (c->n_kv_heads * c->head_dim) % 128)
+    return fail(RT_ERR_INVALID, "q and kv projection widths must be multiples of 128");
+  if (c->ffn < 16 || c->ffn % 16) return fail(RT_ERR_INVALID, "ffn must be a positive multiple of 16");
+  if (c->draft_layers < 1) return fail(RT_ERR_INVALID, "draft_layers must be >= 1");
+  if (c->n_cond_layers < 1 || c->n_cond_layers > RT_MAX_COND_LAYERS)
+    return fail(RT_ERR_INVALID, "n_cond_layers must be in [1, %d]", RT_MAX_COND_LAYERS);
+  for (int i = 0; i < c->n_cond_layers; ++i) {
+    const int id = c->cond_layer_ids[i];
+    if (id < 0 || id >= c->n_layers) return fail(RT_ERR_INVALID, "cond_layer_ids[%d] = %d out of range", i, id);
+    if (i && id <= c->cond_layer_ids[i - 1]) return fail(RT_ERR_INVALID, "cond_layer_ids must increase");
+  }
+  if (c->block_size < 2 || c->block_size > 64) return fail(RT_ERR_INVALID, "block_size must be in [2, 64]");
+  if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab) return fail(RT_ERR_TOKEN, "mask_token_id out of range");
+  if (!isfinite(c->beta)) return fail(RT_ERR_INVALID, "beta must be finite");
+  if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(RT_ERR_INVALID, "rope_theta / rms_eps invalid");
+  if (c->cond_mode != RT_COND_OFF && c->cond_mode != RT_COND_RETRACE) return fail(RT_ERR_INVALID, "cond_mode invalid");
+  if (c->max_batch < 1 || c->max_batch > 1024) return fail(RT_ERR_INVALID, "max_batch must be in [1, 1024]");
+  if (c->max_seq_len < c->block_size + 1 || c->max_seq_len > (1 << 20))
+    return fail(RT_ERR_INVALID, "max_seq_len must be in [block_size + 1, 2^20]");
+  if (c->page_size != 16) return fail(RT_ERR_INVALID, "page_size must be 16");
+  return RT_OK;
+}
+
+int weight_count(const rt_config* c) { return 1 + 11 * c->n_layers + 4 + 11 * c->draft_layers + 1 + 3; }
+
+int make_plan(const rt_config* c, Plan* p) {
+  int st = validate_config(c);
+  if (st) return st;
+  Plan& q = *p;
+  q.V = c->vocab; q.d = c->hidden; q.L = c->n_layers; q.Hq = c->n_q_heads; q.Hkv = c->n_kv_heads;
+  q.hd = c->head_dim; q.F = c->ffn; q.LD = c->draft_layers; q.nc = c->n_cond_layers;
+  q.bk = c->block_size; q.B = q.bk - 1; q.bmax = c->max_batch; q.T = c->max_seq_len;
+  q.G = q.Hq / q.Hkv;
+  q.qN = q.Hq * q.hd; q.kvN = q.Hkv * q.hd; q.qkvN = q.qN + 2 * q.kvN;
+  q.Kp_d = (int)rup(q.d, 32); q.Kp_q = (int)rup(q.qN, 32); q.Kp_F = (int)rup(q.F, 32);
+  q.Kp_nc = (int)rup((size_t)q.nc * q.d, 32); q.Kp_2d = (int)rup(2 * (size_t)q.d, 32);
+  q.esz = c->dtype == RT_BF16 ? 2 : 4;
+  q.ksz = c->dtype == RT_BF16 ? 2 : 4;
+  q.pages_per_seq = (q.T + 15) / 16;
+  q.n_pages = q.bmax * q.pages_per_seq;
+  q.R = q.bmax * q.bk;
+  q.PF = kPrefillChunk;
+  q.Mrows = (int)rup((size_t)(q.R > q.PF ? q.R : q.PF), 128);
+  q.attn_rb = (q.bk * q.G + 63) / 64;
+  {
+    const int base = q.bmax * q.Hkv * q.attn_rb;
+    int sp = (768 + base - 1) / base;
+    const int maxsp = (q.T + 63) / 64;
+    if (sp > maxsp) sp = maxsp;
+    if (sp < 1) sp = 1;
+    q.attn_splits = sp;
+  }
+  q.pf_rb = (q.PF * q.G + 63) / 64;
+  q.cache_layer_elems = (size_t)q.n_pages * q.Hkv * 16 * q.hd;
+
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = rup(off + bytes, 256); return o; };
+  const size_t e = q.esz;
+  auto packed = [&](size_t N, size_t Kp) { return N * Kp * e; };
+  q.embed = take((size_t)q.V * q.d * e);
+  q.lm_head = take(packed(q.V, q.Kp_d));
+  q.t_final_norm = take(q.d * e);
+  q.d_final_norm = take(q.d * e);
+  q.fc = take(packed(q.d, q.Kp_nc));
+  q.hidden_norm = take(q.d * e);
+  q.ctxkv = take(packed((size_t)q.LD * 2 * q.kvN, q.Kp_d));
+  q.ctx_knorm = take((size_t)q.LD * q.hd * e);
+  q.wc = take(packed(q.d, q.Kp_2d));
+  q.wg = take(packed(q.d, q.Kp_2d));
+  q.wv = take(packed(q.d, q.Kp_d));
+  // per-layer block
+  size_t lo = 0;
+  auto ltake = [&](size_t bytes) { size_t o = lo; lo = rup(lo + bytes, 256); return o; };
+  q.lo_qkv = ltake(packed(q.qkvN, q.Kp_d));
+  q.lo_o = ltake(packed(q.d, q.Kp_q));
+  q.lo_gu = ltake(packed(2 * (size_t)q.F, q.Kp_d));
+  q.lo_down = ltake(packed(q.d, q.Kp_F));
+  q.lo_in = ltake(q.d * e);
+  q.lo_post = ltake(q.d * e);
+  q.lo_qn = ltake(q.hd * e);
+  q.lo_kn = ltake(q.hd * e);
+  q.layer_bytes = lo;
+  q.t_layers = take(q.layer_bytes * q.L);
+  q.d_layers = take(q.layer_bytes * q.LD);
+  q.zero_from = off;
+  q.kc = take(q.cache_layer_elems * e * q.L);
+  q.vc = take(q.cache_layer_elems * e * q.L);
+  q.dkc = take(q.cache_layer_elems * e * q.LD);
+  q.dvc = take(q.cache_layer_elems * e * q.LD);
+  q.page_table = take((size_t)q.n_pages * 4);
+  q.rope = take((size_t)q.T * (q.hd / 2) * 2 * 4);
+  q.state = take((size_t)q.bmax * 8 * 4);
+  q.pf_ints = take(16 * 4);
+  q.first_tok = take((size_t)q.bmax * 4);
+  q.counters = take((size_t)kMaxTiles * 4);
+  q.partial = take(kPartialFloats * 4);
+  {
+    size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
+    size_t blocks = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits;
+    (void)rb;
+    q.opart = take(blocks * 64 * q.hd * 4);
+    q.mlpart = take(blocks * 64 * 2 * 4);
+  }
+  const size_t M = q.Mrows;
+  q.x = take(M * q.d * 4);
+  q.xa = take(M * q.Kp_d * e);
+  q.qbuf = take(M * q.qN * e);
+  q.attn = take(M * q.Kp_q * e);
+  q.mlp = take(M * q.Kp_F * e);
+  q.g = take(M * q.Kp_nc * e);
+  q.fcout = take(M * q.d * 4);
+  q.fa = take(M * q.Kp_d * e);
+  q.etilde = take((size_t)q.R * q.d * 4);
+  q.mu = take((size_t)q.R * 2 * q.d * 4 + 64);
+  q.er = take((size_t)q.R * 2 * q.d * 4 + 64);
+  q.gate = take((size_t)q.R * q.d * 4);
+  q.hd_keep = take((size_t)q.R * q.d * q.ksz);
+  q.ht_keep = take((size_t)q.R * q.d * q.ksz);
+  q.dlogits = take((size_t)q.R * q.V * 4);
+  q.vlogits = take((size_t)q.R * q.V * 4);
+  q.dkeys = take(M * 8);
+  q.tkeys = take(M * 8);
+  q.dtok = take((size_t)q.R * 4);
+  q.ttok = take((size_t)q.R * 4);
+  q.out_tok = take((size_t)q.R * 4);
+  q.out_n = take((size_t)q.bmax * 4);
+  q.out_a = take((size_t)q.bmax * 4);
+  q.tokbuf = take((size_t)q.T * 4);
+  q.total = off;
+  return RT_OK;
+}
+
+}  // namespace rt

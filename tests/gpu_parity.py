@@ -1,0 +1,198 @@
+"""Teacher-forced round-by-round comparison of the HIP path (through the C ABI) with
+the oracle, shared by the GPU parity tests.
+
+Per round: the conditioned drafter inputs, retained drafter / target final states
+and both LM heads' logits must agree within `tol` (max abs error); every argmax
+decision whose oracle top-2 gap exceeds `tol` must agree exactly; at near-ties the
+GPU's choice is adopted by the oracle so both continue from the same tokens.  The
+acceptance length, committed tokens and round state must then agree exactly.
+"""
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass, field
+from typing import List
+
+import numpy as np
+
+from oracle import OracleModel, OracleRunner
+from paper_2608_29748_amd import binding as B
+from paper_2608_29748_amd.engine import RoundEngine, config_from
+from workloads import weight_specs
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def engine_for(wl, W, max_batch=None, cond_mode=B.RT_COND_RETRACE):
+    cfg = config_from(wl.target, dtype=wl.dtype, draft_layers=wl.draft_layers,
+                      cond_layers=wl.cond_layers, block_size=wl.block_size,
+                      mask_token_id=wl.mask_token_id, max_batch=max_batch or wl.batch,
+                      max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps,
+                      beta=wl.beta, cond_mode=cond_mode)
+    return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
+
+
+def keep_dtype(wl):
+    return np.float16 if wl.dtype == "bf16" else np.float32
+
+
+def store_to_f64(arr, wl):
+    if wl.dtype == "bf16":
+        return (arr.astype(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return arr.astype(np.float64)
+
+
+def top2_gap(logits):
+    part = np.partition(logits, -2, axis=-1)
+    return part[..., -1] - part[..., -2]
+
+
+@dataclass
+class Report:
+    rounds: int = 0
+    max_err: dict = field(default_factory=dict)
+    near_ties: int = 0
+    decisions: int = 0
+    accept: List[int] = field(default_factory=list)
+
+    p999: dict = field(default_factory=dict)
+
+    def err(self, name, a, b):
+        d = np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64))
+        e = float(np.max(d)) if np.size(a) else 0.0
+        self.max_err[name] = max(self.max_err.get(name, 0.0), e)
+        if np.size(a):
+            self.p999[name] = max(self.p999.get(name, 0.0), float(np.quantile(d, 0.999)))
+        return e
+
+    def stored_err(self, name, a, b, tol, wl):
+        """Error in excess of the allowance for values both sides store in the
+        storage type: where the unrounded values straddle a rounding boundary the
+        stored ones differ by one unit in the last place (2**-7 relative for bf16),
+        so the bound is tol + ulp(|ref|).  Returns the largest excess (<= 0 passes)."""
+        a = np.asarray(a, np.float64)
+        b = np.asarray(b, np.float64)
+        self.err(name, a, b)
+        if not np.size(a):
+            return 0.0
+        ulp = np.ldexp(1.0, np.frexp(np.abs(b))[1] - 8) if wl.dtype == "bf16" else np.zeros_like(b)
+        return float(np.max(np.abs(a - b) - tol - ulp))
+
+
+def check_decisions(rep, o_logits, gpu_tok, tol, what):
+    """Oracle argmax must equal the GPU token wherever the oracle's top-2 gap > tol."""
+    o_tok = np.argmax(o_logits, axis=-1)
+    gap = top2_gap(o_logits)
+    for i in range(len(gpu_tok)):
+        rep.decisions += 1
+        if gap[i] > tol:
+            assert o_tok[i] == gpu_tok[i], f"{what} row {i}: oracle {o_tok[i]} gpu {gpu_tok[i]} gap {gap[i]}"
+        else:
+            rep.near_ties += 1
+
+
+def compare_prefill(eng, R, wl, prompts, seq_states, tol, layers=None):
+    """Target and drafter-context KV of every prompt position."""
+    s = wl.target
+    et = np.uint16 if wl.dtype == "bf16" else np.float32
+    rep = Report()
+    for b, st in enumerate(seq_states):
+        n = len(prompts[b])
+        for l in (layers if layers is not None else range(s.n_layers)):
+            for tid, ref in ((B.RT_T_TARGET_K + l, st.tgt_k[l]), (B.RT_T_TARGET_V + l, st.tgt_v[l])):
+                g = store_to_f64(eng.read(tid, b, (n, s.n_kv_heads, s.head_dim), et), wl)
+                x = rep.stored_err("target_kv", g, ref[:n], tol, wl)
+                assert x <= 0, f"seq {b} layer {l} target kv exceeds bound by {x}"
+        for l in range(wl.draft_layers):
+            for tid, ref in ((B.RT_T_DRAFT_K + l, st.ctx_k[l]), (B.RT_T_DRAFT_V + l, st.ctx_v[l])):
+                g = store_to_f64(eng.read(tid, b, (n, s.n_kv_heads, s.head_dim), et), wl)
+                x = rep.stored_err("draft_ctx_kv", g, ref[:n], tol, wl)
+                assert x <= 0, f"seq {b} drafter layer {l} ctx kv exceeds bound by {x}"
+    return rep
+
+
+def carried_state(eng, b, wl):
+    s, bk = wl.target, wl.block_size
+    kd = keep_dtype(wl)
+    return (eng.read(B.RT_T_HD, b, (bk, s.hidden), kd).astype(np.float64),
+            eng.read(B.RT_T_HT, b, (bk, s.hidden), kd).astype(np.float64))
+
+
+def inject_state(eng, st, b, wl, carried, kv=False):
+    """Starts the oracle's round from the GPU's carried state (read before the GPU
+    round): the retained drafter / target final states, optionally both KV caches."""
+    s = wl.target
+    st.hD_prev, st.hT_prev = carried
+    if kv:
+        et = np.uint16 if wl.dtype == "bf16" else np.float32
+        shp = (st.P, s.n_kv_heads, s.head_dim)
+        for l in range(s.n_layers):
+            st.tgt_k[l, :st.P] = store_to_f64(eng.read(B.RT_T_TARGET_K + l, b, shp, et), wl)
+            st.tgt_v[l, :st.P] = store_to_f64(eng.read(B.RT_T_TARGET_V + l, b, shp, et), wl)
+        for l in range(wl.draft_layers):
+            st.ctx_k[l, :st.P] = store_to_f64(eng.read(B.RT_T_DRAFT_K + l, b, shp, et), wl)
+            st.ctx_v[l, :st.P] = store_to_f64(eng.read(B.RT_T_DRAFT_V + l, b, shp, et), wl)
+
+
+def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forced=None, rep=None,
+                       inject=True, inject_kv=False):
+    """Runs n_rounds GPU rounds (debug: logits stored, no graph) and checks each
+    against the oracle continuing from the same decisions.  With inject, every
+    round starts the oracle from the GPU's carried state, so each comparison
+    measures one round.  forced: optional list (per round) of [n_seqs][B] drafts."""
+    s, bk, B_ = wl.target, wl.block_size, wl.B
+    rep = rep or Report()
+    eng.set_debug(3)
+    kd = keep_dtype(wl)
+    ns = len(seq_states)
+    for t in range(n_rounds):
+        carried = [carried_state(eng, b, wl) if inject else None for b in range(ns)]
+        if forced is not None:
+            tok, n_c, acc = eng.spec_round_forced(forced[t])
+        else:
+            tok, n_c, acc = eng.spec_round()
+        for b, st in enumerate(seq_states):
+            if st.done:
+                assert n_c[b] == 0
+                continue
+            if inject:
+                inject_state(eng, st, b, wl, carried[b], kv=inject_kv and t == 0)
+            d = R.draft(st)
+            g_et = eng.read(B.RT_T_ETILDE, b, (bk, s.hidden), np.float32)
+            e = rep.err("e_tilde", g_et, d.e_tilde)
+            assert e <= tol, f"round {t} seq {b}: e_tilde err {e}"
+            g_hd = eng.read(B.RT_T_HD, b, (bk, s.hidden), kd)
+            e = rep.err("h_draft", g_hd, R.m.prec.k(d.h))
+            assert e <= tol, f"round {t} seq {b}: h^D err {e}"
+            g_dl = eng.read(B.RT_T_DRAFT_LOGITS, b, (bk, s.vocab), np.float32)
+            e = rep.err("draft_logits", g_dl[1:], d.logits[1:])
+            assert e <= tol, f"round {t} seq {b}: draft logits err {e}"
+            g_dt = eng.read(B.RT_T_DRAFT_TOKENS, b, (bk,), np.int32)
+            if forced is None:
+                check_decisions(rep, d.logits[1:], g_dt[1:], tol, f"round {t} seq {b} draft")
+            else:
+                assert list(g_dt[1:]) == list(forced[t][b])
+            y_hat = g_dt[1:].astype(np.int64)
+            v = R.verify(st, y_hat)
+            g_ht = eng.read(B.RT_T_HT, b, (bk, s.hidden), kd)
+            e = rep.err("h_target", g_ht, R.m.prec.k(v.h))
+            assert e <= tol, f"round {t} seq {b}: h^T err {e}"
+            g_vl = eng.read(B.RT_T_VERIFY_LOGITS, b, (bk, s.vocab), np.float32)
+            e = rep.err("verify_logits", g_vl, v.logits)
+            assert e <= tol, f"round {t} seq {b}: verify logits err {e}"
+            g_tt = eng.read(B.RT_T_TARGET_TOKENS, b, (bk,), np.int32)
+            check_decisions(rep, v.logits, g_tt, tol, f"round {t} seq {b} verify")
+            P_before = st.P
+            A, new = R.commit(st, y_hat, g_tt.astype(np.int64), d, v)
+            assert A == acc[b], f"round {t} seq {b}: A oracle {A} gpu {acc[b]}"
+            assert list(tok[b][: n_c[b]]) == new, f"round {t} seq {b}: committed {tok[b][:n_c[b]]} vs {new}"
+            gst = eng.read(B.RT_T_STATE, b, (8,), np.int32)
+            assert gst[0] == st.P and gst[1] == st.anchor, f"state {gst} vs P {st.P} anchor {st.anchor}"
+            assert gst[3] == st.cond_len and (st.cond_len == 0 or gst[2] == st.r), f"carry {gst} vs {st.r},{st.cond_len}"
+            assert gst[5] == P_before and gst[6] == A + 1
+            rep.accept.append(A)
+        rep.rounds += 1
+    return rep

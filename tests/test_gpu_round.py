@@ -1,0 +1,38 @@
+"""GPU parity of the ReTrace round against the oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+from oracle import OracleModel, OracleRunner
+from workloads import get, make_prompts, make_weights
+
+from gpu_parity import compare_prefill, engine_for, log, run_teacher_forced
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _setup(name, **over):
+    wl = get(name, **over)
+    W = make_weights(wl)
+    prompts = make_prompts(wl)
+    return wl, W, prompts
+
+
+@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged"])
+def test_prefill_and_rounds_match_oracle(name):
+    wl, W, prompts = _setup(name, norm_init="perturbed")
+    log(f"[{name}] engine init")
+    eng = engine_for(wl, W)
+    R = OracleRunner(OracleModel(wl, W))
+    log(f"[{name}] prefill")
+    first = eng.prefill(prompts, wl.new_tokens)
+    states = [R.prefill(p, wl.new_tokens) for p in prompts]
+    assert list(first) == [st.anchor for st in states]
+    tol = TOL[wl.dtype]
+    rep = compare_prefill(eng, R, wl, prompts, states, tol)
+    log(f"[{name}] prefill max err {rep.max_err}")
+    rep = run_teacher_forced(eng, R, wl, states, 6, tol)
+    log(f"[{name}] rounds {rep.rounds} max err {rep.max_err} p99.9 {rep.p999} "
+        f"near-ties {rep.near_ties}/{rep.decisions}")
+    eng.close()
