@@ -1,0 +1,206 @@
+#!/usr/bin/env python
+"""Benchmark of one ReTrace speculative-decoding round on one MI355X.
+
+A step is one round (conditioning, drafter, block verify, acceptance + rollback,
+drafter context append) for every sequence of the workload, replayed from a HIP
+graph with all inputs (weights, prompts' KV caches, carried state) resident in
+HBM.  `value` is committed tokens per second over exactly `--steps` rounds after
+`--warmup` rounds.  A profiled phase then times every kernel launch with HIP
+events on the library's stream to give the per-stage breakdown and the roofline
+of the dominant kernel (the weight-streaming MFMA GEMM).  The CPU baseline is the
+float64 oracle, started from the GPU's state, timed on this host.
+
+Random-initialised weights and uniform-random prompts of the workload's shapes
+stand in for the trained checkpoints and the benchmark prompts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0        # dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_engine(wl, W):
+    from paper_2608_29748_amd.engine import RoundEngine, config_from
+    from workloads import weight_specs
+    cfg = config_from(wl.target, dtype=wl.dtype, draft_layers=wl.draft_layers, cond_layers=wl.cond_layers,
+                      block_size=wl.block_size, mask_token_id=wl.mask_token_id, max_batch=wl.batch,
+                      max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps, beta=wl.beta)
+    return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
+
+
+def cpu_baseline(eng, wl, W, prompts, seconds: float):
+    """Oracle rounds for sequence 0, started from the GPU's KV caches and carried state
+    (an oracle prefill of the full prompt is far outside the time budget)."""
+    from threadpoolctl import threadpool_info
+    from oracle import OracleModel, OracleRunner
+    from paper_2608_29748_amd import binding as B
+    s = wl.target
+    model = OracleModel(wl, W)
+    R = OracleRunner(model)
+    st_arr = eng.read(B.RT_T_STATE, 0, (8,), np.int32)
+    P = int(st_arr[0])
+    st = model.new_state(prompts[0], wl.new_tokens)
+    et = np.uint16 if wl.dtype == "bf16" else np.float32
+    f64 = (lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)) if wl.dtype == "bf16" \
+        else (lambda a: a.astype(np.float64))
+    shp = (P, s.n_kv_heads, s.head_dim)
+    for l in range(s.n_layers):
+        st.tgt_k[l, :P] = f64(eng.read(B.RT_T_TARGET_K + l, 0, shp, et))
+        st.tgt_v[l, :P] = f64(eng.read(B.RT_T_TARGET_V + l, 0, shp, et))
+    for l in range(wl.draft_layers):
+        st.ctx_k[l, :P] = f64(eng.read(B.RT_T_DRAFT_K + l, 0, shp, et))
+        st.ctx_v[l, :P] = f64(eng.read(B.RT_T_DRAFT_V + l, 0, shp, et))
+    kd = np.float16 if wl.dtype == "bf16" else np.float32
+    st.hD_prev = eng.read(B.RT_T_HD, 0, (wl.block_size, s.hidden), kd).astype(np.float64)
+    st.hT_prev = eng.read(B.RT_T_HT, 0, (wl.block_size, s.hidden), kd).astype(np.float64)
+    st.P, st.anchor, st.r, st.cond_len = P, int(st_arr[1]), int(st_arr[2]), int(st_arr[3])
+    st.generated = [0] * (wl.new_tokens - int(st_arr[4]))
+    # one-time float64 conversion of the weights (the oracle's setup) outside the sample
+    t0 = time.perf_counter()
+    for name in W:
+        model.W[name]
+    log(f"oracle weight conversion {time.perf_counter() - t0:.1f}s")
+    rounds, committed = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        rec = R.round(st)
+        rounds += 1
+        committed += len(rec.committed)
+        el = time.perf_counter() - t0
+        if el >= seconds or st.done:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {"value": committed / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{rounds} round(s) of sequence 0 at context {P}, started from the GPU's KV caches and "
+                      f"carried state; {el:.1f}s of CPU time; float64 numpy with {threads} BLAS threads",
+            "seconds_per_round": el / rounds}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen3-4b-shape")
+    ap.add_argument("--profile-rounds", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+              "(the round shards by sequence with no exchange; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from workloads import get, make_prompts, make_weights
+
+    wl = get(args.workload)
+    need = args.warmup + args.steps + args.profile_rounds + 2
+    if need > wl.new_tokens - 1:
+        raise SystemExit(f"{need} rounds exceed the workload's generation budget of {wl.new_tokens} tokens")
+    t0 = time.perf_counter()
+    W = make_weights(wl)
+    prompts = make_prompts(wl)
+    log(f"weights {sum(v.nbytes for v in W.values()) / 1e9:.2f} GB generated in {time.perf_counter() - t0:.1f}s")
+    t0 = time.perf_counter()
+    eng = build_engine(wl, W)
+    log(f"engine init {time.perf_counter() - t0:.1f}s")
+    t0 = time.perf_counter()
+    eng.prefill(prompts, wl.new_tokens)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t0
+    log(f"prefill {prefill_s:.2f}s")
+
+    for _ in range(args.warmup):
+        eng.spec_round()
+    torch.cuda.synchronize()
+    committed, accepted, per_round = 0, [], []
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        r0 = time.perf_counter()
+        tok, n, a = eng.spec_round()
+        per_round.append(time.perf_counter() - r0)
+        committed += int(n.sum())
+        accepted.extend(int(x) for x in a)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    value = committed / elapsed
+    log(f"timed {args.steps} rounds: {elapsed * 1e3 / args.steps:.3f} ms/round, {value:.1f} tokens/s")
+
+    # profiled rounds: HIP events around every launch on the library's stream
+    kinds, stages = {}, []
+    for _ in range(args.profile_rounds):
+        stats, st_ms, tok, n, a = eng.profile_round()
+        stages.append(st_ms)
+        for s in stats:
+            k = kinds.setdefault(s["kind"], {"launches": 0, "ms": 0.0, "bytes": 0.0, "flops": 0.0})
+            for f in ("launches", "ms", "bytes", "flops"):
+                k[f] += s[f]
+    from paper_2608_29748_amd.binding import STAGE_NAMES
+    stage_med = {n: float(np.median([s[i] for s in stages])) for i, n in enumerate(STAGE_NAMES)}
+    dom = kinds["gemm_skinny"]
+    per_launch_bytes = dom["bytes"] / max(dom["launches"], 1)
+    per_launch_ms = dom["ms"] / max(dom["launches"], 1)
+    achieved = per_launch_bytes / (per_launch_ms * 1e-3) / 1e9
+    kernels = {k: {"launches_per_round": v["launches"] / args.profile_rounds,
+                   "ms_per_round": v["ms"] / args.profile_rounds,
+                   "GB_per_round": v["bytes"] / args.profile_rounds / 1e9,
+                   "achieved_GBs": (v["bytes"] / (v["ms"] * 1e-3) / 1e9) if v["ms"] > 0 else None,
+                   "achieved_TFLOPs": (v["flops"] / (v["ms"] * 1e-3) / 1e12) if v["ms"] > 0 else None}
+               for k, v in kinds.items() if v["launches"]}
+
+    out = {
+        "metric": "committed tokens/s/GPU, Qwen3-4B shape b=1; verify-pass % MFMA/HBM roofline",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic: seeded N(0,0.02) random-init weights, uniform-random prompt tokens",
+        "config": {"workload": wl.name, "batch": wl.batch, "prompt_len": list(wl.prompt_len),
+                   "block_size": wl.block_size, "new_tokens": wl.new_tokens, "hidden": wl.target.hidden,
+                   "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
+                   "cond_layers": list(wl.cond_layers), "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "gemm_skinny (weight-streaming bf16 MFMA GEMM)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "per_launch_bytes": per_launch_bytes, "per_launch_us": per_launch_ms * 1e3,
+                     "launches_per_round": dom["launches"] / args.profile_rounds},
+        "stages_ms_median": stage_med,
+        "kernels": kernels,
+        "acceptance": {"mean_A": float(np.mean(accepted)) if accepted else None,
+                       "mean_committed_per_round": committed / args.steps / wl.batch},
+        "round_ms_p50": float(np.median(per_round) * 1e3),
+        "prefill_s": prefill_s,
+    }
+    if not args.no_cpu_baseline:
+        try:
+            out["cpu_baseline"] = cpu_baseline(eng, wl, W, prompts, args.cpu_seconds)
+        except MemoryError as e:   # pragma: no cover
+            out["cpu_baseline"] = {"error": f"oracle did not fit in host memory: {e}"}
+    eng.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

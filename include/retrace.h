@@ -122,10 +122,45 @@ int rt_destroy(rt_model* m);
 /* Message for the last non-zero status returned on this thread. */
 const char* rt_last_error(void);
 
+/* ---- measurement --------------------------------------------------------------- */
+
+/* Kernel kinds reported by rt_profile_round. */
+enum {
+  RT_K_GEMM_SKINNY = 0,      /* weight-streaming MFMA GEMM, 16/32-row tiles (projections) */
+  RT_K_GEMM_SKINNY_F32A = 1, /* same, fp32 A operand (conditioning GEMMs, Eq.7-9) */
+  RT_K_GEMM_WIDE = 2,        /* 128-row tiles (prefill, large batches) */
+  RT_K_GEMM_WIDE_F32A = 3,
+  RT_K_ATTENTION = 4,        /* paged attention incl. split merge */
+  RT_K_NORM = 5,             /* RMSNorm */
+  RT_K_MISC = 6,             /* embedding gathers, conditioning gather, acceptance, argmax reduce */
+  RT_K_LM_HEAD = 7,          /* vocabulary projection with fused argmax */
+  RT_K_QKV_POST = 8,         /* q/k norm, RoPE and paged K/V writes */
+  RT_K_KINDS = 9
+};
+/* Stages of one round, in order (a HIP event at every boundary). */
+enum {
+  RT_S_CONDITION = 0, RT_S_DRAFT = 1, RT_S_DRAFT_HEAD = 2, RT_S_VERIFY = 3, RT_S_VERIFY_HEAD = 4,
+  RT_S_ACCEPT = 5, RT_S_CONTEXT = 6, RT_PROF_STAGES = 7
+};
+typedef struct rt_kernel_stat {
+  int32_t kind;
+  int32_t launches;
+  double ms;       /* summed HIP-event time around each launch */
+  double bytes;    /* summed algorithmic HBM bytes (weights + activations + KV read once) */
+  double flops;    /* summed algorithmic FLOPs */
+} rt_kernel_stat;
+
+/* Runs one round without graph replay, with a HIP-event pair around every kernel
+ * launch on the model's stream and an event at every stage boundary; fills
+ * stats[RT_K_KINDS] and stage_ms[RT_PROF_STAGES] plus the usual round outputs. */
+int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32_t* tokens,
+                     int32_t* n_committed, int32_t* accept_len);
+
 /* ---- test hooks -------------------------------------------------------------- */
 
 /* Debug flags: 1 = store fp32 logits of both LM heads; 2 = run rounds without
- * HIP-graph replay. */
+ * HIP-graph replay; 4 = split the reduction of every GEMM four ways (exercises the
+ * split-K path on small models). */
 int rt_set_debug(rt_model* m, int32_t flags);
 
 /* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)

@@ -25,10 +25,17 @@ RT_MAX_COND_LAYERS = 8
 (RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
  RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G) = range(9)
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
+(RT_K_GEMM_SKINNY, RT_K_GEMM_SKINNY_F32A, RT_K_GEMM_WIDE, RT_K_GEMM_WIDE_F32A, RT_K_ATTENTION, RT_K_NORM,
+ RT_K_MISC, RT_K_LM_HEAD, RT_K_QKV_POST) = range(9)
+RT_K_KINDS = 9
+KERNEL_KIND_NAMES = ["gemm_skinny", "gemm_skinny_f32a", "gemm_wide", "gemm_wide_f32a", "attention",
+                     "rmsnorm", "misc", "lm_head", "qkv_post"]
+STAGE_NAMES = ["condition", "draft", "draft_lm_head", "verify", "verify_lm_head", "accept", "context_append"]
+RT_PROF_STAGES = 7
 
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
-           "rt_debug_write"]
+           "rt_debug_write", "rt_profile_round"]
 
 
 class RetraceError(RuntimeError):
@@ -46,6 +53,11 @@ class rt_config(C.Structure):
                 ("mask_token_id", C.c_int32), ("beta", C.c_float), ("cond_mode", C.c_int32),
                 ("dtype", C.c_int32), ("max_batch", C.c_int32), ("max_seq_len", C.c_int32),
                 ("page_size", C.c_int32)]
+
+
+class rt_kernel_stat(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("launches", C.c_int32), ("ms", C.c_double), ("bytes", C.c_double),
+                ("flops", C.c_double)]
 
 
 def load_library(path: str = LIB_PATH) -> C.CDLL:
@@ -70,8 +82,9 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_set_debug.argtypes = [P, C.c_int32]
     lib.rt_debug_read.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_debug_write.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
+    lib.rt_profile_round.argtypes = [P, C.POINTER(rt_kernel_stat), C.POINTER(C.c_double), i32p, i32p, i32p]
     for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
-                 "rt_set_debug", "rt_debug_read", "rt_debug_write"):
+                 "rt_set_debug", "rt_debug_read", "rt_debug_write", "rt_profile_round"):
         getattr(lib, name).restype = C.c_int
     return lib
 
@@ -149,6 +162,21 @@ def rt_spec_round_forced(h: int, drafts: np.ndarray, block_size: int):
                                      n.ctypes.data_as(C.POINTER(C.c_int32)),
                                      a.ctypes.data_as(C.POINTER(C.c_int32))))
     return tok, n, a
+
+
+def rt_profile_round(h: int, n_seqs: int, block_size: int):
+    """One round with an event pair around every launch: returns (per-kind stats list of
+    dicts, per-stage ms list, tokens, n_committed, accept_len)."""
+    stats = (rt_kernel_stat * RT_K_KINDS)()
+    stages = (C.c_double * RT_PROF_STAGES)()
+    tok = np.full((n_seqs, block_size), -1, np.int32)
+    n = np.zeros(n_seqs, np.int32)
+    a = np.zeros(n_seqs, np.int32)
+    _check(_lib.rt_profile_round(C.c_void_p(h), stats, stages, tok.ctypes.data_as(C.POINTER(C.c_int32)),
+                                 n.ctypes.data_as(C.POINTER(C.c_int32)), a.ctypes.data_as(C.POINTER(C.c_int32))))
+    out = [dict(kind=KERNEL_KIND_NAMES[s.kind], launches=s.launches, ms=s.ms, bytes=s.bytes, flops=s.flops)
+           for s in stats]
+    return out, list(stages), tok, n, a
 
 
 def rt_set_debug(h: int, flags: int) -> None:

@@ -72,34 +72,46 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   for (int t = 0; t < NHT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const size_t head_page = (size_t)kPage * HD;   // elements of one (page, head) slice
+  // Each thread stages NP 16-byte pieces of a chunk (K pieces first, then V^T pieces);
+  // the next chunk's pieces are loaded into registers while the current one is used.
+  constexpr int KV16 = kChunk * HD * EB / 16;     // 16-byte pieces of K per chunk (same for V)
+  constexpr int NP = 2 * KV16 / 256;
+  uint4 pf[NP];
+  auto fetch = [&](int c) {
+    const int key0 = c * kChunk;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      const int p = threadIdx.x + j * 256;
+      const bool isv = p >= KV16;
+      const int e0 = (isv ? p - KV16 : p) * (16 / EB);
+      const int pg = e0 / (int)head_page, within = e0 % (int)head_page;
+      const int tok0 = key0 + pg * kPage;
+      pf[j] = make_uint4(0, 0, 0, 0);
+      if (c < c_end && tok0 < kv_end) {
+        const int page = a.page_table[(size_t)s * a.max_pages + tok0 / kPage];
+        const T* src = (const T*)(isv ? a.vcache : a.kcache) + ((size_t)page * a.n_kv_heads + kvh) * head_page + within;
+        pf[j] = *reinterpret_cast<const uint4*>(src);
+      }
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      const int p = threadIdx.x + j * 256;
+      const bool isv = p >= KV16;
+      const int e0 = (isv ? p - KV16 : p) * (16 / EB);
+      const int pg = e0 / (int)head_page, within = e0 % (int)head_page;
+      if (!isv) *reinterpret_cast<uint4*>(&sK[pg * kPage + within / HD][within % HD]) = pf[j];
+      else *reinterpret_cast<uint4*>(&sV[within / kPage][pg * kPage + within % kPage]) = pf[j];
+    }
+  };
+  if (c_beg < c_end) fetch(c_beg);
   for (int c = c_beg; c < c_end; ++c) {
     const int key0 = c * kChunk;
     __syncthreads();
-    // stage K [32][HD] and V^T [HD][32] for this chunk; pages past kv_end are zero-filled
-    constexpr int KV16 = kChunk * HD * EB / 16;   // 16-byte pieces per chunk of K (same for V)
-    for (int p = threadIdx.x; p < 2 * KV16; p += 256) {
-      const bool isv = p >= KV16;
-      const int q = isv ? p - KV16 : p;
-      const int e0 = q * (16 / EB);               // element offset within the 2-page chunk
-      const int pg = e0 / (int)head_page;         // 0 or 1
-      const int within = e0 % (int)head_page;
-      const int tok0 = key0 + pg * kPage;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (tok0 < kv_end) {
-        const int page = a.page_table[(size_t)s * a.max_pages + tok0 / kPage];
-        const T* src = (const T*)(isv ? a.vcache : a.kcache) +
-                       ((size_t)page * a.n_kv_heads + kvh) * head_page + within;
-        val = *reinterpret_cast<const uint4*>(src);
-      }
-      if (!isv) {
-        const int key = pg * kPage + within / HD, col = within % HD;
-        *reinterpret_cast<uint4*>(&sK[key][col]) = val;
-      } else {
-        const int hrow = within / kPage, kcol = pg * kPage + within % kPage;
-        *reinterpret_cast<uint4*>(&sV[hrow][kcol]) = val;
-      }
-    }
+    stage();
     __syncthreads();
+    fetch(c + 1);
     // S = Q K^T for two 16-key subtiles
     f32x4 sacc[2];
 #pragma unroll
@@ -193,34 +205,59 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
+// One wave per (sequence, kv head, row).  Lane j reads split j's running max and sum
+// (64 splits per pass); the weights exp2(m_j - M) are broadcast by shuffles while the
+// lanes accumulate the head dimension, eight splits' partial rows in flight at a time.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  // one workgroup per (seq, kv head, row block); thread -> (row, hd element)
+  constexpr int PL = HD / 64;                 // hd elements per lane
+  const int lane = threadIdx.x & 63;
+  const int rl = blockIdx.x * 4 + (threadIdx.x >> 6);        // row within the row block
   const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks, kvh = blockIdx.y;
   const int G = a.n_q_heads / a.n_kv_heads;
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
-  const int nrows = nq * G;
+  const int r = rb * kAttnRows + rl;
+  if (r >= nq * G) return;
   const size_t blk0 = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits;
-  for (int idx = threadIdx.x; idx < kAttnRows * HD; idx += 256) {
-    const int rl = idx / HD, e = idx % HD;
-    const int r = rb * kAttnRows + rl;
-    if (r >= nrows) continue;
-    float M = -INFINITY;
-    for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, a.mlpart[((blk0 + sp) * kAttnRows + rl) * 2]);
-    float num = 0.f, den = 0.f;
-    if (M != -INFINITY) {
-      for (int sp = 0; sp < a.splits; ++sp) {
-        const float m = a.mlpart[((blk0 + sp) * kAttnRows + rl) * 2];
-        if (m == -INFINITY) continue;
-        const float f = exp2f(m - M);
-        den += f * a.mlpart[((blk0 + sp) * kAttnRows + rl) * 2 + 1];
-        num += f * a.opart[((blk0 + sp) * kAttnRows + rl) * HD + e];
+  float M = -INFINITY;
+  for (int sp = lane; sp < a.splits; sp += 64) M = fmaxf(M, a.mlpart[((blk0 + sp) * kAttnRows + rl) * 2]);
+  M = warp_max(M);
+  float num[PL], den = 0.f;
+#pragma unroll
+  for (int j = 0; j < PL; ++j) num[j] = 0.f;
+  if (M != -INFINITY) {
+    for (int base = 0; base < a.splits; base += 64) {
+      const int sp = base + lane;
+      float f = 0.f;
+      if (sp < a.splits) {
+        const float* ml = a.mlpart + ((blk0 + sp) * kAttnRows + rl) * 2;
+        f = (ml[0] == -INFINITY) ? 0.f : exp2f(ml[0] - M);
+        den += f * ml[1];
+      }
+      const int n = min(64, a.splits - base);
+      for (int j0 = 0; j0 < n; j0 += 8) {
+        float o[8][PL], fw[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int jj = j0 + u < n ? j0 + u : n - 1;
+          fw[u] = __shfl(f, jj, 64) * (j0 + u < n ? 1.f : 0.f);
+          const float* op = a.opart + ((blk0 + base + jj) * kAttnRows + rl) * HD;
+#pragma unroll
+          for (int j = 0; j < PL; ++j) o[u][j] = op[lane + 64 * j];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int j = 0; j < PL; ++j) num[j] += fw[u] * o[u][j];
       }
     }
-    const int tok = r / G, h = kvh * G + r % G;
-    T* op = (T*)a.out + (size_t)(s * a.rows_per_seq + tok) * a.ldo + (size_t)h * HD;
-    op[e] = Elem<T>::from_f32(den > 0.f ? num / den : 0.f);
   }
+  den = warp_sum(den);
+  const int tok = r / G, h = kvh * G + r % G;
+  T* out = (T*)a.out + (size_t)(s * a.rows_per_seq + tok) * a.ldo + (size_t)h * HD;
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+  for (int j = 0; j < PL; ++j) out[lane + 64 * j] = Elem<T>::from_f32(num[j] * inv);
 }
 
 template <typename T>
@@ -229,12 +266,12 @@ hipError_t attention(const AttnArgs& a, hipStream_t s) {
   if (a.head_dim == 128) {
     hipLaunchKernelGGL((attn_kernel<T, 128>), grid, dim3(256), 0, s, a);
     if (a.splits > 1)
-      hipLaunchKernelGGL((attn_merge_kernel<T, 128>), dim3(1, a.n_kv_heads, a.n_seqs * a.row_blocks),
+      hipLaunchKernelGGL((attn_merge_kernel<T, 128>), dim3(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks),
                          dim3(256), 0, s, a);
   } else if (a.head_dim == 64) {
     hipLaunchKernelGGL((attn_kernel<T, 64>), grid, dim3(256), 0, s, a);
     if (a.splits > 1)
-      hipLaunchKernelGGL((attn_merge_kernel<T, 64>), dim3(1, a.n_kv_heads, a.n_seqs * a.row_blocks),
+      hipLaunchKernelGGL((attn_merge_kernel<T, 64>), dim3(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks),
                          dim3(256), 0, s, a);
   } else {
     return hipErrorInvalidValue;

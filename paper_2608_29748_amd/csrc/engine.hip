@@ -38,7 +38,31 @@ struct EngineBase {
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
   int32_t* h_out = nullptr;      // pinned: tokens [R], n [bmax], a [bmax], first [bmax]
+  // profiling: an event pair around every launch, aggregated per kernel kind
+  bool profiling = false;
+  std::vector<hipEvent_t> ev_pool;
+  struct ProfRec { int kind; hipEvent_t b, e; double bytes, flops; };
+  std::vector<ProfRec> prof;
+  hipEvent_t stage_ev[RT_PROF_STAGES + 1] = {};
+  std::vector<int32_t> prof_ctx;   // host copy of each sequence's context length
+  size_t ev_next = 0;
+  void prof_begin(int kind, double bytes, double flops) {
+    if (!profiling) return;
+    ProfRec r{kind, ev_pool[ev_next], ev_pool[ev_next + 1], bytes, flops};
+    ev_next += 2;
+    (void)hipEventRecord(r.b, stream);
+    prof.push_back(r);
+  }
+  void prof_end() {
+    if (!profiling) return;
+    (void)hipEventRecord(prof.back().e, stream);
+  }
+  void stage(int i) {
+    if (profiling) (void)hipEventRecord(stage_ev[i], stream);
+  }
   virtual ~EngineBase() {
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+    for (hipEvent_t e : stage_ev) if (e) (void)hipEventDestroy(e);
     drop_graph();
     if (h_out) (void)hipHostFree(h_out);
     if (own_stream && stream) (void)hipStreamDestroy(stream);
@@ -54,6 +78,7 @@ struct EngineBase {
   virtual int prefill(int ns, const int32_t* lens, const int32_t* ids, int budget, int32_t* first) = 0;
   virtual int run_round(bool forced) = 0;
   int round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc);
+  int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int debug_read(int id, int seq, void* dst, size_t bytes);
   int debug_write(int id, int seq, const void* src, size_t bytes);
 };
@@ -64,27 +89,38 @@ struct Engine : EngineBase {
   const char* dlayer(int l) const { return ws + p.d_layers + (size_t)l * p.layer_bytes; }
 
   int gemm_call(const void* A, int lda, int a_rows, bool af32, const void* B, int N, int Kp, int M,
-                EpiArgs e) {
+                EpiArgs e, int k_logical = 0) {
     if (M <= 0) return RT_OK;
+    if (k_logical <= 0) k_logical = Kp;
     e.M = M;
     e.N = N;
-    const int shape = M > 64 ? SHAPE_WIDE : SHAPE_SKINNY;
-    const int rows = gemm_tile_rows(shape);
-    const int tiles = ((N + 127) / 128) * ((M + rows - 1) / rows);
+    const int shape = M > 32 ? SHAPE_WIDE : SHAPE_SKINNY;
     const int KT = Kp / 32;
     int ks = 1;
-    if (tiles < 512) {
-      ks = (640 + tiles - 1) / tiles;
-      int maxk = KT / (shape == SHAPE_SKINNY ? 8 : 4);
-      if (maxk < 1) maxk = 1;
-      if (ks > maxk) ks = maxk;
+    if (shape == SHAPE_WIDE) {
+      const int tiles = ((N + 127) / 128) * ((M + 127) / 128);
+      if (flags & 4) {                       // test hook: force a k split wherever possible
+        ks = KT < 4 ? KT : 4;
+      } else if (tiles < 256) {
+        ks = (320 + tiles - 1) / tiles;
+        int maxk = KT / 4;
+        if (maxk < 1) maxk = 1;
+        if (ks > maxk) ks = maxk;
+      }
+      while (ks > 1 && (size_t)tiles * ks * 128 * 128 > kPartialFloats) --ks;
+      if (tiles > kMaxTiles) ks = 1;
     }
-    while (ks > 1 && (size_t)tiles * ks * rows * 128 > kPartialFloats) --ks;
-    if (tiles > kMaxTiles) ks = 1;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
     a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
+    if (profiling) {
+      const double Kl = (double)k_logical;
+      const int kind = (shape == SHAPE_SKINNY ? RT_K_GEMM_SKINNY : RT_K_GEMM_WIDE) + (af32 ? 1 : 0);
+      prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + (double)M * N * 4,
+                 2.0 * M * N * Kl);
+    }
     HIPCHK(gemm<T>(a, shape, af32, stream));
+    prof_end();
     return RT_OK;
   }
 
@@ -96,41 +132,82 @@ struct Engine : EngineBase {
     T* kc;
     T* vc;
     T* cap;
+    const int32_t* prof_ctx;     // host copy of each sequence's context length (profiling only)
   };
 
   int layer(const char* lw, const LayerCtx& c) {
     const Plan& q = p;
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
+    prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_in), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr, 0,
                   stream);
+    prof_end();
     EpiArgs e{};
-    e.kind = EPI_QKV; e.out_act = at<T>(q.qbuf); e.ldo = q.qN;
-    e.rows_per_seq = c.rows_per_seq; e.seq_stride = c.stride; e.pos0 = c.pos0; e.nrows = nullptr;
-    e.q_cols = q.qN; e.kv_cols = q.kvN; e.head_dim = q.hd; e.n_kv_heads = q.Hkv; e.layer_cols = q.qkvN;
-    e.q_norm = lw + q.lo_qn; e.k_norm = lw + q.lo_kn; e.norm_layer_stride = 0;
-    e.kcache = c.kc; e.vcache = c.vc; e.cache_layer_stride = 0;
-    e.page_table = c.pt; e.max_pages = q.pages_per_seq;
-    e.rope = at<float>(q.rope); e.rope_max_pos = q.T; e.eps = cfg.rms_eps;
-    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e));
+    e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
+    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
+    QkvPostArgs qp{};
+    qp.src = at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
+    qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
+    qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv; qp.q_out = at<T>(q.qbuf); qp.ldq = q.qN;
+    qp.q_norm = lw + q.lo_qn; qp.k_norm = lw + q.lo_kn; qp.norm_layer_stride = 0;
+    qp.kcache = c.kc; qp.vcache = c.vc; qp.cache_layer_stride = 0;
+    qp.page_table = c.pt; qp.max_pages = q.pages_per_seq;
+    qp.rope = at<float>(q.rope); qp.rope_max_pos = q.T; qp.eps = cfg.rms_eps;
+    qp.rows_per_seq = c.rows_per_seq; qp.seq_stride = c.stride; qp.pos0 = c.pos0; qp.nrows = nullptr;
+    prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 + sizeof(T)), 0);
+    HIPCHK(qkv_post<T>(qp, stream));
+    prof_end();
     AttnArgs a{};
     a.q = at<T>(q.qbuf); a.kcache = c.kc; a.vcache = c.vc; a.page_table = c.pt; a.max_pages = q.pages_per_seq;
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
     a.out = at<T>(q.attn); a.ldo = q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
+    if (profiling) {
+      // keys read: every sequence's context plus the block, K and V, once per KV head
+      double keys = 0;
+      for (int s = 0; s < c.n_seqs; ++s) keys += (double)(c.prof_ctx[s] + c.rows_per_seq);
+      const double kvb = keys * 2.0 * q.Hkv * q.hd * sizeof(T);
+      const double rows = (double)c.n_seqs * c.rows_per_seq;
+      prof_begin(RT_K_ATTENTION, kvb + rows * q.qN * sizeof(T) * 2, 4.0 * keys * c.rows_per_seq * q.Hq * q.hd);
+    }
     HIPCHK(attention<T>(a, stream));
+    prof_end();
     e = EpiArgs{};
     e.kind = EPI_RESID; e.resid = x; e.ldr = q.d;
     CHK(gemm_call(at<T>(q.attn), q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e));
+    prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr,
                   0, stream);
+    prof_end();
     e = EpiArgs{};
     e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = q.Kp_F;
     CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e));
     e = EpiArgs{};
     e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = q.Kp_nc;
-    CHK(gemm_call(at<T>(q.mlp), q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e));
+    CHK(gemm_call(at<T>(q.mlp), q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
+    return RT_OK;
+  }
+
+  // LM head over rows of xa with a fused argmax into keys[M] (optional fp32 logits).
+  int lm_head_argmax(int M, uint64_t* keys, float* logits) {
+    const Plan& q = p;
+    const int parts = lmhead_grid(q.V);
+    for (int r0 = 0; r0 < M; r0 += 32) {          // 32-row passes over the vocabulary
+      const int m = M - r0 < 32 ? M - r0 : 32;
+      LmHeadArgs h{};
+      h.A = at<T>(q.xa) + (size_t)r0 * q.Kp_d; h.lda = q.Kp_d; h.a_rows = q.Mrows - r0; h.M = m;
+      h.B = at<T>(q.lm_head); h.N = q.V; h.Kp = q.Kp_d;
+      h.part_keys = at<uint64_t>(q.part_keys); h.logits = logits ? logits + (size_t)r0 * q.V : nullptr;
+      h.ldl = q.V;
+      prof_begin(RT_K_LM_HEAD, (double)q.V * q.d * sizeof(T) + (double)m * q.d * sizeof(T), 2.0 * m * q.V * q.d);
+      HIPCHK(lm_head<T>(h, stream));
+      prof_end();
+      prof_begin(RT_K_MISC, (double)parts * m * 8, 0);
+      HIPCHK(argmax_reduce(at<uint64_t>(q.part_keys), parts, m, keys + r0, stream));
+      prof_end();
+    }
     return RT_OK;
   }
 
@@ -146,17 +223,26 @@ struct Engine : EngineBase {
     const Plan& q = p;
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.fcout); e.ldo = q.d;
-    CHK(gemm_call(at<T>(q.g), q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e));
+    CHK(gemm_call(at<T>(q.g), q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
+    prof_begin(RT_K_NORM, (double)M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), q.Kp_d,
                   nullptr, 0, nullptr, 0, stream);
+    prof_end();
     e = EpiArgs{};
-    e.kind = EPI_QKV; e.rows_per_seq = rows_per_seq; e.seq_stride = stride; e.pos0 = pos0; e.nrows = nrows;
-    e.q_cols = 0; e.kv_cols = q.kvN; e.head_dim = q.hd; e.n_kv_heads = q.Hkv; e.layer_cols = 2 * q.kvN;
-    e.k_norm = at<T>(q.ctx_knorm); e.norm_layer_stride = q.hd;
-    e.kcache = at<T>(q.dkc); e.vcache = at<T>(q.dvc); e.cache_layer_stride = q.cache_layer_elems;
-    e.page_table = pt; e.max_pages = q.pages_per_seq;
-    e.rope = at<float>(q.rope); e.rope_max_pos = q.T; e.eps = cfg.rms_eps;
-    CHK(gemm_call(at<T>(q.fa), q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e));
+    e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.LD * 2 * q.kvN;
+    CHK(gemm_call(at<T>(q.fa), q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e, q.d));
+    QkvPostArgs qp{};
+    qp.src = at<float>(q.qkvf); qp.lds = q.LD * 2 * q.kvN; qp.M = M;
+    qp.q_cols = 0; qp.kv_cols = q.kvN; qp.layer_cols = 2 * q.kvN; qp.n_layers = q.LD;
+    qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv;
+    qp.k_norm = at<T>(q.ctx_knorm); qp.norm_layer_stride = q.hd;
+    qp.kcache = at<T>(q.dkc); qp.vcache = at<T>(q.dvc); qp.cache_layer_stride = q.cache_layer_elems;
+    qp.page_table = pt; qp.max_pages = q.pages_per_seq;
+    qp.rope = at<float>(q.rope); qp.rope_max_pos = q.T; qp.eps = cfg.rms_eps;
+    qp.rows_per_seq = rows_per_seq; qp.seq_stride = stride; qp.pos0 = pos0; qp.nrows = nrows;
+    prof_begin(RT_K_QKV_POST, (double)M * q.LD * 2 * q.kvN * (4 + sizeof(T)), 0);
+    HIPCHK(qkv_post<T>(qp, stream));
+    prof_end();
     return RT_OK;
   }
 
@@ -246,16 +332,14 @@ struct Engine : EngineBase {
           const int slot = cond_slot(l);
           LayerCtx c{n, q.PF, 1, 0, 1, 1, (n * q.G + 63) / 64, pf, pf + 1, pt,
                      at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
-                     slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr};
+                     slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr, &c0};
           CHK(layer(tlayer(l), c));
         }
         CHK(context_append(n, q.PF, pf, nullptr, 0, pt));
         if (c0 + n == len) {
           rmsnorm<T, K>(at<float>(q.x) + (size_t)(n - 1) * q.d, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, 1,
-                        at<T>(q.xa), q.Kp_d, nullptr, 0, at<uint64_t>(q.tkeys), 1, stream);
-          EpiArgs e{};
-          e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.tkeys);
-          CHK(gemm_call(at<T>(q.xa), q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, 1, e));
+                        at<T>(q.xa), q.Kp_d, nullptr, 0, nullptr, 0, stream);
+          CHK(lm_head_argmax(1, at<uint64_t>(q.tkeys), nullptr));
           first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), len, budget, at<int32_t>(q.first_tok), stream);
         }
         HIPCHK(hipGetLastError());
@@ -281,9 +365,12 @@ struct Engine : EngineBase {
     T* xa = at<T>(q.xa);
     const int32_t* pt = at<int32_t>(q.page_table);
     // (1) rejected-trajectory conditioning (Eq.5-9)
+    stage(0);
     if (cfg.cond_mode == RT_COND_RETRACE) {
+      prof_begin(RT_K_MISC, (double)R * q.d * (4 * q.ksz + sizeof(T) + 16), 0);
       cond_prep<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, at<K>(q.hd_keep), at<K>(q.ht_keep), n_seqs, q.bk,
                       at<float>(q.mu), at<float>(q.er), stream);
+      prof_end();
       EpiArgs e{};
       e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er) + q.d; e.ldo = 2 * q.d;
       e.cond_m = at<float>(q.mu); e.ld_cond_m = 2 * q.d; e.beta = cfg.beta;
@@ -298,42 +385,53 @@ struct Engine : EngineBase {
       e.rows_per_seq = q.bk;
       CHK(gemm_call(at<float>(q.er) + q.d, 2 * q.d, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e));
     } else {
+      prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 8), 0);
       embed_block<T>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), q.d, stream);
+      prof_end();
     }
+    stage(1);
     // (2) drafter: B+1 rows at P..P+B over its context cache (no causal mask in the block)
     for (int l = 0; l < q.LD; ++l) {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
-                 nullptr};
+                 nullptr, prof_ctx.data()};
       CHK(layer(dlayer(l), c));
     }
+    stage(2);
+    prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
     rmsnorm<T, K>(x, q.d, at<T>(q.d_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.hd_keep), q.d,
-                  at<uint64_t>(q.dkeys), R, stream);
-    EpiArgs e{};
-    e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.dkeys);
-    e.out_f32 = (flags & 1) ? at<float>(q.dlogits) : nullptr; e.ldo = q.V;
-    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, R, e));
+                  nullptr, 0, stream);
+    prof_end();
+    CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (flags & 1) ? at<float>(q.dlogits) : nullptr));
     // (3) verify: [anchor, drafts] at P..P+B, causal over the target cache
+    stage(3);
+    prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 4), 0);
     embed_verify<T>(at<T>(q.embed), q.d, st, at<uint64_t>(q.dkeys), forced ? 1 : 0, at<int32_t>(q.dtok), n_seqs,
                     q.bk, x, q.d, stream);
+    prof_end();
     for (int l = 0; l < q.L; ++l) {
       const int slot = cond_slot(l);
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
-                 slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr};
+                 slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr, prof_ctx.data()};
       CHK(layer(tlayer(l), c));
     }
+    stage(4);
+    prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
     rmsnorm<T, K>(x, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.ht_keep), q.d,
-                  at<uint64_t>(q.tkeys), R, stream);
-    e = EpiArgs{};
-    e.kind = EPI_ARGMAX; e.keys = at<uint64_t>(q.tkeys);
-    e.out_f32 = (flags & 1) ? at<float>(q.vlogits) : nullptr; e.ldo = q.V;
-    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, at<T>(q.lm_head), q.V, q.Kp_d, R, e));
+                  nullptr, 0, stream);
+    prof_end();
+    CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
     // (4) acceptance, commit, rollback, carry / reset
+    stage(5);
+    prof_begin(RT_K_MISC, (double)R * 16, 0);
     accept(st, at<int32_t>(q.dtok), at<uint64_t>(q.tkeys), at<int32_t>(q.ttok), n_seqs, q.bk, at<int32_t>(q.out_tok),
            at<int32_t>(q.out_n), at<int32_t>(q.out_a), stream);
+    prof_end();
     // drafter context pathway for the committed rows 0..A at P..P+A
+    stage(6);
     CHK(context_append(R, q.bk, st + ST_ROUND_POS, st + ST_APPEND, kStateFields, pt));
+    stage(7);
     HIPCHK(hipGetLastError());
     return RT_OK;
   }
@@ -376,6 +474,52 @@ int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, i
   memcpy(tokens, h_out, R * 4);
   memcpy(n_comm, h_out + q.R, (size_t)n_seqs * 4);
   memcpy(acc, h_out + q.R + q.bmax, (size_t)n_seqs * 4);
+  return RT_OK;
+}
+
+int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm,
+                              int32_t* acc) {
+  if (!prefilled) return fail(RT_ERR_STATE, "rt_profile_round called before rt_prefill");
+  const Plan& q = p;
+  if (ev_pool.empty()) {
+    ev_pool.resize(8192);
+    for (auto& e : ev_pool) HIPCHK(hipEventCreate(&e));
+    for (auto& e : stage_ev) HIPCHK(hipEventCreate(&e));
+  }
+  std::vector<int32_t> st((size_t)n_seqs * kStateFields);
+  HIPCHK(hipStreamSynchronize(stream));
+  HIPCHK(hipMemcpy(st.data(), ws + q.state, st.size() * 4, hipMemcpyDeviceToHost));
+  prof_ctx.assign(n_seqs, 0);
+  for (int s = 0; s < n_seqs; ++s) prof_ctx[s] = st[(size_t)s * kStateFields + ST_SEQ_LEN];
+  prof.clear();
+  ev_next = 0;
+  profiling = true;
+  int rc = run_round(false);
+  profiling = false;
+  if (rc != RT_OK) return rc;
+  const size_t R = (size_t)n_seqs * q.bk;
+  HIPCHK(hipMemcpyAsync(h_out, ws + q.out_tok, R * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipMemcpyAsync(h_out + q.R, ws + q.out_n, (size_t)n_seqs * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipMemcpyAsync(h_out + q.R + q.bmax, ws + q.out_a, (size_t)n_seqs * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  memcpy(tokens, h_out, R * 4);
+  memcpy(n_comm, h_out + q.R, (size_t)n_seqs * 4);
+  memcpy(acc, h_out + q.R + q.bmax, (size_t)n_seqs * 4);
+  for (int k = 0; k < RT_K_KINDS; ++k) stats[k] = rt_kernel_stat{k, 0, 0.0, 0.0, 0.0};
+  for (const ProfRec& r : prof) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, r.b, r.e));
+    rt_kernel_stat& s = stats[r.kind];
+    s.launches += 1;
+    s.ms += ms;
+    s.bytes += r.bytes;
+    s.flops += r.flops;
+  }
+  for (int i = 0; i < RT_PROF_STAGES; ++i) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, stage_ev[i], stage_ev[i + 1]));
+    stage_ms[i] = ms;
+  }
   return RT_OK;
 }
 
@@ -570,9 +714,20 @@ int rt_spec_round_forced(rt_model* m, const int32_t* drafts, int32_t* tokens, in
   }
 }
 
+int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32_t* tokens,
+                     int32_t* n_committed, int32_t* accept_len) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    if (!stats || !stage_ms || !tokens || !n_committed || !accept_len) return fail(RT_ERR_INVALID, "null pointer argument");
+    return m->e->profile_round(stats, stage_ms, tokens, n_committed, accept_len);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_profile_round");
+  }
+}
+
 int rt_set_debug(rt_model* m, int32_t flags) {
   if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
-  if (flags < 0 || flags > 3) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  if (flags < 0 || flags > 7) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
   m->e->flags = flags;
   m->e->drop_graph();
   return RT_OK;

@@ -17,9 +17,7 @@ enum EpiKind : int {
   EPI_STORE_F32 = 0,   // out_f32[m][n] = y
   EPI_STORE_ACT,       // out_act[m][n] = T(y)
   EPI_RESID,           // resid[m][n] += y; optional capture cap[m][n] = T(resid)
-  EPI_SWIGLU,          // interleaved gate/up 16-column tiles: out_act[m][n/2] = T(silu(g) * u)
-  EPI_ARGMAX,          // keys[m] = max(keys[m], (y, n)); optional out_f32 logits
-  EPI_QKV,             // q/k/v heads: per-head RMSNorm + RoPE, q -> out_act, k/v -> paged caches
+  EPI_SWIGLU,          // gate|up 8-column halves of each 16-column tile: out_act[m][n/2] = T(silu(g) * u)
   EPI_COND_R,          // r = m + beta * y  -> out_f32 (the corrected signal, Eq.8)
   EPI_COND_GATE,       // out_f32 = sigmoid(y)                               (Eq.9 gate)
   EPI_COND_OUT,        // x = e + y * gate on conditioned rows, e elsewhere  (Eq.9)
@@ -32,22 +30,11 @@ struct EpiArgs {
   float* out_f32; void* out_act; int ldo;
   float* resid; int ldr;
   void* cap; int ldcap;          // capture (act type), may be null
-  uint64_t* keys;                // argmax keys per row
   // per-row sequence mapping
   int rows_per_seq;              // row m belongs to sequence m / rows_per_seq, block row m % rows_per_seq
   int seq_stride;                // int32 stride between sequences in pos0 / nrows / anchor / cond_len
   const int32_t* pos0;           // [seq] absolute position of block row 0
   const int32_t* nrows;          // [seq] number of valid block rows (null: all)
-  // QKV epilogue
-  int q_cols, kv_cols;           // column regions [0,q) q, [q,q+kv) k, [q+kv,q+2kv) v (repeats per layer)
-  int head_dim, n_kv_heads;
-  int layer_cols;                // columns per layer block (q + 2 kv) when several layers share a GEMM
-  const void* q_norm; const void* k_norm; int norm_layer_stride;
-  void* kcache; void* vcache; size_t cache_layer_stride;   // elements
-  const int32_t* page_table; int max_pages;
-  const float* rope;             // [pos][hd/2] cos followed by [pos][hd/2] sin at rope + max_pos*hd/2
-  int rope_max_pos;
-  float eps;
   // conditioning
   const float* cond_m; int ld_cond_m;     // m rows (fp32) for EPI_COND_R
   float beta;
@@ -65,6 +52,36 @@ struct GemmArgs {
   EpiArgs e;
 };
 
+// Per-head post-processing of a fused q|k|v projection (fp32 [M][layers*(q+2kv)]):
+// q and k get a per-head RMSNorm and rotate-half RoPE at their absolute position; q is
+// stored to q_out, k and v to the paged caches (K [page][kv head][token][hd], V
+// [page][kv head][hd][token]).  q_cols = 0 processes k|v blocks only (one per layer).
+struct QkvPostArgs {
+  const float* src; int lds;
+  int M;
+  int q_cols, kv_cols, layer_cols, n_layers;
+  int head_dim, n_kv_heads;
+  void* q_out; int ldq;
+  const void* q_norm; const void* k_norm; int norm_layer_stride;
+  void* kcache; void* vcache; size_t cache_layer_stride;
+  const int32_t* page_table; int max_pages;
+  const float* rope; int rope_max_pos;
+  float eps;
+  int rows_per_seq, seq_stride;
+  const int32_t* pos0; const int32_t* nrows;
+};
+
+// LM head with a fused argmax: logits = X * W^T over the vocabulary; each workgroup
+// reduces its columns to one (value, index) key per row in part_keys[wg][M]
+// (max value, lowest index among equal values), reduced by argmax_reduce.
+struct LmHeadArgs {
+  const void* A; int lda; int a_rows; int M;
+  const void* B; int N; int Kp;
+  uint64_t* part_keys;             // [gridDim.x][M]
+  float* logits; int ldl;          // optional fp32 logits
+};
+int lmhead_grid(int N);
+
 // Host-side launch helpers (implemented in gemm.hip).
 template <typename T>
 void pack_weights(const T* W, int N, int K, int Kp, T* out, hipStream_t s);
@@ -72,9 +89,17 @@ template <typename T>
 void pack_interleaved(const T* Wa, const T* Wb, int N, int K, int Kp, T* out, hipStream_t s);
 
 enum GemmShape : int { SHAPE_SKINNY = 0, SHAPE_WIDE = 1 };
+// SHAPE_SKINNY: M <= 32, 16 or 32-row tiles, the k range split across the workgroup's
+// waves and reduced in LDS (no ksplit).  SHAPE_WIDE: 128x128 tiles, optional ksplit.
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s);
-int gemm_tile_cols(int shape);
-int gemm_tile_rows(int shape);
+int gemm_tile_cols(int shape, int N);
+int gemm_tile_rows(int shape, int M);
+template <typename T>
+hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s);
+template <typename T>
+hipError_t lm_head(const LmHeadArgs& a, hipStream_t s);
+// keys[m] = max over part_keys[0..nparts)[m]; optional token ids
+hipError_t argmax_reduce(const uint64_t* part_keys, int nparts, int M, uint64_t* keys, hipStream_t s);
 
 }  // namespace rt

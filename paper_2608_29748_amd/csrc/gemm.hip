@@ -5,8 +5,9 @@ namespace rt {
 
 // ------------------------------------------------------------------ packing
 
-// out tile (nt, kt), lane l, element e  <-  W[n = src_tile*16 + l%16][k = kt*32 + (l/16)*8 + e]
-// (zero for k >= K).  With Wb set, output tiles alternate Wa tile j / Wb tile j.
+// out tile (nt, kt), lane l, element e  <-  W[n = nt*16 + l%16][k = kt*32 + (l/16)*8 + e]
+// (zero for k >= K).  With Wb set, output tile nt holds rows nt*8..nt*8+7 of Wa in its
+// columns 0..7 and the same rows of Wb in columns 8..15 (gate | up pairs side by side).
 template <typename T>
 __global__ void pack_kernel(const T* __restrict__ Wa, const T* __restrict__ Wb, int N, int K, int Kp,
                             T* __restrict__ out) {
@@ -20,9 +21,12 @@ __global__ void pack_kernel(const T* __restrict__ Wa, const T* __restrict__ Wb, 
     const int kt = (int)(tile % KT);
     const int nt = (int)(tile / KT);
     const T* src = Wa;
-    int st = nt;
-    if (Wb) { src = (nt & 1) ? Wb : Wa; st = nt >> 1; }
-    const int n = st * kTileN + (lane % 16);
+    int n = nt * kTileN + (lane % 16);
+    if (Wb) {
+      const int c = lane % 16;
+      src = c < 8 ? Wa : Wb;
+      n = nt * 8 + (c % 8);
+    }
     const int k0 = kt * kTileK + (lane / 16) * 8;
     T* dst = out + c * 8;
     for (int e = 0; e < 8; ++e) {
@@ -83,146 +87,149 @@ template <> struct AFrag<float, true> : AFrag<float, false> {};
 
 // ------------------------------------------------------------------ epilogues
 
-template <typename T, int ROWS, int COLS, int LDT>
+// Runs on a complete fp32 output tile t[ROWS][COLS] held in LDS (NTH threads).
+template <typename T, int ROWS, int COLS, int LDT, int NTH>
 __device__ void run_epilogue(const EpiArgs& e, float (*t)[LDT], int m0, int n0) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  switch (e.kind) {
-    case EPI_STORE_F32:
-    case EPI_STORE_ACT:
-    case EPI_RESID:
-    case EPI_COND_R:
-    case EPI_COND_GATE:
-    case EPI_COND_OUT: {
-      for (int idx = tid; idx < ROWS * COLS; idx += 256) {
-        const int r = idx / COLS, c = idx % COLS;
-        const int m = m0 + r, n = n0 + c;
-        if (m >= e.M || n >= e.N) continue;
-        const float y = t[r][c];
-        if (e.kind == EPI_STORE_F32) {
-          e.out_f32[(size_t)m * e.ldo + n] = y;
-        } else if (e.kind == EPI_STORE_ACT) {
-          ((T*)e.out_act)[(size_t)m * e.ldo + n] = Elem<T>::from_f32(y);
-        } else if (e.kind == EPI_RESID) {
-          float* px = e.resid + (size_t)m * e.ldr + n;
-          const float x = *px + y;
-          *px = x;
-          if (e.cap) ((T*)e.cap)[(size_t)m * e.ldcap + n] = Elem<T>::from_f32(x);
-        } else if (e.kind == EPI_COND_R) {
-          e.out_f32[(size_t)m * e.ldo + n] = e.cond_m[(size_t)m * e.ld_cond_m + n] + e.beta * y;
-        } else if (e.kind == EPI_COND_GATE) {
-          e.out_f32[(size_t)m * e.ldo + n] = 1.0f / (1.0f + expf(-y));
-        } else {  // EPI_COND_OUT
-          const int s = m / e.rows_per_seq, j = m % e.rows_per_seq;
-          const int tok = (j == 0) ? e.anchor[s * e.seq_stride] : e.mask_token;
-          const float ev = Elem<T>::to_f32(((const T*)e.embed)[(size_t)tok * e.N + n]);
-          const bool cond = (j >= 1) && (j <= e.cond_len[s * e.seq_stride]);
-          const float x = cond ? ev + y * e.gate[(size_t)m * e.ld_gate + n] : ev;
-          e.resid[(size_t)m * e.ldr + n] = x;
-          e.etilde[(size_t)m * e.ldr + n] = x;
-        }
-      }
-      break;
+  const int tid = threadIdx.x;
+  if (e.kind == EPI_SWIGLU) {
+    // per 16-column tile: columns 0..7 gate, 8..15 up, for 8 consecutive outputs
+    constexpr int OC = COLS / 2;
+    for (int idx = tid; idx < ROWS * OC; idx += NTH) {
+      const int r = idx / OC, j = idx % OC;
+      const int m = m0 + r;
+      const int cg = (j / 8) * 16 + (j % 8);
+      if (m >= e.M || n0 + cg >= e.N) continue;
+      const float g = t[r][cg], u = t[r][cg + 8];
+      const float act = g / (1.0f + expf(-g)) * u;
+      ((T*)e.out_act)[(size_t)m * e.ldo + n0 / 2 + j] = Elem<T>::from_f32(act);
     }
-    case EPI_SWIGLU: {
-      // LDS columns: per 32-column group g, [g*32, g*32+16) gate tile, [g*32+16, g*32+32) up tile.
-      constexpr int OC = COLS / 2;
-      for (int idx = tid; idx < ROWS * OC; idx += 256) {
-        const int r = idx / OC, j = idx % OC;
-        const int m = m0 + r;
-        const int cg = (j / 16) * 32 + (j % 16);
-        if (m >= e.M || n0 + cg >= e.N) continue;
-        const float g = t[r][cg], u = t[r][cg + 16];
-        const float a = g / (1.0f + expf(-g)) * u;
-        ((T*)e.out_act)[(size_t)m * e.ldo + n0 / 2 + j] = Elem<T>::from_f32(a);
+    return;
+  }
+  for (int idx = tid; idx < ROWS * COLS; idx += NTH) {
+    const int r = idx / COLS, c = idx % COLS;
+    const int m = m0 + r, n = n0 + c;
+    if (m >= e.M || n >= e.N) continue;
+    const float y = t[r][c];
+    switch (e.kind) {
+      case EPI_STORE_F32: e.out_f32[(size_t)m * e.ldo + n] = y; break;
+      case EPI_STORE_ACT: ((T*)e.out_act)[(size_t)m * e.ldo + n] = Elem<T>::from_f32(y); break;
+      case EPI_RESID: {
+        float* px = e.resid + (size_t)m * e.ldr + n;
+        const float x = *px + y;
+        *px = x;
+        if (e.cap) ((T*)e.cap)[(size_t)m * e.ldcap + n] = Elem<T>::from_f32(x);
+        break;
       }
-      break;
-    }
-    case EPI_ARGMAX: {
-      for (int r = w; r < ROWS; r += 4) {
-        const int m = m0 + r;
-        if (m >= e.M) continue;
-        uint64_t best = 0;
-        for (int c = lane; c < COLS; c += 64) {
-          const int n = n0 + c;
-          if (n >= e.N) continue;
-          const float y = t[r][c];
-          if (e.out_f32) e.out_f32[(size_t)m * e.ldo + n] = y;
-          const uint64_t k = argmax_key(y, (uint32_t)n);
-          best = k > best ? k : best;
-        }
-        for (int o = 32; o > 0; o >>= 1) {
-          const uint64_t other = __shfl_xor(best, o, 64);
-          best = other > best ? other : best;
-        }
-        if (lane == 0) atomicMax((unsigned long long*)&e.keys[m], (unsigned long long)best);
+      case EPI_COND_R:
+        e.out_f32[(size_t)m * e.ldo + n] = e.cond_m[(size_t)m * e.ld_cond_m + n] + e.beta * y;
+        break;
+      case EPI_COND_GATE: e.out_f32[(size_t)m * e.ldo + n] = 1.0f / (1.0f + expf(-y)); break;
+      default: {  // EPI_COND_OUT
+        const int s = m / e.rows_per_seq, j = m % e.rows_per_seq;
+        const int tok = (j == 0) ? e.anchor[s * e.seq_stride] : e.mask_token;
+        const float ev = Elem<T>::to_f32(((const T*)e.embed)[(size_t)tok * e.N + n]);
+        const bool cond = (j >= 1) && (j <= e.cond_len[s * e.seq_stride]);
+        const float x = cond ? ev + y * e.gate[(size_t)m * e.ld_gate + n] : ev;
+        e.resid[(size_t)m * e.ldr + n] = x;
+        e.etilde[(size_t)m * e.ldr + n] = x;
       }
-      break;
-    }
-    case EPI_QKV: {
-      const int hd = e.head_dim, half = hd / 2;
-      const int heads_per_item = 64 / half;          // 1 (hd 128) or 2 (hd 64)
-      const int hh = lane / half, ei = lane % half;
-      const int layer = n0 / e.layer_cols;
-      const int cin = n0 % e.layer_cols;
-      int region, hbase;                              // 0 q, 1 k, 2 v; first head of the tile
-      if (cin < e.q_cols) { region = 0; hbase = cin / hd; }
-      else if (cin < e.q_cols + e.kv_cols) { region = 1; hbase = (cin - e.q_cols) / hd; }
-      else { region = 2; hbase = (cin - e.q_cols - e.kv_cols) / hd; }
-      const int items_per_row = COLS / (hd * heads_per_item);
-      for (int it = w; it < ROWS * items_per_row; it += 4) {
-        const int r = it / items_per_row;
-        const int c0 = (it % items_per_row) * hd * heads_per_item + hh * hd;
-        const int m = m0 + r;
-        if (m >= e.M) continue;
-        const int s = m / e.rows_per_seq, i = m % e.rows_per_seq;
-        if (e.nrows && i >= e.nrows[s * e.seq_stride]) continue;
-        const int pos = e.pos0[s * e.seq_stride] + i;
-        float x0 = t[r][c0 + ei], x1 = t[r][c0 + ei + half];
-        const int head = hbase + (c0 / hd);
-        if (region < 2) {
-          float ss = x0 * x0 + x1 * x1;
-          for (int o = half / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
-          const float inv = 1.0f / sqrtf(ss / (float)hd + e.eps);
-          const T* nw = (const T*)(region == 0 ? e.q_norm : e.k_norm) + (size_t)layer * e.norm_layer_stride;
-          x0 = x0 * inv * Elem<T>::to_f32(nw[ei]);
-          x1 = x1 * inv * Elem<T>::to_f32(nw[ei + half]);
-          const float cs = e.rope[(size_t)pos * half + ei];
-          const float sn = e.rope[(size_t)e.rope_max_pos * half + (size_t)pos * half + ei];
-          const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
-          x0 = y0; x1 = y1;
-        }
-        if (region == 0) {
-          T* q = (T*)e.out_act + (size_t)m * e.ldo + (size_t)head * hd;
-          q[ei] = Elem<T>::from_f32(x0);
-          q[ei + half] = Elem<T>::from_f32(x1);
-        } else {
-          const int page = e.page_table[(size_t)s * e.max_pages + pos / kPage];
-          const int tok = pos % kPage;
-          const size_t pbase = ((size_t)page * e.n_kv_heads + head) * (size_t)kPage * hd;
-          if (region == 1) {   // K page layout [page][kv head][token][hd]
-            T* k = (T*)e.kcache + (size_t)layer * e.cache_layer_stride + pbase + (size_t)tok * hd;
-            k[ei] = Elem<T>::from_f32(x0);
-            k[ei + half] = Elem<T>::from_f32(x1);
-          } else {             // V page layout [page][kv head][hd][token]
-            T* v = (T*)e.vcache + (size_t)layer * e.cache_layer_stride + pbase + tok;
-            v[(size_t)ei * kPage] = Elem<T>::from_f32(x0);
-            v[(size_t)(ei + half) * kPage] = Elem<T>::from_f32(x1);
-          }
-        }
-      }
-      break;
     }
   }
 }
 
-// ------------------------------------------------------------------ kernel
+// ------------------------------------------------------------------ skinny GEMM (M <= 32)
+// Workgroup tile (MT*16) x (NT*16); its NW waves split the reduction into contiguous
+// k ranges (each streams its own run of packed weight tiles) and the partial tiles are
+// summed in wave order through LDS.
+
+template <typename T, bool AF32, int MT, int NT, int NW, int U>
+__global__ __launch_bounds__(NW * 64) void gemm16_kernel(GemmArgs a) {
+  constexpr int ROWS = MT * 16, COLS = NT * 16, LDT = COLS + 1;
+  constexpr int AB = AF32 ? 4 : Elem<T>::kBytes;
+  __shared__ float red[NW][ROWS][COLS];
+  __shared__ float tile[ROWS][LDT];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m0 = blockIdx.y * ROWS, n0 = blockIdx.x * COLS;
+  const int KT = a.Kp / kTileK;
+  const int kb = KT * w / NW, ke = KT * (w + 1) / NW;
+  const int n_tiles_valid = a.e.N / kTileN;
+  const T* bptr[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int ntg = n0 / kTileN + nt;
+    bptr[nt] = (const T*)a.B + ((size_t)(ntg < n_tiles_valid ? ntg : 0) * KT) * 512 + lane * 8;
+  }
+  const char* aptr[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    int row = m0 + mt * 16 + (lane % 16);
+    if (row >= a.a_rows) row = a.a_rows - 1;
+    aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + (lane / 16) * 8) * AB;
+  }
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int kt = kb;
+  for (; kt + U <= ke; kt += U) {
+    Frag<T> bf[U][NT];
+    AFrag<T, AF32> af[U][MT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)(kt + u) * 512);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)(kt + u) * kTileK * AB);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keep all U tiles' loads in flight before the MFMAs
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) af[u][mt].mma_into(acc[mt][nt], bf[u][nt]);
+  }
+  for (; kt < ke; ++kt) {
+    Frag<T> bf[NT];
+    AFrag<T, AF32> af[MT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) bf[nt].load(bptr[nt] + (size_t)kt * 512);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) af[mt].load(aptr[mt] + (size_t)kt * kTileK * AB);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) af[mt].mma_into(acc[mt][nt], bf[nt]);
+  }
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * (lane / 16) + i][nt * 16 + (lane % 16)] = acc[mt][nt][i];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < ROWS * COLS; idx += NW * 64) {
+    const int r = idx / COLS, c = idx % COLS;
+    float sum = 0.f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) sum += red[v][r][c];
+    tile[r][c] = sum;
+  }
+  __syncthreads();
+  run_epilogue<T, ROWS, COLS, LDT, NW * 64>(a.e, tile, m0, n0);
+}
+
+// ------------------------------------------------------------------ wide GEMM (large M)
 
 template <typename T, bool AF32, int MT, int NT, int WM, int WN, int U>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
   constexpr int ROWS = WM * MT * 16, COLS = WN * NT * 16, LDT = COLS + 4;
   __shared__ float tile[ROWS][LDT];
   __shared__ int s_last;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w / WN, wn = w % WN;
   const int bx = blockIdx.x, by = blockIdx.y, kz = blockIdx.z;
   const int m0 = by * ROWS, n0 = bx * COLS;
@@ -230,15 +237,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   const int kb = (int)((long long)KT * kz / a.ksplit);
   const int ke = (int)((long long)KT * (kz + 1) / a.ksplit);
   const int n_tiles_valid = a.e.N / kTileN;
-  constexpr int AB = AF32 ? 4 : Elem<T>::kBytes;     // bytes per A element
-
+  constexpr int AB = AF32 ? 4 : Elem<T>::kBytes;
   const T* bptr[NT];
-  bool bval[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int ntg = (n0 + wn * NT * 16) / kTileN + nt;
-    bval[nt] = ntg < n_tiles_valid;
-    bptr[nt] = (const T*)a.B + ((size_t)(bval[nt] ? ntg : 0) * KT) * 512 + lane * 8;
+    bptr[nt] = (const T*)a.B + ((size_t)(ntg < n_tiles_valid ? ntg : 0) * KT) * 512 + lane * 8;
   }
   const char* aptr[MT];
 #pragma unroll
@@ -247,25 +251,21 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     if (row >= a.a_rows) row = a.a_rows - 1;
     aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + (lane / 16) * 8) * AB;
   }
-
   f32x4 acc[MT][NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   for (int kt = kb; kt < ke; kt += U) {
     Frag<T> bf[U][NT];
     AFrag<T, AF32> af[U][MT];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (kt + u < ke) {
+      const int k = kt + u < ke ? kt + u : ke - 1;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-          if (bval[nt]) bf[u][nt].load(bptr[nt] + (size_t)(kt + u) * 512);
+      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)(kt + u) * kTileK * AB);
-      }
+      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * kTileK * AB);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -273,12 +273,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-            if (bval[nt]) af[u][mt].mma_into(acc[mt][nt], bf[u][nt]);
+          for (int nt = 0; nt < NT; ++nt) af[u][mt].mma_into(acc[mt][nt], bf[u][nt]);
       }
     }
   }
-
   const int tile_id = by * gridDim.x + bx;
   if (a.ksplit == 1) {
 #pragma unroll
@@ -291,6 +289,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
               acc[mt][nt][i];
     __syncthreads();
   } else {
+    // split k: fp32 partial tiles; the last workgroup of a tile sums them in split order
     float* part = a.partial + ((size_t)tile_id * a.ksplit + kz) * (ROWS * COLS);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -298,8 +297,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          part[(wm * MT * 16 + mt * 16 + 4 * (lane / 16) + i) * COLS + wn * NT * 16 + nt * 16 +
-               (lane % 16)] = acc[mt][nt][i];
+          part[(wm * MT * 16 + mt * 16 + 4 * (lane / 16) + i) * COLS + wn * NT * 16 + nt * 16 + (lane % 16)] =
+              acc[mt][nt][i];
     __threadfence();
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -309,39 +308,271 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
+    __threadfence();   // acquire: every split's partial tile is visible
+    constexpr int PER = ROWS * COLS / 256;
+    float sum[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) sum[i] = 0.f;
     const float* base = a.partial + (size_t)tile_id * a.ksplit * (ROWS * COLS);
-    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += 256) {
-      float sum = 0.f;
-      for (int z = 0; z < a.ksplit; ++z)
-        sum += __hip_atomic_load(base + (size_t)z * ROWS * COLS + idx, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-      tile[idx / COLS][idx % COLS] = sum;
+    for (int z = 0; z < a.ksplit; ++z) {
+      const float* pz = base + (size_t)z * ROWS * COLS + threadIdx.x;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) sum[i] += pz[i * 256];
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = threadIdx.x + i * 256;
+      tile[idx / COLS][idx % COLS] = sum[i];
     }
     if (threadIdx.x == 0) a.counters[tile_id] = 0u;
     __syncthreads();
   }
-  run_epilogue<T, ROWS, COLS, LDT>(a.e, tile, m0, n0);
+  run_epilogue<T, ROWS, COLS, LDT, 256>(a.e, tile, m0, n0);
 }
 
-int gemm_tile_cols(int) { return 128; }
-int gemm_tile_rows(int shape) { return shape == SHAPE_SKINNY ? 16 : 128; }
+int gemm_tile_rows(int shape, int M) { return shape == SHAPE_SKINNY ? (M > 16 ? 32 : 16) : 128; }
+int gemm_tile_cols(int shape, int) { return shape == SHAPE_SKINNY ? 16 : 128; }
 
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
-  const int rows = gemm_tile_rows(shape);
-  dim3 grid((a.e.N + 127) / 128, (a.e.M + rows - 1) / rows, a.ksplit);
-  if (grid.x == 0 || grid.y == 0) return hipSuccess;
+  const int M = a.e.M, N = a.e.N;
+  if (M <= 0 || N <= 0) return hipSuccess;
   if (shape == SHAPE_SKINNY) {
-    if (a_f32) hipLaunchKernelGGL((gemm_kernel<T, true, 1, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<T, false, 1, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
+    if (M > 32) return hipErrorInvalidValue;
+    dim3 grid((N + 15) / 16, 1, 1);
+    if (a_f32) {
+      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
+    } else {
+      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, false, 2, 1, 8, 8>), grid, dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);
+    }
   } else {
-    if (a_f32) hipLaunchKernelGGL((gemm_kernel<T, true, 4, 4, 2, 2, 1>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<T, false, 4, 4, 2, 2, 2>), grid, dim3(256), 0, s, a);
+    dim3 grid((N + 127) / 128, (M + 127) / 128, a.ksplit);
+    if (a_f32) hipLaunchKernelGGL((gemm_wide_kernel<T, true, 4, 4, 2, 2, 1>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((gemm_wide_kernel<T, false, 4, 4, 2, 2, 2>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
 template hipError_t gemm<bf16_t>(const GemmArgs&, int, bool, hipStream_t);
 template hipError_t gemm<float>(const GemmArgs&, int, bool, hipStream_t);
+
+// ------------------------------------------------------------------ q/k/v post-processing
+
+template <typename T>
+__global__ __launch_bounds__(256) void qkv_post_kernel(QkvPostArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int hd = a.head_dim, half = hd / 2;
+  const int heads_per_layer = a.layer_cols / hd;
+  const int heads = heads_per_layer * a.n_layers;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= a.M * heads) return;
+  const int m = item / heads, hid = item % heads;
+  const int layer = hid / heads_per_layer, hin = hid % heads_per_layer;
+  const int s = m / a.rows_per_seq, i = m % a.rows_per_seq;
+  if (a.nrows && i >= a.nrows[s * a.seq_stride]) return;
+  const int pos = a.pos0[s * a.seq_stride] + i;
+  const int qh = a.q_cols / hd, kvh = a.kv_cols / hd;
+  const int region = hin < qh ? 0 : (hin < qh + kvh ? 1 : 2);
+  const int head = region == 0 ? hin : (region == 1 ? hin - qh : hin - qh - kvh);
+  if (lane >= half) return;
+  const float* src = a.src + (size_t)m * a.lds + (size_t)layer * a.layer_cols + (size_t)hin * hd;
+  float x0 = src[lane], x1 = src[lane + half];
+  if (region < 2) {
+    float ss = x0 * x0 + x1 * x1;
+    for (int o = half / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    const float inv = 1.0f / sqrtf(ss / (float)hd + a.eps);
+    const T* nw = (const T*)(region == 0 ? a.q_norm : a.k_norm) + (size_t)layer * a.norm_layer_stride;
+    x0 = x0 * inv * Elem<T>::to_f32(nw[lane]);
+    x1 = x1 * inv * Elem<T>::to_f32(nw[lane + half]);
+    const float cs = a.rope[(size_t)pos * half + lane];
+    const float sn = a.rope[(size_t)a.rope_max_pos * half + (size_t)pos * half + lane];
+    const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+    x0 = y0;
+    x1 = y1;
+  }
+  if (region == 0) {
+    T* q = (T*)a.q_out + (size_t)m * a.ldq + (size_t)head * hd;
+    q[lane] = Elem<T>::from_f32(x0);
+    q[lane + half] = Elem<T>::from_f32(x1);
+    return;
+  }
+  const int page = a.page_table[(size_t)s * a.max_pages + pos / kPage];
+  const int tok = pos % kPage;
+  const size_t pbase = (size_t)layer * a.cache_layer_stride + ((size_t)page * a.n_kv_heads + head) * (size_t)kPage * hd;
+  if (region == 1) {   // K page layout [page][kv head][token][hd]
+    T* k = (T*)a.kcache + pbase + (size_t)tok * hd;
+    k[lane] = Elem<T>::from_f32(x0);
+    k[lane + half] = Elem<T>::from_f32(x1);
+  } else {             // V page layout [page][kv head][hd][token]
+    T* v = (T*)a.vcache + pbase + tok;
+    v[(size_t)lane * kPage] = Elem<T>::from_f32(x0);
+    v[(size_t)(lane + half) * kPage] = Elem<T>::from_f32(x1);
+  }
+}
+
+template <typename T>
+hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s) {
+  const int heads = (a.layer_cols / a.head_dim) * a.n_layers;
+  const long long items = (long long)a.M * heads;
+  if (items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t qkv_post<bf16_t>(const QkvPostArgs&, hipStream_t);
+template hipError_t qkv_post<float>(const QkvPostArgs&, hipStream_t);
+
+// ------------------------------------------------------------------ LM head + argmax
+
+constexpr int kLmTilesPerWave = 2;
+int lmhead_grid(int N) {
+  const int tiles = (N + 31) / 32;
+  return (tiles + 4 * kLmTilesPerWave - 1) / (4 * kLmTilesPerWave);
+}
+
+// Each wave owns 32-column tiles (two 16-column MFMA tiles) over the full reduction and
+// keeps, per row, the best (value, index) key seen; the workgroup's four waves then
+// combine their keys through LDS.
+template <typename T, int MT, int U>
+__global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
+  constexpr int ROWS = MT * 16;
+  __shared__ uint64_t wkeys[4][ROWS];
+  const int lane = threadIdx.x & 63, g4 = lane / 16, c16 = lane % 16;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int KT = a.Kp / kTileK;
+  const int n_tiles16 = a.N / kTileN;
+  const char* aptr[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    int row = mt * 16 + c16;
+    if (row >= a.a_rows) row = a.a_rows - 1;
+    aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + g4 * 8) * Elem<T>::kBytes;
+  }
+  uint64_t best[MT][4];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) best[mt][i] = 0ull;
+  const int tiles32 = (a.N + 31) / 32;
+  for (int t = blockIdx.x * 4 + w; t < tiles32; t += gridDim.x * 4) {
+    const T* bptr[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int ntg = t * 2 + nt;
+      bptr[nt] = (const T*)a.B + ((size_t)(ntg < n_tiles16 ? ntg : 0) * KT) * 512 + lane * 8;
+    }
+    f32x4 acc[MT][2];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int kt = 0;
+    for (; kt + U <= KT; kt += U) {
+      Frag<T> bf[U][2];
+      Frag<T> af[U][MT];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        bf[u][0].load(bptr[0] + (size_t)(kt + u) * 512);
+        bf[u][1].load(bptr[1] + (size_t)(kt + u) * 512);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) af[u][mt].load((const T*)(aptr[mt]) + (size_t)(kt + u) * kTileK);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          mma(acc[mt][0], af[u][mt], bf[u][0]);
+          mma(acc[mt][1], af[u][mt], bf[u][1]);
+        }
+    }
+    for (; kt < KT; ++kt) {
+      Frag<T> b0, b1, af[MT];
+      b0.load(bptr[0] + (size_t)kt * 512);
+      b1.load(bptr[1] + (size_t)kt * 512);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) af[mt].load((const T*)(aptr[mt]) + (size_t)kt * kTileK);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        mma(acc[mt][0], af[mt], b0);
+        mma(acc[mt][1], af[mt], b1);
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = mt * 16 + 4 * g4 + i;
+        uint64_t k = 0ull;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int n = t * 32 + nt * 16 + c16;
+          if (n < a.N) {
+            const float y = acc[mt][nt][i];
+            if (a.logits && row < a.M) a.logits[(size_t)row * a.ldl + n] = y;
+            const uint64_t kk = argmax_key(y, (uint32_t)n);
+            k = kk > k ? kk : k;
+          }
+        }
+        best[mt][i] = k > best[mt][i] ? k : best[mt][i];
+      }
+  }
+  // reduce over the 16 lanes holding the same rows, then over the four waves
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint64_t k = best[mt][i];
+      for (int o = 8; o > 0; o >>= 1) {
+        const uint64_t other = __shfl_xor(k, o, 64);
+        k = other > k ? other : k;
+      }
+      if (c16 == 0) wkeys[w][mt * 16 + 4 * g4 + i] = k;
+    }
+  __syncthreads();
+  if (threadIdx.x < ROWS && (int)threadIdx.x < a.M) {
+    uint64_t k = wkeys[0][threadIdx.x];
+#pragma unroll
+    for (int v = 1; v < 4; ++v) k = wkeys[v][threadIdx.x] > k ? wkeys[v][threadIdx.x] : k;
+    a.part_keys[(size_t)blockIdx.x * a.M + threadIdx.x] = k;
+  }
+}
+
+template <typename T>
+hipError_t lm_head(const LmHeadArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.M > 32) return hipErrorInvalidValue;
+  dim3 grid(lmhead_grid(a.N));
+  if (a.M > 16) hipLaunchKernelGGL((lmhead_kernel<T, 2, 8>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((lmhead_kernel<T, 1, 8>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t lm_head<bf16_t>(const LmHeadArgs&, hipStream_t);
+template hipError_t lm_head<float>(const LmHeadArgs&, hipStream_t);
+
+__global__ __launch_bounds__(256) void argmax_reduce_kernel(const uint64_t* __restrict__ part, int nparts, int M,
+                                                            uint64_t* keys) {
+  __shared__ uint64_t red[4];
+  const int row = blockIdx.x;
+  uint64_t k = 0ull;
+  for (int j = threadIdx.x; j < nparts; j += 256) {
+    const uint64_t v = part[(size_t)j * M + row];
+    k = v > k ? v : k;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t other = __shfl_xor(k, o, 64);
+    k = other > k ? other : k;
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = k;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t b = red[0];
+    for (int v = 1; v < 4; ++v) b = red[v] > b ? red[v] : b;
+    keys[row] = b;
+  }
+}
+hipError_t argmax_reduce(const uint64_t* part_keys, int nparts, int M, uint64_t* keys, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(M), dim3(256), 0, s, part_keys, nparts, M, keys);
+  return hipGetLastError();
+}
 
 }  // namespace rt

@@ -42,6 +42,8 @@ struct Plan {
   size_t page_table, rope, state, pf_ints, first_tok, counters, partial, opart, mlpart;
   size_t x, xa, qbuf, attn, mlp, g, fcout, fa, etilde, mu, er, gate;
   size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
+  size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys
+  int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init
   size_t total;
 };

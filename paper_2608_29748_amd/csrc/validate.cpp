@@ -84,8 +84,9 @@ int make_plan(const rt_config* c, Plan* p) {
   q.Mrows = (int)rup((size_t)(q.R > q.PF ? q.R : q.PF), 128);
   q.attn_rb = (q.bk * q.G + 63) / 64;
   {
+    // key splits: about two workgroups per compute unit, each split at least 64 keys
     const int base = q.bmax * q.Hkv * q.attn_rb;
-    int sp = (768 + base - 1) / base;
+    int sp = (512 + base - 1) / base;
     const int maxsp = (q.T + 63) / 64;
     if (sp > maxsp) sp = maxsp;
     if (sp < 1) sp = 1;
@@ -161,6 +162,12 @@ int make_plan(const rt_config* c, Plan* p) {
   q.vlogits = take((size_t)q.R * q.V * 4);
   q.dkeys = take(M * 8);
   q.tkeys = take(M * 8);
+  {
+    const size_t qc = (size_t)q.qkvN > (size_t)q.LD * 2 * q.kvN ? (size_t)q.qkvN : (size_t)q.LD * 2 * q.kvN;
+    q.qkvf = take(M * qc * 4);
+    q.lm_parts = (q.V + 31) / 32 / 8 + 1;
+    q.part_keys = take((size_t)q.lm_parts * M * 8);
+  }
   q.dtok = take((size_t)q.R * 4);
   q.ttok = take((size_t)q.R * 4);
   q.out_tok = take((size_t)q.R * 4);

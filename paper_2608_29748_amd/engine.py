@@ -71,6 +71,9 @@ class RoundEngine:
     def spec_round_forced(self, drafts: np.ndarray):
         return B.rt_spec_round_forced(self.h, drafts, self.cfg.block_size)
 
+    def profile_round(self):
+        return B.rt_profile_round(self.h, self.n_seqs, self.cfg.block_size)
+
     def set_debug(self, flags: int) -> None:
         B.rt_set_debug(self.h, flags)
 
