@@ -19,7 +19,7 @@ struct AttnArgs {
   int splits;                    // key-range splits per (seq, kv head, row block)
   int row_blocks;                // row blocks of 64 (token, head) rows per sequence
   float* opart; float* mlpart;   // split partials
-  void* out; int ldo;            // [row][n_q_heads * head_dim]
+  void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)
 };
 

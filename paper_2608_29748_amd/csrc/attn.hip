@@ -187,9 +187,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       if (r >= nrows) continue;
       const int tok = r / G, h = kvh * G + r % G;
       const float inv = lrun[i] > 0.f ? 1.f / lrun[i] : 0.f;
-      T* op = (T*)a.out + (size_t)(s * a.rows_per_seq + tok) * a.ldo + (size_t)h * HD;
+      T* op = (T*)a.out;
+      const int orow = s * a.rows_per_seq + tok;
 #pragma unroll
-      for (int t = 0; t < NHT; ++t) op[t * 16 + c16] = Elem<T>::from_f32(o[t][i] * inv);
+      for (int t = 0; t < NHT; ++t) op[pa_index(orow, h * HD + t * 16 + c16, a.ldo)] = Elem<T>::from_f32(o[t][i] * inv);
     }
   } else {
     const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
@@ -254,10 +255,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   }
   den = warp_sum(den);
   const int tok = r / G, h = kvh * G + r % G;
-  T* out = (T*)a.out + (size_t)(s * a.rows_per_seq + tok) * a.ldo + (size_t)h * HD;
+  T* out = (T*)a.out;
+  const int orow = s * a.rows_per_seq + tok;
   const float inv = den > 0.f ? 1.f / den : 0.f;
 #pragma unroll
-  for (int j = 0; j < PL; ++j) out[lane + 64 * j] = Elem<T>::from_f32(num[j] * inv);
+  for (int j = 0; j < PL; ++j) out[pa_index(orow, h * HD + lane + 64 * j, a.ldo)] = Elem<T>::from_f32(num[j] * inv);
 }
 
 template <typename T>

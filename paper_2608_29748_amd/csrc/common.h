@@ -47,6 +47,7 @@ template <typename T> struct Frag;
 template <> struct Frag<bf16_t> {
   bf16x8 v;
   __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const bf16x8*>(p); }
+  __device__ __forceinline__ void store(bf16_t* p) const { *reinterpret_cast<bf16x8*>(p) = v; }
   __device__ __forceinline__ void zero() { for (int i = 0; i < 8; ++i) v[i] = 0; }
   __device__ __forceinline__ float get(int i) const { return bf16_to_f32((bf16_t)v[i]); }
   __device__ __forceinline__ void set(int i, float f) { v[i] = (short)f32_to_bf16(f); }
@@ -55,6 +56,9 @@ template <> struct Frag<float> {
   float4 lo, hi;
   __device__ __forceinline__ void load(const float* p) {
     lo = *reinterpret_cast<const float4*>(p); hi = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void store(float* p) const {
+    *reinterpret_cast<float4*>(p) = lo; *reinterpret_cast<float4*>(p + 4) = hi;
   }
   __device__ __forceinline__ void zero() { lo = make_float4(0, 0, 0, 0); hi = lo; }
   __device__ __forceinline__ float get(int i) const {
@@ -92,6 +96,14 @@ __device__ __forceinline__ float warp_sum(float v, int width = 64) {
 __device__ __forceinline__ float warp_max(float v, int width = 64) {
   for (int o = width / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
+}
+
+// Fragment-ordered ("packed") layout of GEMM A operands: element (m, k) of an [M][Kp]
+// operand lives at (m/16)*ldg + (k/32)*512 + ((m%16) + 16*((k%32)/8))*8 + k%8 with
+// ldg = 16*Kp, so the fragment one wave needs for a 16-row group and a 32-wide k tile is
+// 512 contiguous elements (lane l reads elements l*8 .. l*8+7).
+__host__ __device__ __forceinline__ size_t pa_index(int m, int k, size_t ldg) {
+  return (size_t)(m >> 4) * ldg + (size_t)(k >> 5) * 512 + (size_t)((((m & 15) + 16 * ((k & 31) >> 3)) << 3) + (k & 7));
 }
 
 // Monotone map float -> uint32 (larger float -> larger key).

@@ -131,7 +131,8 @@ struct Engine : EngineBase {
     const int32_t* pt;
     T* kc;
     T* vc;
-    T* cap;
+    T* cap;                      // packed capture buffer of the updated residual (null: none)
+    int cap_k0;                  // column offset of this layer's slot in the capture
     const int32_t* prof_ctx;     // host copy of each sequence's context length (profiling only)
   };
 
@@ -140,12 +141,11 @@ struct Engine : EngineBase {
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
     prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
-    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_in), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr, 0,
-                  stream);
+    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_in), q.d, cfg.rms_eps, c.M, xa, 16 * q.Kp_d, nullptr, 0, stream);
     prof_end();
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
-    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
+    CHK(gemm_call(xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
     QkvPostArgs qp{};
     qp.src = at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
     qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
@@ -163,7 +163,7 @@ struct Engine : EngineBase {
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
-    a.out = at<T>(q.attn); a.ldo = q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
+    a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
     if (profiling) {
       // keys read: every sequence's context plus the block, K and V, once per KV head
       double keys = 0;
@@ -176,17 +176,16 @@ struct Engine : EngineBase {
     prof_end();
     e = EpiArgs{};
     e.kind = EPI_RESID; e.resid = x; e.ldr = q.d;
-    CHK(gemm_call(at<T>(q.attn), q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e));
+    CHK(gemm_call(at<T>(q.attn), 16 * q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e, q.qN));
     prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
-    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, q.Kp_d, nullptr, 0, nullptr,
-                  0, stream);
+    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, 16 * q.Kp_d, nullptr, 0, stream);
     prof_end();
     e = EpiArgs{};
-    e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = q.Kp_F;
-    CHK(gemm_call(xa, q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e));
+    e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = 16 * q.Kp_F;
+    CHK(gemm_call(xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e, q.d));
     e = EpiArgs{};
-    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = q.Kp_nc;
-    CHK(gemm_call(at<T>(q.mlp), q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
+    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = 16 * q.Kp_nc; e.cap_k0 = c.cap_k0;
+    CHK(gemm_call(at<T>(q.mlp), 16 * q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
     return RT_OK;
   }
 
@@ -197,7 +196,7 @@ struct Engine : EngineBase {
     for (int r0 = 0; r0 < M; r0 += 32) {          // 32-row passes over the vocabulary
       const int m = M - r0 < 32 ? M - r0 : 32;
       LmHeadArgs h{};
-      h.A = at<T>(q.xa) + (size_t)r0 * q.Kp_d; h.lda = q.Kp_d; h.a_rows = q.Mrows - r0; h.M = m;
+      h.A = at<T>(q.xa) + (size_t)(r0 / 16) * 16 * q.Kp_d; h.lda = 16 * q.Kp_d; h.a_rows = q.Mrows - r0; h.M = m;
       h.B = at<T>(q.lm_head); h.N = q.V; h.Kp = q.Kp_d;
       h.part_keys = at<uint64_t>(q.part_keys); h.logits = logits ? logits + (size_t)r0 * q.V : nullptr;
       h.ldl = q.V;
@@ -223,14 +222,14 @@ struct Engine : EngineBase {
     const Plan& q = p;
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.fcout); e.ldo = q.d;
-    CHK(gemm_call(at<T>(q.g), q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
+    CHK(gemm_call(at<T>(q.g), 16 * q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
     prof_begin(RT_K_NORM, (double)M * q.d * (4 + sizeof(T)), 0);
-    rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), q.Kp_d,
-                  nullptr, 0, nullptr, 0, stream);
+    rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), 16 * q.Kp_d,
+                  nullptr, 0, stream);
     prof_end();
     e = EpiArgs{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.LD * 2 * q.kvN;
-    CHK(gemm_call(at<T>(q.fa), q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e, q.d));
+    CHK(gemm_call(at<T>(q.fa), 16 * q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e, q.d));
     QkvPostArgs qp{};
     qp.src = at<float>(q.qkvf); qp.lds = q.LD * 2 * q.kvN; qp.M = M;
     qp.q_cols = 0; qp.kv_cols = q.kvN; qp.layer_cols = 2 * q.kvN; qp.n_layers = q.LD;
@@ -332,13 +331,13 @@ struct Engine : EngineBase {
           const int slot = cond_slot(l);
           LayerCtx c{n, q.PF, 1, 0, 1, 1, (n * q.G + 63) / 64, pf, pf + 1, pt,
                      at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
-                     slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr, &c0};
+                     slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, &c0};
           CHK(layer(tlayer(l), c));
         }
         CHK(context_append(n, q.PF, pf, nullptr, 0, pt));
         if (c0 + n == len) {
           rmsnorm<T, K>(at<float>(q.x) + (size_t)(n - 1) * q.d, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, 1,
-                        at<T>(q.xa), q.Kp_d, nullptr, 0, nullptr, 0, stream);
+                        at<T>(q.xa), 16 * q.Kp_d, nullptr, 0, stream);
           CHK(lm_head_argmax(1, at<uint64_t>(q.tkeys), nullptr));
           first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), len, budget, at<int32_t>(q.first_tok), stream);
         }
@@ -368,22 +367,24 @@ struct Engine : EngineBase {
     stage(0);
     if (cfg.cond_mode == RT_COND_RETRACE) {
       prof_begin(RT_K_MISC, (double)R * q.d * (4 * q.ksz + sizeof(T) + 16), 0);
+      const int ldg2 = 16 * q.Kp_2d;
       cond_prep<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, at<K>(q.hd_keep), at<K>(q.ht_keep), n_seqs, q.bk,
-                      at<float>(q.mu), at<float>(q.er), stream);
+                      at<float>(q.mu), at<float>(q.er), ldg2, stream);
       prof_end();
       EpiArgs e{};
-      e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er) + q.d; e.ldo = 2 * q.d;
-      e.cond_m = at<float>(q.mu); e.ld_cond_m = 2 * q.d; e.beta = cfg.beta;
-      CHK(gemm_call(at<float>(q.mu), 2 * q.d, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e));
+      e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er); e.ldo = ldg2; e.out_k0 = q.d;
+      e.cond_m = at<float>(q.mu); e.ld_cond_m = ldg2; e.beta = cfg.beta;
+      CHK(gemm_call(at<float>(q.mu), ldg2, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e, 2 * q.d));
       e = EpiArgs{};
       e.kind = EPI_COND_GATE; e.out_f32 = at<float>(q.gate); e.ldo = q.d;
-      CHK(gemm_call(at<float>(q.er), 2 * q.d, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e));
+      CHK(gemm_call(at<float>(q.er), ldg2, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e, 2 * q.d));
       e = EpiArgs{};
       e.kind = EPI_COND_OUT; e.resid = x; e.ldr = q.d; e.etilde = at<float>(q.etilde);
       e.gate = at<float>(q.gate); e.ld_gate = q.d; e.embed = at<T>(q.embed); e.mask_token = cfg.mask_token_id;
       e.anchor = st + ST_ANCHOR; e.cond_len = st + ST_COND_LEN; e.seq_stride = kStateFields;
       e.rows_per_seq = q.bk;
-      CHK(gemm_call(at<float>(q.er) + q.d, 2 * q.d, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e));
+      // r occupies packed k tiles d/32 .. 2d/32 of er
+      CHK(gemm_call(at<float>(q.er) + (size_t)(q.d / 32) * 512, ldg2, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e, q.d));
     } else {
       prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 8), 0);
       embed_block<T>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), q.d, stream);
@@ -394,13 +395,13 @@ struct Engine : EngineBase {
     for (int l = 0; l < q.LD; ++l) {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
-                 nullptr, prof_ctx.data()};
+                 nullptr, 0, prof_ctx.data()};
       CHK(layer(dlayer(l), c));
     }
     stage(2);
     prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
-    rmsnorm<T, K>(x, q.d, at<T>(q.d_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.hd_keep), q.d,
-                  nullptr, 0, stream);
+    rmsnorm<T, K>(x, q.d, at<T>(q.d_final_norm), q.d, cfg.rms_eps, R, xa, 16 * q.Kp_d, at<K>(q.hd_keep), q.d,
+                  stream);
     prof_end();
     CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (flags & 1) ? at<float>(q.dlogits) : nullptr));
     // (3) verify: [anchor, drafts] at P..P+B, causal over the target cache
@@ -413,13 +414,13 @@ struct Engine : EngineBase {
       const int slot = cond_slot(l);
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
-                 slot >= 0 ? at<T>(q.g) + (size_t)slot * q.d : nullptr, prof_ctx.data()};
+                 slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data()};
       CHK(layer(tlayer(l), c));
     }
     stage(4);
     prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
-    rmsnorm<T, K>(x, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, R, xa, q.Kp_d, at<K>(q.ht_keep), q.d,
-                  nullptr, 0, stream);
+    rmsnorm<T, K>(x, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, R, xa, 16 * q.Kp_d, at<K>(q.ht_keep), q.d,
+                  stream);
     prof_end();
     CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
     // (4) acceptance, commit, rollback, carry / reset
@@ -565,11 +566,20 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
     case RT_T_TARGET_TOKENS: off = q.ttok + seq * bk * 4; cap = bk * 4; break;
     case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
     case RT_T_G: {
-      const size_t row = (size_t)q.nc * q.d * q.esz;
-      if (bytes > bk * row) return fail(RT_ERR_INVALID, "read too large");
+      // packed [group][k tile][lane][8] -> row-major [bk][n_cond * d]
+      const size_t ncd = (size_t)q.nc * q.d, ldg = (size_t)16 * q.Kp_nc;
+      if (bytes > bk * ncd * q.esz) return fail(RT_ERR_INVALID, "read too large");
+      const int r0 = seq * q.bk, r1 = r0 + q.bk;
+      const int g0 = r0 / 16, g1 = (r1 + 15) / 16;
+      std::vector<char> buf((size_t)(g1 - g0) * ldg * q.esz);
       HIPCHK(hipStreamSynchronize(stream));
-      HIPCHK(hipMemcpy2D(dst, row, ws + q.g + seq * bk * q.Kp_nc * q.esz, (size_t)q.Kp_nc * q.esz, row,
-                         bytes / row, hipMemcpyDeviceToHost));
+      HIPCHK(hipMemcpy(buf.data(), ws + q.g + (size_t)g0 * ldg * q.esz, buf.size(), hipMemcpyDeviceToHost));
+      char* out = (char*)dst;
+      const size_t nrow = bytes / (ncd * q.esz);
+      for (size_t r = 0; r < nrow; ++r)
+        for (size_t k = 0; k < ncd; ++k)
+          memcpy(out + (r * ncd + k) * q.esz, buf.data() + (pa_index((int)(r0 + r), (int)k, ldg) - (size_t)g0 * ldg) * q.esz,
+                 q.esz);
       return RT_OK;
     }
     default: {

@@ -26,17 +26,18 @@ enum EpiKind : int {
 struct EpiArgs {
   int kind;
   int M, N;                      // valid output extent
-  // generic outputs
-  float* out_f32; void* out_act; int ldo;
+  // generic outputs: out_f32 row-major with ldo, except EPI_COND_R (packed, ldo = group
+  // stride, columns offset by out_k0); out_act always packed (ldo = group stride)
+  float* out_f32; void* out_act; int ldo; int out_k0;
   float* resid; int ldr;
-  void* cap; int ldcap;          // capture (act type), may be null
+  void* cap; int ldcap; int cap_k0;   // packed capture of the updated residual (act type), may be null
   // per-row sequence mapping
   int rows_per_seq;              // row m belongs to sequence m / rows_per_seq, block row m % rows_per_seq
   int seq_stride;                // int32 stride between sequences in pos0 / nrows / anchor / cond_len
   const int32_t* pos0;           // [seq] absolute position of block row 0
   const int32_t* nrows;          // [seq] number of valid block rows (null: all)
   // conditioning
-  const float* cond_m; int ld_cond_m;     // m rows (fp32) for EPI_COND_R
+  const float* cond_m; int ld_cond_m;     // m rows (packed fp32, group stride) for EPI_COND_R
   float beta;
   const float* gate; int ld_gate;
   const void* embed; int mask_token;      // e rows are embedding rows (anchor at block row 0)
@@ -45,7 +46,7 @@ struct EpiArgs {
 };
 
 struct GemmArgs {
-  const void* A; int lda; int a_rows;     // A rows allocated (loads are clamped below it)
+  const void* A; int lda; int a_rows;     // packed A: lda = group stride (elements); rows allocated
   const void* B; int Kp;                  // packed weights, K padded to a multiple of 32
   int ksplit;
   float* partial; uint32_t* counters;
@@ -75,7 +76,7 @@ struct QkvPostArgs {
 // reduces its columns to one (value, index) key per row in part_keys[wg][M]
 // (max value, lowest index among equal values), reduced by argmax_reduce.
 struct LmHeadArgs {
-  const void* A; int lda; int a_rows; int M;
+  const void* A; int lda; int a_rows; int M;   // packed A (lda = group stride)
   const void* B; int N; int Kp;
   uint64_t* part_keys;             // [gridDim.x][M]
   float* logits; int ldl;          // optional fp32 logits

@@ -101,7 +101,7 @@ __device__ void run_epilogue(const EpiArgs& e, float (*t)[LDT], int m0, int n0) 
       if (m >= e.M || n0 + cg >= e.N) continue;
       const float g = t[r][cg], u = t[r][cg + 8];
       const float act = g / (1.0f + expf(-g)) * u;
-      ((T*)e.out_act)[(size_t)m * e.ldo + n0 / 2 + j] = Elem<T>::from_f32(act);
+      ((T*)e.out_act)[pa_index(m, n0 / 2 + j, e.ldo)] = Elem<T>::from_f32(act);
     }
     return;
   }
@@ -112,16 +112,16 @@ __device__ void run_epilogue(const EpiArgs& e, float (*t)[LDT], int m0, int n0) 
     const float y = t[r][c];
     switch (e.kind) {
       case EPI_STORE_F32: e.out_f32[(size_t)m * e.ldo + n] = y; break;
-      case EPI_STORE_ACT: ((T*)e.out_act)[(size_t)m * e.ldo + n] = Elem<T>::from_f32(y); break;
+      case EPI_STORE_ACT: ((T*)e.out_act)[pa_index(m, n, e.ldo)] = Elem<T>::from_f32(y); break;
       case EPI_RESID: {
         float* px = e.resid + (size_t)m * e.ldr + n;
         const float x = *px + y;
         *px = x;
-        if (e.cap) ((T*)e.cap)[(size_t)m * e.ldcap + n] = Elem<T>::from_f32(x);
+        if (e.cap) ((T*)e.cap)[pa_index(m, e.cap_k0 + n, e.ldcap)] = Elem<T>::from_f32(x);
         break;
       }
       case EPI_COND_R:
-        e.out_f32[(size_t)m * e.ldo + n] = e.cond_m[(size_t)m * e.ld_cond_m + n] + e.beta * y;
+        e.out_f32[pa_index(m, e.out_k0 + n, e.ldo)] = e.cond_m[pa_index(m, n, e.ld_cond_m)] + e.beta * y;
         break;
       case EPI_COND_GATE: e.out_f32[(size_t)m * e.ldo + n] = 1.0f / (1.0f + expf(-y)); break;
       default: {  // EPI_COND_OUT
@@ -160,48 +160,42 @@ __global__ __launch_bounds__(NW * 64) void gemm16_kernel(GemmArgs a) {
     const int ntg = n0 / kTileN + nt;
     bptr[nt] = (const T*)a.B + ((size_t)(ntg < n_tiles_valid ? ntg : 0) * KT) * 512 + lane * 8;
   }
+  const int max_group = (a.a_rows - 1) >> 4;
   const char* aptr[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    int row = m0 + mt * 16 + (lane % 16);
-    if (row >= a.a_rows) row = a.a_rows - 1;
-    aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + (lane / 16) * 8) * AB;
+    int grp = (m0 >> 4) + mt;
+    if (grp > max_group) grp = max_group;
+    aptr[mt] = (const char*)a.A + ((size_t)grp * a.lda + lane * 8) * AB;
   }
   f32x4 acc[MT][NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int kt = kb;
-  for (; kt + U <= ke; kt += U) {
+  // groups of U k tiles; the last group's loads are clamped to ke-1 and its extra MFMAs
+  // skipped, so the tail costs no additional round trip
+  for (int kt = kb; kt < ke; kt += U) {
     Frag<T> bf[U][NT];
     AFrag<T, AF32> af[U][MT];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      const int k = kt + u < ke ? kt + u : ke - 1;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)(kt + u) * 512);
+      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)(kt + u) * kTileK * AB);
+      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * 512 * AB);
     }
     __builtin_amdgcn_sched_barrier(0);   // keep all U tiles' loads in flight before the MFMAs
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      if (kt + u < ke) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) af[u][mt].mma_into(acc[mt][nt], bf[u][nt]);
-  }
-  for (; kt < ke; ++kt) {
-    Frag<T> bf[NT];
-    AFrag<T, AF32> af[MT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) bf[nt].load(bptr[nt] + (size_t)kt * 512);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) af[mt].load(aptr[mt] + (size_t)kt * kTileK * AB);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) af[mt].mma_into(acc[mt][nt], bf[nt]);
+          for (int nt = 0; nt < NT; ++nt) af[u][mt].mma_into(acc[mt][nt], bf[u][nt]);
+      }
+    }
   }
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -244,12 +238,13 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
     const int ntg = (n0 + wn * NT * 16) / kTileN + nt;
     bptr[nt] = (const T*)a.B + ((size_t)(ntg < n_tiles_valid ? ntg : 0) * KT) * 512 + lane * 8;
   }
+  const int max_group = (a.a_rows - 1) >> 4;
   const char* aptr[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    int row = m0 + wm * MT * 16 + mt * 16 + (lane % 16);
-    if (row >= a.a_rows) row = a.a_rows - 1;
-    aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + (lane / 16) * 8) * AB;
+    int grp = ((m0 + wm * MT * 16) >> 4) + mt;
+    if (grp > max_group) grp = max_group;
+    aptr[mt] = (const char*)a.A + ((size_t)grp * a.lda + lane * 8) * AB;
   }
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -265,7 +260,7 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * kTileK * AB);
+      for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * 512 * AB);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -441,13 +436,10 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int KT = a.Kp / kTileK;
   const int n_tiles16 = a.N / kTileN;
-  const char* aptr[MT];
+  const int max_group = (a.a_rows - 1) >> 4;
+  const T* aptr[MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    int row = mt * 16 + c16;
-    if (row >= a.a_rows) row = a.a_rows - 1;
-    aptr[mt] = (const char*)a.A + ((size_t)row * a.lda + g4 * 8) * Elem<T>::kBytes;
-  }
+  for (int mt = 0; mt < MT; ++mt) aptr[mt] = (const T*)a.A + (size_t)(mt < max_group ? mt : max_group) * a.lda + lane * 8;
   uint64_t best[MT][4];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -473,7 +465,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
         bf[u][0].load(bptr[0] + (size_t)(kt + u) * 512);
         bf[u][1].load(bptr[1] + (size_t)(kt + u) * 512);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) af[u][mt].load((const T*)(aptr[mt]) + (size_t)(kt + u) * kTileK);
+        for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)(kt + u) * 512);
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -489,7 +481,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
       b0.load(bptr[0] + (size_t)kt * 512);
       b1.load(bptr[1] + (size_t)kt * 512);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) af[mt].load((const T*)(aptr[mt]) + (size_t)kt * kTileK);
+      for (int mt = 0; mt < MT; ++mt) af[mt].load(aptr[mt] + (size_t)kt * 512);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         mma(acc[mt][0], af[mt], b0);

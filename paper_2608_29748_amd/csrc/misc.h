@@ -18,9 +18,10 @@ enum StateField : int {
   kStateFields
 };
 
+// out: packed GEMM-operand layout with group stride ldg; keep: optional row-major copy.
 template <typename T, typename K>
-void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldo,
-             K* keep, int ldk, uint64_t* zero_keys, int nzero, hipStream_t s);
+void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
+             K* keep, int ldk, hipStream_t s);
 template <typename T>
 void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s);
 // Drafter input without conditioning: row (s, 0) = E[anchor], rows (s, j>0) = E[mask].
@@ -32,10 +33,11 @@ void embed_block(const T* embed, int d, const int32_t* state, int mask_token, in
 template <typename T>
 void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* dkeys, int forced,
                   int32_t* dtok, int n_seqs, int bk, float* x, int ldx, hipStream_t s);
-// Conditioning gather (Eq.5/6): mu = [m | u] rows, er[:, :d] = e rows.
+// Conditioning gather (Eq.5/6): mu = [m | u] rows, er[:, :d] = e rows (both packed fp32,
+// group stride ldg).
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
-               int n_seqs, int bk, float* mu, float* er, hipStream_t s);
+               int n_seqs, int bk, float* mu, float* er, int ldg, hipStream_t s);
 void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs,
             int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
 void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s);

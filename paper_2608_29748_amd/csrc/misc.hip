@@ -7,41 +7,63 @@ template <typename K> struct KeepT;
 template <> struct KeepT<uint16_t> { __device__ static uint16_t of(float v) { return f32_to_f16(v); } };
 template <> struct KeepT<float> { __device__ static float of(float v) { return v; } };
 
+// One workgroup per row, single pass: each thread keeps its 8-element chunks of the row
+// in registers (hidden <= 8192), and writes the normalised row in the packed GEMM-operand
+// layout (one 8-element run per chunk) plus an optional row-major retained copy.
 template <typename T, typename K>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
                                                       const T* __restrict__ w, int d, float eps,
-                                                      T* __restrict__ out, int ldo, K* keep, int ldk,
-                                                      uint64_t* zero_keys, int nzero) {
+                                                      T* __restrict__ out, int ldg, K* keep, int ldk) {
   __shared__ float red[4];
   const int row = blockIdx.x;
   const float* xr = x + (size_t)row * ldx;
+  const int nch = d / 8;
+  float v[4][8];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) { const float v = xr[i]; ss += v * v; }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = threadIdx.x + j * 256;
+    if (c < nch) {
+      const float4 a = *reinterpret_cast<const float4*>(xr + 8 * c);
+      const float4 b = *reinterpret_cast<const float4*>(xr + 8 * c + 4);
+      v[j][0] = a.x; v[j][1] = a.y; v[j][2] = a.z; v[j][3] = a.w;
+      v[j][4] = b.x; v[j][5] = b.y; v[j][6] = b.z; v[j][7] = b.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[j][e] * v[j][e];
+    }
+  }
   ss = warp_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) {
-    const float v = xr[i] * inv * Elem<T>::to_f32(w[i]);
-    out[(size_t)row * ldo + i] = Elem<T>::from_f32(v);
-    if (keep) keep[(size_t)row * ldk + i] = KeepT<K>::of(v);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = threadIdx.x + j * 256;
+    if (c < nch) {
+      Frag<T> f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float y = v[j][e] * inv * Elem<T>::to_f32(w[8 * c + e]);
+        f.set(e, y);
+        if (keep) keep[(size_t)row * ldk + 8 * c + e] = KeepT<K>::of(y);
+      }
+      f.store(out + pa_index(row, 8 * c, (size_t)ldg));
+    }
   }
-  if (zero_keys && row == 0)
-    for (int i = threadIdx.x; i < nzero; i += 256) zero_keys[i] = 0ull;
 }
 
 template <typename T, typename K>
-void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldo,
-             K* keep, int ldk, uint64_t* zero_keys, int nzero, hipStream_t s) {
+void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
+             K* keep, int ldk, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldo,
-                     keep, ldk, zero_keys, nzero);
+  hipLaunchKernelGGL((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg,
+                     keep, ldk);
 }
 template void rmsnorm<bf16_t, uint16_t>(const float*, int, const bf16_t*, int, float, int, bf16_t*, int,
-                                        uint16_t*, int, uint64_t*, int, hipStream_t);
+                                        uint16_t*, int, hipStream_t);
 template void rmsnorm<float, float>(const float*, int, const float*, int, float, int, float*, int,
-                                    float*, int, uint64_t*, int, hipStream_t);
+                                    float*, int, hipStream_t);
 
 // ------------------------------------------------------------------ embeddings
 template <typename T>
@@ -105,7 +127,7 @@ template <> struct KeepRead<float> { __device__ static float of(float v) { retur
 template <typename T, typename K>
 __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st, int mask,
                                  const K* __restrict__ hD, const K* __restrict__ hT, int bk,
-                                 float* __restrict__ mu, float* __restrict__ er) {
+                                 float* __restrict__ mu, float* __restrict__ er, int ldg) {
   const int row = blockIdx.x, sq = row / bk, j = row % bk;
   const int r = st[sq * kStateFields + ST_R], cl = st[sq * kStateFields + ST_COND_LEN];
   const bool cond = j >= 1 && j <= cl;
@@ -113,19 +135,17 @@ __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* 
   const K* pu = hT + ((size_t)sq * bk + (cond ? r + j - 1 : 0)) * d;
   const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
   const T* pe = E + (size_t)tok * d;
-  float* mrow = mu + (size_t)row * 2 * d;
-  float* erow = er + (size_t)row * 2 * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    mrow[i] = cond ? KeepRead<K>::of(pm[i]) : 0.f;
-    mrow[d + i] = cond ? KeepRead<K>::of(pu[i]) : 0.f;
-    erow[i] = Elem<T>::to_f32(pe[i]);
+    mu[pa_index(row, i, ldg)] = cond ? KeepRead<K>::of(pm[i]) : 0.f;
+    mu[pa_index(row, d + i, ldg)] = cond ? KeepRead<K>::of(pu[i]) : 0.f;
+    er[pa_index(row, i, ldg)] = Elem<T>::to_f32(pe[i]);
   }
 }
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
-               int n_seqs, int bk, float* mu, float* er, hipStream_t s) {
+               int n_seqs, int bk, float* mu, float* er, int ldg, hipStream_t s) {
   hipLaunchKernelGGL((cond_prep_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
-                     mask_token, hD, hT, bk, mu, er);
+                     mask_token, hD, hT, bk, mu, er, ldg);
 }
 
 // ------------------------------------------------------------------ acceptance / rollback
@@ -228,8 +248,8 @@ template void embed_verify<bf16_t>(const bf16_t*, int, const int32_t*, const uin
 template void embed_verify<float>(const float*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
                                   int, float*, int, hipStream_t);
 template void cond_prep<bf16_t, uint16_t>(const bf16_t*, int, const int32_t*, int, const uint16_t*,
-                                          const uint16_t*, int, int, float*, float*, hipStream_t);
+                                          const uint16_t*, int, int, float*, float*, int, hipStream_t);
 template void cond_prep<float, float>(const float*, int, const int32_t*, int, const float*, const float*, int,
-                                      int, float*, float*, hipStream_t);
+                                      int, float*, float*, int, hipStream_t);
 
 }  // namespace rt

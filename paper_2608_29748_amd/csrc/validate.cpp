@@ -34,7 +34,8 @@ int validate_config(const rt_config* c) {
   if (!c) return fail(RT_ERR_INVALID, "config is null");
   if (c->dtype != RT_F32 && c->dtype != RT_BF16) return fail(RT_ERR_INVALID, "dtype must be RT_F32 or RT_BF16");
   if (c->vocab < 16 || c->vocab % 16) return fail(RT_ERR_INVALID, "vocab must be a positive multiple of 16");
-  if (c->hidden < 32 || c->hidden % 32) return fail(RT_ERR_INVALID, "hidden must be a positive multiple of 32");
+  if (c->hidden < 32 || c->hidden % 32 || c->hidden > 8192)
+    return fail(RT_ERR_INVALID, "hidden must be a multiple of 32 in [32, 8192]");
   if (c->n_layers < 1) return fail(RT_ERR_INVALID, "n_layers must be >= 1");
   if (c->head_dim != 64 && c->head_dim != 128) return fail(RT_ERR_INVALID, "head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
@@ -152,10 +153,11 @@ int make_plan(const rt_config* c, Plan* p) {
   q.g = take(M * q.Kp_nc * e);
   q.fcout = take(M * q.d * 4);
   q.fa = take(M * q.Kp_d * e);
+  const size_t Rp = rup(q.R, 32);
   q.etilde = take((size_t)q.R * q.d * 4);
-  q.mu = take((size_t)q.R * 2 * q.d * 4 + 64);
-  q.er = take((size_t)q.R * 2 * q.d * 4 + 64);
-  q.gate = take((size_t)q.R * q.d * 4);
+  q.mu = take(Rp * q.Kp_2d * 4);
+  q.er = take(Rp * q.Kp_2d * 4);
+  q.gate = take(Rp * q.d * 4);
   q.hd_keep = take((size_t)q.R * q.d * q.ksz);
   q.ht_keep = take((size_t)q.R * q.d * q.ksz);
   q.dlogits = take((size_t)q.R * q.V * 4);
