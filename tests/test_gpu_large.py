@@ -1,0 +1,67 @@
+"""GPU parity at the measured model shapes.
+
+Qwen3-0.6B shape: full oracle prefill and teacher-forced rounds.  Qwen3-4B shape:
+the oracle cannot prefill 4096 tokens in test time, so the GPU's prefill is checked
+on a causal prefix (KV rows of the first tokens depend on nothing later) and the
+rounds start the oracle from the GPU's KV caches and carried state."""
+import time
+
+import numpy as np
+import pytest
+
+from oracle import OracleModel, OracleRunner, Precision
+from workloads import get, make_prompts, make_weights
+
+from gpu_parity import compare_prefill, engine_for, log, run_teacher_forced
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def test_qwen3_06b_shape_prefill_and_rounds():
+    wl = get("qwen3-0.6b-shape")
+    t0 = time.time()
+    W = make_weights(wl)
+    prompts = make_prompts(wl)
+    eng = engine_for(wl, W)
+    first = eng.prefill(prompts, wl.new_tokens)
+    log(f"[0.6b] gpu ready {time.time() - t0:.1f}s")
+    R = OracleRunner(OracleModel(wl, W))
+    states = [R.prefill(p, wl.new_tokens) for p in prompts]
+    log(f"[0.6b] oracle prefill done {time.time() - t0:.1f}s")
+    RX = OracleRunner(OracleModel(wl, W, prec=Precision.for_dtype("f64")))
+    exact = [RX.prefill(p, wl.new_tokens) for p in prompts]
+    rep = compare_prefill(eng, R, wl, prompts, states, TOL, layers=[0, 1, 13, 27], exact_states=exact)
+    log(f"[0.6b] prefill max err {rep.max_err}")
+    RX.m.W = R.m.W
+    rep = run_teacher_forced(eng, R, wl, states, 3, TOL, exact=RX)
+    log(f"[0.6b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    eng.close()
+
+
+def test_qwen3_4b_shape_prefix_and_injected_rounds():
+    wl = get("qwen3-4b-shape")
+    t0 = time.time()
+    W = make_weights(wl)
+    prompts = make_prompts(wl)
+    eng = engine_for(wl, W)
+    eng.prefill(prompts, wl.new_tokens)
+    log(f"[4b] gpu prefill done {time.time() - t0:.1f}s")
+    R = OracleRunner(OracleModel(wl, W))
+    n = 48
+    pre = R.prefill(prompts[0][:n], wl.new_tokens)
+    pre.prompt = prompts[0][:n]
+    log(f"[4b] oracle prefix prefill done {time.time() - t0:.1f}s")
+    RX = OracleRunner(OracleModel(wl, W, prec=Precision.for_dtype("f64")))
+    pre_x = RX.prefill(prompts[0][:n], wl.new_tokens)
+    rep = compare_prefill(eng, R, wl, [prompts[0][:n]], [pre], TOL, layers=[0, 1, 17, 35], exact_states=[pre_x])
+    log(f"[4b] prefix KV max err {rep.max_err}")
+    st = R.m.new_state(prompts[0], wl.new_tokens)
+    stv = eng.read(7, 0, (8,), np.int32)
+    st.P, st.anchor, st.generated = int(stv[0]), int(stv[1]), [int(stv[1])]
+    st.hD_prev = np.zeros((wl.block_size, wl.target.hidden))
+    st.hT_prev = np.zeros((wl.block_size, wl.target.hidden))
+    RX.m.W = R.m.W                                   # share the float64 weight cache
+    rep = run_teacher_forced(eng, R, wl, [st], 2, TOL, inject_kv=True, exact=RX)
+    log(f"[4b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    eng.close()
