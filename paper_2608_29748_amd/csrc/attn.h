@@ -29,5 +29,7 @@ constexpr int kAttnRows = 64;
 template <typename T>
 hipError_t attention(const AttnArgs& a, hipStream_t s);
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim);
+// Smallest split count for which one split's page ids fit the kernel's table.
+int attn_min_splits(int max_keys);
 
 }  // namespace rt

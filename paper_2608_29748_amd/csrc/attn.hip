@@ -9,25 +9,34 @@
 
 namespace rt {
 
-constexpr int kChunk = 32;      // keys per LDS chunk (two pages)
+constexpr int kChunk = 64;      // keys per LDS chunk (four pages)
+constexpr int kMaxSplitPages = 1024;   // page ids of one split held in LDS (16384 keys)
 
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim) {
   return (size_t)n_seqs * n_kv_heads * row_blocks * splits * kAttnRows * head_dim;
 }
+int attn_min_splits(int max_keys) { return (max_keys + kMaxSplitPages * kPage - 1) / (kMaxSplitPages * kPage); }
 
+// Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
+// keys 4*(lane/16)+i of one query (column lane%16), so the softmax is a per-lane
+// reduction plus two cross-lane steps, and the probabilities feed O^T = V^T P^T as the
+// B operand straight from registers (no LDS transpose).  In each 32-key MFMA step a
+// lane supplies keys {4g..4g+3} and {16+4g..16+4g+3} of the step (g = lane/16); the
+// V^T fragment from LDS uses the same key order.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int EB = Elem<T>::kBytes;
   constexpr int KPAD = HD + 16 / EB;       // LDS row pitch (elements) for K
-  constexpr int VPAD = kChunk + 16 / EB;   // LDS row pitch for V^T and P
+  constexpr int VPAD = kChunk + 16 / EB;   // LDS row pitch for V^T
   constexpr int NHT = HD / 16;             // output hd tiles
   constexpr int NKS = HD / 32;             // k-steps over hd for S
+  constexpr int NSUB = kChunk / 16;        // 16-key score tiles per chunk
+  constexpr int PAGES = kChunk / kPage;
   __shared__ __attribute__((aligned(16))) T sK[kChunk][KPAD];
   __shared__ __attribute__((aligned(16))) T sV[HD][VPAD];
-  __shared__ __attribute__((aligned(16))) T sP[4][16][VPAD];
+  __shared__ int sPage[kMaxSplitPages];
   // bf16: probabilities enter P V as hi + lo bf16 parts (~16 significand bits)
   constexpr bool kSplitP = sizeof(T) == 2;
-  __shared__ __attribute__((aligned(16))) T sPl[kSplitP ? 4 : 1][16][VPAD];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g4 = lane / 16, c16 = lane % 16;
   const int split = blockIdx.x, kvh = blockIdx.y;
@@ -43,33 +52,30 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
   const int cps = (nchunks + a.splits - 1) / a.splits;
   const int c_beg = split * cps, c_end = min(nchunks, c_beg + cps);
+  // page ids of this split's keys (pages past kv_end are never dereferenced)
+  const int pg_beg = c_beg * PAGES;
+  const int npg = max(0, min((kv_end + kPage - 1) / kPage, c_end * PAGES) - pg_beg);
+  for (int i = threadIdx.x; i < npg && i < kMaxSplitPages; i += 256)
+    sPage[i] = a.page_table[(size_t)s * a.max_pages + pg_beg + i];
 
-  // This wave's 16 rows: row = row0 + w*16 + (lane%16) for A fragments;
-  // accumulator rows are row0 + w*16 + 4*g4 + i.
-  const int arow = row0 + w * 16 + c16;
+  // This lane's query: row = row0 + w*16 + lane%16 (all four lanes groups share it).
+  const int qrow = row0 + w * 16 + c16;
+  const bool qvalid = qrow < nrows;
+  const int qpos = P + (qvalid ? qrow / G : 0);
   Frag<T> qf[NKS];
   {
-    const int r = min(arow, nrows - 1);
+    const int r = min(qrow, nrows - 1);
     const int tok = r / G, h = kvh * G + r % G;
     const T* qp = (const T*)a.q + (size_t)(s * a.rows_per_seq + tok) * a.n_q_heads * HD + (size_t)h * HD;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks].load(qp + ks * 32 + g4 * 8);
   }
-  int qpos[4];
-  bool rvalid[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = row0 + w * 16 + 4 * g4 + i;
-    rvalid[i] = r < nrows;
-    qpos[i] = P + (rvalid[i] ? r / G : 0);
-  }
   const float sl2 = a.scale * 1.4426950408889634f;
-  float mrun[4], lrun[4];
-  f32x4 o[NHT];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { mrun[i] = -INFINITY; lrun[i] = 0.f; }
+  float mrun = -INFINITY, lrun = 0.f;
+  f32x4 o[NHT];                                   // O^T tiles: lane holds hd 16t+4g..+4 of its query
 #pragma unroll
   for (int t = 0; t < NHT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();   // sPage ready
 
   const size_t head_page = (size_t)kPage * HD;   // elements of one (page, head) slice
   // Each thread stages NP 16-byte pieces of a chunk (K pieces first, then V^T pieces);
@@ -79,16 +85,21 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   uint4 pf[NP];
   auto fetch = [&](int c) {
     const int key0 = c * kChunk;
+    int pid[PAGES];
+#pragma unroll
+    for (int q = 0; q < PAGES; ++q)
+      pid[q] = (c < c_end && key0 + q * kPage < kv_end) ? sPage[(c - c_beg) * PAGES + q] : -1;
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
       const int p = threadIdx.x + j * 256;
       const bool isv = p >= KV16;
       const int e0 = (isv ? p - KV16 : p) * (16 / EB);
       const int pg = e0 / (int)head_page, within = e0 % (int)head_page;
-      const int tok0 = key0 + pg * kPage;
+      int page = pid[0];
+#pragma unroll
+      for (int q = 1; q < PAGES; ++q) page = pg == q ? pid[q] : page;
       pf[j] = make_uint4(0, 0, 0, 0);
-      if (c < c_end && tok0 < kv_end) {
-        const int page = a.page_table[(size_t)s * a.max_pages + tok0 / kPage];
+      if (page >= 0) {
         const T* src = (const T*)(isv ? a.vcache : a.kcache) + ((size_t)page * a.n_kv_heads + kvh) * head_page + within;
         pf[j] = *reinterpret_cast<const uint4*>(src);
       }
@@ -112,97 +123,113 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     stage();
     __syncthreads();
     fetch(c + 1);
-    // S = Q K^T for two 16-key subtiles
-    f32x4 sacc[2];
+    // S^T = K Q^T, NSUB 16-key tiles
+    f32x4 st[NSUB];
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      sacc[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int sub = 0; sub < NSUB; ++sub) {
+      st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         Frag<T> kf;
         kf.load(&sK[sub * 16 + c16][ks * 32 + g4 * 8]);
-        mma(sacc[sub], qf[ks], kf);
+        mma(st[sub], kf, qf[ks]);
       }
     }
-    // mask, online softmax
-    float p[2][4], alpha[4];
+    // scale, mask (only chunks that reach the causal edge or kv_end), online softmax
+    float mx = -INFINITY;
+    if (key0 + kChunk <= P && key0 + kChunk <= kv_end) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float mx = -INFINITY;
+      for (int sub = 0; sub < NSUB; ++sub)
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        const int kp = key0 + sub * 16 + c16;
-        const bool vis = rvalid[i] && kp < kv_end && (!a.causal || kp <= qpos[i]);
-        const float v = vis ? sacc[sub][i] * sl2 : -INFINITY;
-        p[sub][i] = v;
-        mx = fmaxf(mx, v);
-      }
-      for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-      const float mnew = fmaxf(mrun[i], mx);
-      if (mnew == -INFINITY) {
-        alpha[i] = 1.f;
-        p[0][i] = 0.f; p[1][i] = 0.f;
-      } else {
-        alpha[i] = exp2f(mrun[i] - mnew);
-        p[0][i] = exp2f(p[0][i] - mnew);
-        p[1][i] = exp2f(p[1][i] - mnew);
-      }
-      float rs = p[0][i] + p[1][i];
-      for (int off = 8; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 64);
-      lrun[i] = lrun[i] * alpha[i] + rs;
-      mrun[i] = mnew;
+        for (int i = 0; i < 4; ++i) {
+          st[sub][i] *= sl2;
+          mx = fmaxf(mx, st[sub][i]);
+        }
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kp = key0 + sub * 16 + 4 * g4 + i;
+          const bool vis = kp < kv_end && (!a.causal || kp <= qpos);
+          st[sub][i] = vis ? st[sub][i] * sl2 : -INFINITY;
+          mx = fmaxf(mx, st[sub][i]);
+        }
     }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mnew = fmaxf(mrun, mx);
+    float alpha = 1.f, rs = 0.f;
+    if (mnew != -INFINITY) {
+      alpha = __builtin_amdgcn_exp2f(mrun - mnew);
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          st[sub][i] = __builtin_amdgcn_exp2f(st[sub][i] - mnew);
+          rs += st[sub][i];
+        }
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st[sub][i] = 0.f;
+    }
+    rs += __shfl_xor(rs, 16, 64);
+    rs += __shfl_xor(rs, 32, 64);
+    lrun = lrun * alpha + rs;
+    mrun = mnew;
 #pragma unroll
     for (int t = 0; t < NHT; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o[t][i] *= alpha[i];
-    // P: accumulator layout -> A-operand layout through this wave's LDS slot
+      for (int i = 0; i < 4; ++i) o[t][i] *= alpha;
+    // O^T += V^T P^T, 32 keys per step: B (P^T) from registers, A (V^T) from LDS
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
+    for (int kk = 0; kk < kChunk / 32; ++kk) {
+      Frag<T> ph, pl;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const T hi = Elem<T>::from_f32(p[sub][i]);
-        sP[w][4 * g4 + i][sub * 16 + c16] = hi;
-        if constexpr (kSplitP)
-          sPl[w][4 * g4 + i][sub * 16 + c16] = Elem<T>::from_f32(p[sub][i] - Elem<T>::to_f32(hi));
+        const float x0 = st[2 * kk][i], x1 = st[2 * kk + 1][i];
+        ph.set(i, x0);
+        ph.set(4 + i, x1);
+        if constexpr (kSplitP) {
+          pl.set(i, x0 - ph.get(i));
+          pl.set(4 + i, x1 - ph.get(4 + i));
+        }
       }
-    __syncthreads();
-    Frag<T> pf, pfl;
-    pf.load(&sP[w][c16][g4 * 8]);
-    if constexpr (kSplitP) pfl.load(&sPl[w][c16][g4 * 8]);
 #pragma unroll
-    for (int t = 0; t < NHT; ++t) {
-      Frag<T> vf;
-      vf.load(&sV[t * 16 + c16][g4 * 8]);
-      mma(o[t], pf, vf);
-      if constexpr (kSplitP) mma(o[t], pfl, vf);
+      for (int t = 0; t < NHT; ++t) {
+        Frag<T> vf;
+        const T* vrow = &sV[t * 16 + c16][kk * 32];
+        vf.load_halves(vrow + 4 * g4, vrow + 16 + 4 * g4);
+        mma(o[t], vf, ph);
+        if constexpr (kSplitP) mma(o[t], vf, pl);
+      }
     }
   }
 
-  // write result (single split) or partials
+  // write result (single split) or partials; lane holds hd 16t+4g4+i of query qrow
   if (a.splits == 1) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = row0 + w * 16 + 4 * g4 + i;
-      if (r >= nrows) continue;
-      const int tok = r / G, h = kvh * G + r % G;
-      const float inv = lrun[i] > 0.f ? 1.f / lrun[i] : 0.f;
+    if (qvalid) {
+      const int tok = qrow / G, h = kvh * G + qrow % G;
+      const float inv = lrun > 0.f ? 1.f / lrun : 0.f;
       T* op = (T*)a.out;
       const int orow = s * a.rows_per_seq + tok;
 #pragma unroll
-      for (int t = 0; t < NHT; ++t) op[pa_index(orow, h * HD + t * 16 + c16, a.ldo)] = Elem<T>::from_f32(o[t][i] * inv);
+      for (int t = 0; t < NHT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          op[pa_index(orow, h * HD + t * 16 + 4 * g4 + i, a.ldo)] = Elem<T>::from_f32(o[t][i] * inv);
     }
   } else {
     const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
     float* op = a.opart + blk * kAttnRows * HD;
     float* ml = a.mlpart + blk * kAttnRows * 2;
+    const int rl = w * 16 + c16;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int rl = w * 16 + 4 * g4 + i;
-#pragma unroll
-      for (int t = 0; t < NHT; ++t) op[(size_t)rl * HD + t * 16 + c16] = o[t][i];
-      if (c16 == 0) { ml[rl * 2] = mrun[i]; ml[rl * 2 + 1] = lrun[i]; }
-    }
+    for (int t = 0; t < NHT; ++t)
+      *reinterpret_cast<float4*>(op + (size_t)rl * HD + t * 16 + 4 * g4) = make_float4(o[t][0], o[t][1], o[t][2], o[t][3]);
+    if (g4 == 0) { ml[rl * 2] = mrun; ml[rl * 2 + 1] = lrun; }
   }
 }
 

@@ -51,6 +51,12 @@ template <> struct Frag<bf16_t> {
   __device__ __forceinline__ void zero() { for (int i = 0; i < 8; ++i) v[i] = 0; }
   __device__ __forceinline__ float get(int i) const { return bf16_to_f32((bf16_t)v[i]); }
   __device__ __forceinline__ void set(int i, float f) { v[i] = (short)f32_to_bf16(f); }
+  // elements 0..3 from p0[0..3] and 4..7 from p1[0..3] (8-byte aligned)
+  __device__ __forceinline__ void load_halves(const bf16_t* p0, const bf16_t* p1) {
+    const uint2 a = *reinterpret_cast<const uint2*>(p0), b = *reinterpret_cast<const uint2*>(p1);
+    v[0] = (short)(a.x & 0xffff); v[1] = (short)(a.x >> 16); v[2] = (short)(a.y & 0xffff); v[3] = (short)(a.y >> 16);
+    v[4] = (short)(b.x & 0xffff); v[5] = (short)(b.x >> 16); v[6] = (short)(b.y & 0xffff); v[7] = (short)(b.y >> 16);
+  }
 };
 template <> struct Frag<float> {
   float4 lo, hi;
@@ -69,6 +75,10 @@ template <> struct Frag<float> {
     switch (i) { case 0: lo.x = f; break; case 1: lo.y = f; break; case 2: lo.z = f; break;
                  case 3: lo.w = f; break; case 4: hi.x = f; break; case 5: hi.y = f; break;
                  case 6: hi.z = f; break; default: hi.w = f; }
+  }
+  __device__ __forceinline__ void load_halves(const float* p0, const float* p1) {
+    lo = *reinterpret_cast<const float4*>(p0);
+    hi = *reinterpret_cast<const float4*>(p1);
   }
 };
 
@@ -104,6 +114,27 @@ __device__ __forceinline__ float warp_max(float v, int width = 64) {
 // 512 contiguous elements (lane l reads elements l*8 .. l*8+7).
 __host__ __device__ __forceinline__ size_t pa_index(int m, int k, size_t ldg) {
   return (size_t)(m >> 4) * ldg + (size_t)(k >> 5) * 512 + (size_t)((((m & 15) + 16 * ((k & 31) >> 3)) << 3) + (k & 7));
+}
+
+// Reductions over the 16 lanes of a DPP row (lanes 16r..16r+15), by row rotations:
+// every lane of the row ends with the result.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0x128>(v));   // row_ror:8
+  v = fmaxf(v, dpp<0x124>(v));   // row_ror:4
+  v = fmaxf(v, dpp<0x122>(v));   // row_ror:2
+  v = fmaxf(v, dpp<0x121>(v));   // row_ror:1
+  return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0x128>(v);
+  v += dpp<0x124>(v);
+  v += dpp<0x122>(v);
+  v += dpp<0x121>(v);
+  return v;
 }
 
 // Monotone map float -> uint32 (larger float -> larger key).

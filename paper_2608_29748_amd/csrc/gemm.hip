@@ -326,7 +326,7 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
 }
 
 int gemm_tile_rows(int shape, int M) { return shape == SHAPE_SKINNY ? (M > 16 ? 32 : 16) : 128; }
-int gemm_tile_cols(int shape, int) { return shape == SHAPE_SKINNY ? 16 : 128; }
+int gemm_tile_cols(int shape, int N) { return shape == SHAPE_SKINNY ? (N >= 5120 ? 32 : 16) : 128; }
 
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
@@ -338,6 +338,10 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
     if (a_f32) {
       if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
       else hipLaunchKernelGGL((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
+    } else if (N >= 5120) {        // 32-column tiles: half the activation re-reads, >= 160 workgroups
+      dim3 g2((N + 31) / 32, 1, 1);
+      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, false, 2, 2, 8, 8>), g2, dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((gemm16_kernel<T, false, 1, 2, 8, 8>), g2, dim3(512), 0, s, a);
     } else {
       if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, false, 2, 1, 8, 8>), grid, dim3(512), 0, s, a);
       else hipLaunchKernelGGL((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);
