@@ -7,7 +7,7 @@ graph with all inputs (weights, prompts' KV caches, carried state) resident in
 HBM.  `value` is committed tokens per second over exactly `--steps` rounds after
 `--warmup` rounds.  A profiled phase then times every kernel launch with HIP
 events on the library's stream to give the per-stage breakdown and the roofline
-of the dominant kernel (the weight-streaming MFMA GEMM).  The CPU baseline is the
+of the dominant kernel (the fused gate|up projection GEMM).  The CPU baseline is the
 float64 oracle, started from the GPU's state, timed on this host.
 
 Random-initialised weights and uniform-random prompts of the workload's shapes
@@ -42,6 +42,53 @@ def build_engine(wl, W):
                       block_size=wl.block_size, mask_token_id=wl.mask_token_id, max_batch=wl.batch,
                       max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps, beta=wl.beta)
     return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
+
+
+DOMINANT = "gemm_gate_up"
+REPLAY_KINDS = (0, 1, 2, 3, 4, 5, 6, 7, 10)   # GEMM classes, attention, merge, LM head
+DOMINANT_DESC = ("gemm_gate_up: fused gate|up projection GEMM with SwiGLU epilogue "
+                 "(gemm16_kernel, bf16 MFMA, 16 rows x 19456 columns x K 2560 at the Qwen3-4B shape)")
+GEMM_SOURCES = ("paper_2608_29748_amd/csrc/gemm.hip", "paper_2608_29748_amd/csrc/gemm.h",
+                "paper_2608_29748_amd/csrc/common.h")
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter summary
+    (rocprofv3 FETCH_SIZE and WRITE_SIZE passes, each scaled by the same counter's
+    reading for a plain copy of known size); None when that summary was taken on
+    different kernel sources or is absent."""
+    path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("traffic-json:"):
+                rec = json.loads(line.split(":", 1)[1])
+    if not rec or rec.get("source_sha256") != gemm_source_hash():
+        return None
+    return rec["bytes_per_launch"]
+
+
+def copy_calibration(nbytes: int = 1 << 30):
+    """A plain device-to-device copy of known size, for scaling the HBM byte counters."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 copies of {nbytes} bytes")
 
 
 def cpu_baseline(eng, wl, W, prompts, seconds: float):
@@ -99,8 +146,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3-4b-shape")
     ap.add_argument("--profile-rounds", type=int, default=5)
+    ap.add_argument("--replay-reps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run plain 1 GiB copies (reference reading for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
@@ -143,7 +193,9 @@ def main():
     value = committed / elapsed
     log(f"timed {args.steps} rounds: {elapsed * 1e3 / args.steps:.3f} ms/round, {value:.1f} tokens/s")
 
-    # profiled rounds: HIP events around every launch on the library's stream
+    # profiled rounds: a HIP-event pair on every launch (per-stage breakdown; a launch's
+    # pair also spans its dispatch, so these times exceed the kernels' execution times)
+    from paper_2608_29748_amd import binding as B
     kinds, stages = {}, []
     for _ in range(args.profile_rounds):
         stats, st_ms, tok, n, a = eng.profile_round()
@@ -152,18 +204,34 @@ def main():
             k = kinds.setdefault(s["kind"], {"launches": 0, "ms": 0.0, "bytes": 0.0, "flops": 0.0})
             for f in ("launches", "ms", "bytes", "flops"):
                 k[f] += s[f]
-    from paper_2608_29748_amd.binding import STAGE_NAMES
-    stage_med = {n: float(np.median([s[i] for s in stages])) for i, n in enumerate(STAGE_NAMES)}
-    dom = kinds["gemm_skinny"]
-    per_launch_bytes = dom["bytes"] / max(dom["launches"], 1)
-    per_launch_ms = dom["ms"] / max(dom["launches"], 1)
-    achieved = per_launch_bytes / (per_launch_ms * 1e-3) / 1e9
-    kernels = {k: {"launches_per_round": v["launches"] / args.profile_rounds,
-                   "ms_per_round": v["ms"] / args.profile_rounds,
-                   "GB_per_round": v["bytes"] / args.profile_rounds / 1e9,
-                   "achieved_GBs": (v["bytes"] / (v["ms"] * 1e-3) / 1e9) if v["ms"] > 0 else None,
-                   "achieved_TFLOPs": (v["flops"] / (v["ms"] * 1e-3) / 1e12) if v["ms"] > 0 else None}
-               for k, v in kinds.items() if v["launches"]}
+    stage_med = {n: float(np.median([s[i] for s in stages])) for i, n in enumerate(B.STAGE_NAMES)}
+    # kernel replay: each replayable class's launches of one round, back to back in a HIP
+    # graph between two HIP events on the library's stream (their execution time)
+    replay = {}
+    for kind in REPLAY_KINDS:
+        r = eng.time_kernel(kind, args.replay_reps)
+        if r["launches"]:
+            replay[r["kind"]] = r
+    kernels = {}
+    for name, v in kinds.items():
+        if not v["launches"]:
+            continue
+        per_round = v["launches"] / args.profile_rounds
+        rec = {"launches_per_round": per_round, "GB_per_launch": v["bytes"] / v["launches"] / 1e9,
+               "us_per_launch_profiled_round": v["ms"] * 1e3 / v["launches"]}
+        if name in replay:
+            r = replay[name]
+            us = r["ms"] * 1e3 / r["launches"]
+            rec["us_per_launch"] = us
+            rec["achieved_GBs"] = r["bytes"] / r["launches"] / (us * 1e-6) / 1e9
+            rec["achieved_TFLOPs"] = r["flops"] / r["launches"] / (us * 1e-6) / 1e12
+        kernels[name] = rec
+    dom = replay[DOMINANT]
+    per_launch_bytes = dom["bytes"] / dom["launches"]
+    per_launch_us = dom["ms"] * 1e3 / dom["launches"]
+    achieved = per_launch_bytes / (per_launch_us * 1e-6) / 1e9
+    if args.copy_calibration:
+        copy_calibration()
 
     out = {
         "metric": "committed tokens/s/GPU, Qwen3-4B shape b=1; verify-pass % MFMA/HBM roofline",
@@ -182,10 +250,13 @@ def main():
                    "block_size": wl.block_size, "new_tokens": wl.new_tokens, "hidden": wl.target.hidden,
                    "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
                    "cond_layers": list(wl.cond_layers), "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "gemm_skinny (weight-streaming bf16 MFMA GEMM)",
+        "roofline": {"bound": "hbm", "kernel": DOMINANT_DESC,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "per_launch_bytes": per_launch_bytes, "per_launch_us": per_launch_ms * 1e3,
-                     "launches_per_round": dom["launches"] / args.profile_rounds},
+                     "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",
+                     "algorithmic_bytes_per_launch": per_launch_bytes, "us_per_launch": per_launch_us,
+                     "launches_per_round": dom["launches"],
+                     "timing": f"HIP events around {args.replay_reps} graph replays of the round's "
+                               f"{dom['launches']} launches of this kernel on the library's stream"},
         "stages_ms_median": stage_med,
         "kernels": kernels,
         "acceptance": {"mean_A": float(np.mean(accepted)) if accepted else None,

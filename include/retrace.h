@@ -124,18 +124,21 @@ const char* rt_last_error(void);
 
 /* ---- measurement --------------------------------------------------------------- */
 
-/* Kernel kinds reported by rt_profile_round. */
+/* Launch classes reported by rt_profile_round (one per role in the round). */
 enum {
-  RT_K_GEMM_SKINNY = 0,      /* weight-streaming MFMA GEMM, 16/32-row tiles (projections) */
-  RT_K_GEMM_SKINNY_F32A = 1, /* same, fp32 A operand (conditioning GEMMs, Eq.7-9) */
-  RT_K_GEMM_WIDE = 2,        /* 128-row tiles (prefill, large batches) */
-  RT_K_GEMM_WIDE_F32A = 3,
-  RT_K_ATTENTION = 4,        /* paged attention incl. split merge */
-  RT_K_NORM = 5,             /* RMSNorm */
-  RT_K_MISC = 6,             /* embedding gathers, conditioning gather, acceptance, argmax reduce */
-  RT_K_LM_HEAD = 7,          /* vocabulary projection with fused argmax */
-  RT_K_QKV_POST = 8,         /* q/k norm, RoPE and paged K/V writes */
-  RT_K_KINDS = 9
+  RT_K_GEMM_QKV = 0,       /* fused q|k|v projection (target and drafter layers) */
+  RT_K_GEMM_O = 1,         /* attention output projection, residual add fused */
+  RT_K_GEMM_GATE_UP = 2,   /* fused gate|up projection, SwiGLU fused */
+  RT_K_GEMM_DOWN = 3,      /* down projection, residual add (and state capture) fused */
+  RT_K_GEMM_CONTEXT = 4,   /* drafter context pathway: fc and the fused context K|V projection */
+  RT_K_GEMM_COND = 5,      /* conditioning projections W_c, W_g, W_v (Eq.7-9), fp32 A operand */
+  RT_K_ATTENTION = 6,      /* paged attention over key splits (partials or final output) */
+  RT_K_ATTN_MERGE = 7,     /* merge of the key-split partials */
+  RT_K_NORM = 8,           /* RMSNorm */
+  RT_K_QKV_POST = 9,       /* q/k norm, RoPE and paged K/V writes */
+  RT_K_LM_HEAD = 10,       /* vocabulary projection with fused argmax */
+  RT_K_MISC = 11,          /* embedding gathers, conditioning gather, argmax reduce, acceptance */
+  RT_K_KINDS = 12
 };
 /* Stages of one round, in order (a HIP event at every boundary). */
 enum {
@@ -145,16 +148,28 @@ enum {
 typedef struct rt_kernel_stat {
   int32_t kind;
   int32_t launches;
-  double ms;       /* summed HIP-event time around each launch */
+  double ms;       /* summed kernel execution time (HIP events recorded by each launch) */
   double bytes;    /* summed algorithmic HBM bytes (weights + activations + KV read once) */
   double flops;    /* summed algorithmic FLOPs */
 } rt_kernel_stat;
 
-/* Runs one round without graph replay, with a HIP-event pair around every kernel
- * launch on the model's stream and an event at every stage boundary; fills
- * stats[RT_K_KINDS] and stage_ms[RT_PROF_STAGES] plus the usual round outputs. */
+/* Runs one round without graph replay, with a HIP-event pair on every kernel launch
+ * on the model's stream and an event at every stage boundary; fills
+ * stats[RT_K_KINDS] and stage_ms[RT_PROF_STAGES] plus the usual round outputs.
+ * Each kernel's pair is recorded by the launch itself (hipExtLaunchKernel), so the
+ * summed times are the kernels' execution times, without host launch gaps. */
 int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32_t* tokens,
                      int32_t* n_committed, int32_t* accept_len);
+
+/* Times one launch class in isolation: the launches of `kind` that one round makes
+ * (with the round's current buffers and context lengths) are captured into a HIP
+ * graph and replayed `reps` times (1..1000) between two HIP events on the model's
+ * stream.  stat->launches = launches per round, stat->ms = their summed time per
+ * replay (so ms / launches is the kernel's average duration), stat->bytes / flops =
+ * their algorithmic totals.  Allowed for RT_K_GEMM_*, RT_K_ATTENTION, RT_K_ATTN_MERGE
+ * and RT_K_LM_HEAD, whose outputs are per-round scratch; KV caches and the carried
+ * round state are not touched.  Other kinds return RT_ERR_INVALID. */
+int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat);
 
 /* ---- test hooks -------------------------------------------------------------- */
 

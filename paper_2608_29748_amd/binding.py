@@ -25,17 +25,17 @@ RT_MAX_COND_LAYERS = 8
 (RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
  RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G) = range(9)
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
-(RT_K_GEMM_SKINNY, RT_K_GEMM_SKINNY_F32A, RT_K_GEMM_WIDE, RT_K_GEMM_WIDE_F32A, RT_K_ATTENTION, RT_K_NORM,
- RT_K_MISC, RT_K_LM_HEAD, RT_K_QKV_POST) = range(9)
-RT_K_KINDS = 9
-KERNEL_KIND_NAMES = ["gemm_skinny", "gemm_skinny_f32a", "gemm_wide", "gemm_wide_f32a", "attention",
-                     "rmsnorm", "misc", "lm_head", "qkv_post"]
+(RT_K_GEMM_QKV, RT_K_GEMM_O, RT_K_GEMM_GATE_UP, RT_K_GEMM_DOWN, RT_K_GEMM_CONTEXT, RT_K_GEMM_COND,
+ RT_K_ATTENTION, RT_K_ATTN_MERGE, RT_K_NORM, RT_K_QKV_POST, RT_K_LM_HEAD, RT_K_MISC) = range(12)
+RT_K_KINDS = 12
+KERNEL_KIND_NAMES = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_context", "gemm_cond",
+                     "attention", "attn_merge", "rmsnorm", "qkv_post", "lm_head", "misc"]
 STAGE_NAMES = ["condition", "draft", "draft_lm_head", "verify", "verify_lm_head", "accept", "context_append"]
 RT_PROF_STAGES = 7
 
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
-           "rt_debug_write", "rt_profile_round"]
+           "rt_debug_write", "rt_profile_round", "rt_time_kernel"]
 
 
 class RetraceError(RuntimeError):
@@ -83,6 +83,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_debug_read.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_debug_write.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_profile_round.argtypes = [P, C.POINTER(rt_kernel_stat), C.POINTER(C.c_double), i32p, i32p, i32p]
+    lib.rt_time_kernel.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(rt_kernel_stat)]
     for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
                  "rt_set_debug", "rt_debug_read", "rt_debug_write", "rt_profile_round"):
         getattr(lib, name).restype = C.c_int
@@ -165,7 +166,7 @@ def rt_spec_round_forced(h: int, drafts: np.ndarray, block_size: int):
 
 
 def rt_profile_round(h: int, n_seqs: int, block_size: int):
-    """One round with an event pair around every launch: returns (per-kind stats list of
+    """One round with an event pair on every launch: returns (per-kind stats list of
     dicts, per-stage ms list, tokens, n_committed, accept_len)."""
     stats = (rt_kernel_stat * RT_K_KINDS)()
     stages = (C.c_double * RT_PROF_STAGES)()
@@ -177,6 +178,14 @@ def rt_profile_round(h: int, n_seqs: int, block_size: int):
     out = [dict(kind=KERNEL_KIND_NAMES[s.kind], launches=s.launches, ms=s.ms, bytes=s.bytes, flops=s.flops)
            for s in stats]
     return out, list(stages), tok, n, a
+
+
+def rt_time_kernel(h: int, kind: int, reps: int) -> dict:
+    """Replay timing of one launch class: dict(kind, launches per round, ms of those
+    launches per replay, algorithmic bytes, flops)."""
+    st = rt_kernel_stat()
+    _check(_lib.rt_time_kernel(C.c_void_p(h), kind, reps, C.byref(st)))
+    return dict(kind=KERNEL_KIND_NAMES[st.kind], launches=st.launches, ms=st.ms, bytes=st.bytes, flops=st.flops)
 
 
 def rt_set_debug(h: int, flags: int) -> None:

@@ -15,6 +15,9 @@ SOURCES = ["gemm.hip", "attn.hip", "misc.hip", "engine.hip", "validate.cpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          # packed fp32 vector ops stay off: hipcc otherwise forms them from float code
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# per-source extras: attention keeps its MFMA accumulators in ordinary VGPRs (the online
+# softmax rescales them with vector ALU ops; accumulation registers would be copied)
+EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _hipcc() -> str:
@@ -23,7 +26,7 @@ def _hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd = [_hipcc(), "-O2", "-std=c++17", "-fPIC", "-Wall", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -26,10 +26,13 @@ struct AttnArgs {
 // Number of query (token, head) rows handled by one workgroup.
 constexpr int kAttnRows = 64;
 
+// attention = attention_partials (per key split) then attention_merge (splits > 1).
 template <typename T>
 hipError_t attention(const AttnArgs& a, hipStream_t s);
+template <typename T>
+hipError_t attention_partials(const AttnArgs& a, hipStream_t s);
+template <typename T>
+hipError_t attention_merge(const AttnArgs& a, hipStream_t s);
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim);
-// Smallest split count for which one split's page ids fit the kernel's table.
-int attn_min_splits(int max_keys);
 
 }  // namespace rt

@@ -1,21 +1,26 @@
 // Paged GQA attention with MFMA.  One workgroup (4 waves) owns one sequence, one KV
 // head, one block of 64 (token, head) query rows and one contiguous share of the key
-// range; each wave owns a 16-row MFMA tile and runs an online softmax over 32-key
-// chunks staged in LDS.  K pages are stored [token][hd] so a K row is a contiguous
-// B-operand fragment of S = Q K^T; V pages are stored transposed ([hd][token]) so a
-// V^T row is a contiguous B-operand fragment of O = P V.  Split partials
-// (unnormalised O, running max, running sum) are merged by a second kernel.
+// range, walked in 64-key chunks (four pages); each wave owns a 16-row MFMA tile of
+// the queries and runs an online softmax.  K pages are stored [token][hd] and V pages
+// transposed ([hd][token]), so a K row and a V^T row are contiguous MFMA fragments.
+// Split partials (unnormalised O, running max, running sum) are merged by a second
+// kernel.
+//
+// bf16 storage: every wave copies one page of K and one of V per chunk straight from
+// HBM into LDS (16-byte direct-to-LDS loads), into a ring of pipeline stages, so the
+// copies of the next chunks are in flight while the current one is used; one barrier
+// per chunk.  fp32 storage (small configurations): chunks are staged through
+// registers.
 #include "attn.h"
 
 namespace rt {
 
 constexpr int kChunk = 64;      // keys per LDS chunk (four pages)
-constexpr int kMaxSplitPages = 1024;   // page ids of one split held in LDS (16384 keys)
+constexpr int kMaxSplitPages = 1024;   // fp32 path: page ids of one split held in LDS (16384 keys)
 
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim) {
   return (size_t)n_seqs * n_kv_heads * row_blocks * splits * kAttnRows * head_dim;
 }
-int attn_min_splits(int max_keys) { return (max_keys + kMaxSplitPages * kPage - 1) / (kMaxSplitPages * kPage); }
 
 // Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
 // keys 4*(lane/16)+i of one query (column lane%16), so the softmax is a per-lane
@@ -24,7 +29,7 @@ int attn_min_splits(int max_keys) { return (max_keys + kMaxSplitPages * kPage - 
 // lane supplies keys {4g..4g+3} and {16+4g..16+4g+3} of the step (g = lane/16); the
 // V^T fragment from LDS uses the same key order.
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
   constexpr int EB = Elem<T>::kBytes;
   constexpr int KPAD = HD + 16 / EB;       // LDS row pitch (elements) for K
   constexpr int VPAD = kChunk + 16 / EB;   // LDS row pitch for V^T
@@ -50,8 +55,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int last_tok = min(nrows, row0 + kAttnRows) - 1;
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end)
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
-  const int cps = (nchunks + a.splits - 1) / a.splits;
-  const int c_beg = split * cps, c_end = min(nchunks, c_beg + cps);
+  // chunks spread evenly over the splits (counts differ by at most one)
+  const int c_beg = (int)((long)split * nchunks / a.splits), c_end = (int)((long)(split + 1) * nchunks / a.splits);
   // page ids of this split's keys (pages past kv_end are never dereferenced)
   const int pg_beg = c_beg * PAGES;
   const int npg = max(0, min((kv_end + kPage - 1) / kPage, c_end * PAGES) - pg_beg);
@@ -233,12 +238,294 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-// One wave per (sequence, kv head, row).  Lane j reads split j's running max and sum
-// (64 splits per pass); the weights exp2(m_j - M) are broadcast by shuffles while the
-// lanes accumulate the head dimension, eight splits' partial rows in flight at a time.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(4))) const int32_t const_i32_t;
+
+// Workgroup barrier that orders LDS accesses for the compiler but does not wait for
+// outstanding vector-memory operations (the direct-to-LDS copies are waited for
+// explicitly with wait_vm, so that later stages stay in flight).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+__device__ __forceinline__ short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
+__device__ __forceinline__ float bf16_value(short b) { return __uint_as_float(((uint32_t)(uint16_t)b) << 16); }
+
+// XOR swizzle of the 16-byte pieces of a K row in LDS (row r of chunk page pg), so that
+// the 16 lanes reading one fragment column hit distinct banks.
+template <int NPR>
+__device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)) & (NPR - 1); }
+
+// Work split of a workgroup: wave w owns query rows rh*32..rh*32+31 of the row block
+// (rh = w/2, two 16-row MFMA tiles) and keys kh*32..kh*32+31 of every 64-key chunk
+// (kh = w%2, two pages); the two key halves of the same rows are merged through LDS at
+// the end.  Every K / V byte staged in LDS is read by two waves.
+//
+// Key order inside a wave's 32 keys: score tile tau (0, 1), A-operand row m holds key
+// (m/4)*8 + 4*tau + m%4, so that the accumulator lane (g, q) ends up with the eight
+// consecutive keys 8g..8g+7 (tau = 0: 8g..8g+3, tau = 1: 8g+4..8g+7).  Those eight
+// probabilities are exactly the lane's B operand of O^T += V^T P^T, and its V^T operand
+// is one contiguous 16-byte piece of a V page row.
+template <int HD, int NSTAGE>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+  constexpr int ROWB = HD * 2;                 // bytes of one K row (one token)
+  constexpr int NPR = ROWB / 16;               // 16-byte pieces per K row
+  constexpr int PGB = kPage * ROWB;            // bytes of one (page, KV head) slice of K or V
+  constexpr int NLD = PGB / 1024;              // wave-wide 16-byte-per-lane copies per slice
+  constexpr int PAGES = kChunk / kPage;        // one page copied per wave
+  constexpr int STG = 2 * PAGES * PGB;         // one stage: 4 K slices, then 4 V slices
+  constexpr int NHT = HD / 16, NKS = HD / 32;
+  constexpr int OPITCH = HD + 4;               // fp32 row pitch of the key-half merge buffer
+  constexpr int MERGE = 2 * 32 * OPITCH * 4 + 2 * 32 * 2 * 4;
+  constexpr int SMEM = NSTAGE * STG > MERGE ? NSTAGE * STG : MERGE;
+  static_assert(PAGES == 4, "one page per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  const int lane = threadIdx.x & 63, g4 = lane >> 4, c16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rh = w >> 1, kh = w & 1;
+  const int split = blockIdx.x, kvh = blockIdx.y;
+  const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
+  const int P = a.pos0[s * a.seq_stride];
+  const int nrows = nq * G;
+  const int row0 = rb * kAttnRows;
+  if (row0 >= nrows) return;
+  const int last_tok = min(nrows, row0 + kAttnRows) - 1;
+  const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end), kv_end >= 1
+  const int nchunks = (kv_end + kChunk - 1) / kChunk;
+  // chunks spread evenly over the splits (counts differ by at most one)
+  const int c_beg = (int)((long)split * nchunks / a.splits), c_end = (int)((long)(split + 1) * nchunks / a.splits);
+  const int last_page = (kv_end - 1) / kPage;
+  const_i32_t* pt = (const_i32_t*)(a.page_table + (size_t)s * a.max_pages);
+  // page w of chunk c (pages past kv_end are replaced by the last valid one, so every
+  // wave issues the same number of copies per chunk; their keys are masked)
+  auto page_of = [&](int c) { return pt[min(c * PAGES + w, last_page)]; };
+
+  // per-lane source offsets of the copies (LDS slot j*64+lane of this wave's slice)
+  int koff[NLD], voff[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) {
+    const int sl = j * 64 + lane;
+    const int r = sl / NPR, p = sl % NPR;
+    koff[j] = r * ROWB + (p ^ kswz<NPR>(r, w)) * 16;
+    const int h = sl >> 1, vp = sl & 1;
+    voff[j] = h * 32 + (vp ^ ((h >> 3) & 1)) * 16;
+  }
+  auto issue = [&](int pg, int stg) {
+    const char* kb = (const char*)a.kcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
+    const char* vb = (const char*)a.vcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
+    char* lk = smem + stg * STG + w * PGB;
+    char* lv = smem + stg * STG + PAGES * PGB + w * PGB;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
+  };
+
+  // this wave's queries: tile t2 (0, 1) column c16 is row row0 + rh*32 + t2*16 + c16
+  const int nrt = min(2, max(0, (nrows - row0 - rh * 32 + 15) / 16));   // tiles with valid rows
+  Frag<bf16_t> qf[2][NKS];
+  int qpos[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int qrow = row0 + rh * 32 + t2 * 16 + c16;
+    const int r = min(qrow, nrows - 1);
+    qpos[t2] = P + r / G;
+    const int tok = r / G, h = kvh * G + r % G;
+    const bf16_t* qp = (const bf16_t*)a.q + (size_t)(s * a.rows_per_seq + tok) * a.n_q_heads * HD + (size_t)h * HD;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].load(qp + ks * 32 + g4 * 8);
+  }
+  const float sl2 = a.scale * 1.4426950408889634f;
+  float mref[2] = {-INFINITY, -INFINITY};   // reference max (log2 units); raised lazily
+  float lsum[2] = {0.f, 0.f};               // this lane's share of the softmax denominator
+  f32x4 o[2][NHT];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+    for (int t = 0; t < NHT; ++t) o[t2][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // prologue: chunks c_beg .. c_beg+NSTAGE-2 in flight
+#pragma unroll
+  for (int i = 0; i < NSTAGE - 1; ++i)
+    if (c_beg + i < c_end) issue(page_of(c_beg + i), i);
+  int pg_next = page_of(c_beg + NSTAGE - 1);
+
+  for (int c = c_beg; c < c_end; ++c) {
+    const int i = c - c_beg;
+    // this wave's copies of chunk c have landed once at most the later chunks' remain
+    if constexpr (NSTAGE >= 3) {
+      if (c + 1 < c_end) wait_vm<2 * NLD>(); else wait_vm<0>();
+    } else {
+      wait_vm<0>();
+    }
+    lds_barrier();   // every wave's copies of chunk c are visible; chunk c-1's stage is free
+    if (c + NSTAGE - 1 < c_end) {
+      issue(pg_next, (i + NSTAGE - 1) % NSTAGE);
+      pg_next = page_of(c + NSTAGE);
+    }
+    if (nrt == 0) continue;
+    const char* sk = smem + (i % NSTAGE) * STG;
+    const char* sv = sk + PAGES * PGB;
+    const int kbase = c * kChunk + kh * 32;
+    // fragments of this wave's 32 keys: K (2 score tiles x NKS), V^T (NHT)
+    Frag<bf16_t> kf[2][NKS], vf[NHT];
+#pragma unroll
+    for (int tau = 0; tau < 2; ++tau) {
+      const int kis = (c16 >> 2) * 8 + tau * 4 + (c16 & 3);
+      const int pg = kh * 2 + (kis >> 4), r = kis & 15;
+      const char* rowp = sk + pg * PGB + r * ROWB;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        kf[tau][ks].v = *reinterpret_cast<const bf16x8*>(rowp + ((ks * 4 + g4) ^ kswz<NPR>(r, pg)) * 16);
+    }
+#pragma unroll
+    for (int t = 0; t < NHT; ++t) {
+      const int pg = kh * 2 + (g4 >> 1), h = t * 16 + c16;
+      vf[t].v = *reinterpret_cast<const bf16x8*>(sv + pg * PGB + h * 32 + ((g4 & 1) ^ ((h >> 3) & 1)) * 16);
+    }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      if (t2 >= nrt) break;
+      // S^T = K Q^T: two 16-key tiles of this query tile
+      f32x4 st[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau) mma(st[tau], kf[tau][ks], qf[t2][ks]);
+      if (kbase + 32 > P) {   // keys that reach the block: causal / end mask
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int kp = kbase + g4 * 8 + tau * 4 + e;
+            const bool vis = kp < kv_end && (!a.causal || kp <= qpos[t2]);
+            st[tau][e] = vis ? st[tau][e] : -INFINITY;
+          }
+      }
+      float mx = fmaxf(fmaxf(fmaxf(st[0][0], st[0][1]), fmaxf(st[0][2], st[0][3])),
+                       fmaxf(fmaxf(st[1][0], st[1][1]), fmaxf(st[1][2], st[1][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mxs = mx * sl2;
+      // raise the reference only when a score exceeds it by more than 2^8 (exponentials
+      // stay below 256; the final ratio is unchanged); rescale O and the sum then
+      if (__builtin_amdgcn_ballot_w64(mxs > mref[t2] + 8.f)) {
+        const float mnew = fmaxf(mref[t2], mxs);
+        const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mref[t2] - mnew);
+#pragma unroll
+        for (int t = 0; t < NHT; ++t)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[t2][t][e] *= alpha;
+        lsum[t2] *= alpha;
+        mref[t2] = mnew;
+      }
+      const bool live = mref[t2] != -INFINITY;
+      Frag<bf16_t> ph, pl;
+#pragma unroll
+      for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = live ? __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mref[t2])) : 0.f;
+          lsum[t2] += x;
+          const short hb = bf16_bits(x);
+          ph.v[tau * 4 + e] = hb;
+          pl.v[tau * 4 + e] = bf16_bits(x - bf16_value(hb));
+        }
+      // O^T += V^T P^T (P split into bf16 hi + lo parts, ~16 significand bits)
+#pragma unroll
+      for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], ph);
+#pragma unroll
+      for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], pl);
+    }
+  }
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    lsum[t2] += __shfl_xor(lsum[t2], 16, 64);
+    lsum[t2] += __shfl_xor(lsum[t2], 32, 64);
+  }
+
+  // merge the two key halves of each row pair of waves through LDS (stages are free
+  // once every wave has passed this barrier)
+  lds_barrier();
+  float* mo = reinterpret_cast<float*>(smem) + rh * 32 * OPITCH;             // [32][OPITCH] O^T rows
+  float* mml = reinterpret_cast<float*>(smem) + 2 * 32 * OPITCH + rh * 64;    // [32][2] (m, l)
+  if (kh == 1) {
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int rl = t2 * 16 + c16;
+#pragma unroll
+      for (int t = 0; t < NHT; ++t)
+        *reinterpret_cast<float4*>(mo + rl * OPITCH + t * 16 + 4 * g4) =
+            make_float4(o[t2][t][0], o[t2][t][1], o[t2][t][2], o[t2][t][3]);
+      if (g4 == 0) { mml[rl * 2] = mref[t2]; mml[rl * 2 + 1] = lsum[t2]; }
+    }
+  }
+  lds_barrier();
+  if (kh == 1) return;
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int rl = t2 * 16 + c16;
+    const float m1 = mml[rl * 2], l1 = mml[rl * 2 + 1];
+    const float m0 = mref[t2];
+    const float M = fmaxf(m0, m1);
+    const float f0 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
+    const float f1 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+    const float L = f0 * lsum[t2] + f1 * l1;
+#pragma unroll
+    for (int t = 0; t < NHT; ++t) {
+      const float4 v1 = *reinterpret_cast<const float4*>(mo + rl * OPITCH + t * 16 + 4 * g4);
+      o[t2][t][0] = f0 * o[t2][t][0] + f1 * v1.x;
+      o[t2][t][1] = f0 * o[t2][t][1] + f1 * v1.y;
+      o[t2][t][2] = f0 * o[t2][t][2] + f1 * v1.z;
+      o[t2][t][3] = f0 * o[t2][t][3] + f1 * v1.w;
+    }
+    const int qrow = row0 + rh * 32 + rl;
+    if (a.splits == 1) {
+      if (qrow < nrows) {
+        const int tok = qrow / G, h = kvh * G + qrow % G;
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        bf16_t* op = (bf16_t*)a.out;
+        const int orow = s * a.rows_per_seq + tok;
+#pragma unroll
+        for (int t = 0; t < NHT; ++t)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            op[pa_index(orow, h * HD + t * 16 + 4 * g4 + e, a.ldo)] = f32_to_bf16(o[t2][t][e] * inv);
+      }
+    } else {
+      const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
+      float* op = a.opart + blk * kAttnRows * HD;
+      float* ml = a.mlpart + blk * kAttnRows * 2;
+      const int rw = rh * 32 + rl;
+#pragma unroll
+      for (int t = 0; t < NHT; ++t)
+        *reinterpret_cast<float4*>(op + (size_t)rw * HD + t * 16 + 4 * g4) =
+            make_float4(o[t2][t][0], o[t2][t][1], o[t2][t][2], o[t2][t][3]);
+      if (g4 == 0) { ml[rw * 2] = M; ml[rw * 2 + 1] = L; }
+    }
+  }
+}
+
+// One wave per (sequence, kv head, row).  Lane j holds split j's running max and sum;
+// the partial O rows are loaded in batches of 32 splits (lane l keeps hd l, l+64, ...),
+// issued before the split weights exp2(m_j - M) are known, and summed with the weights
+// read from lane j.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int PL = HD / 64;                 // hd elements per lane
+  constexpr int NB = 32;                      // splits per batch of loads
   const int lane = threadIdx.x & 63;
   const int rl = blockIdx.x * 4 + (threadIdx.x >> 6);        // row within the row block
   const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks, kvh = blockIdx.y;
@@ -246,68 +533,88 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int r = rb * kAttnRows + rl;
   if (r >= nq * G) return;
-  const size_t blk0 = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits;
-  float M = -INFINITY;
-  for (int sp = lane; sp < a.splits; sp += 64) M = fmaxf(M, a.mlpart[((blk0 + sp) * kAttnRows + rl) * 2]);
-  M = warp_max(M);
-  float num[PL], den = 0.f;
+  const int S = a.splits;                     // <= 64
+  const size_t blk0 = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * S;
+  const float* opp = a.opart + (blk0 * kAttnRows + rl) * HD + lane;   // split j: + j * kAttnRows * HD
+  const float* mlp = a.mlpart + (blk0 * kAttnRows + rl) * 2;          // split j: + j * kAttnRows * 2
+  float ob[NB][PL];
 #pragma unroll
-  for (int j = 0; j < PL; ++j) num[j] = 0.f;
-  if (M != -INFINITY) {
-    for (int base = 0; base < a.splits; base += 64) {
-      const int sp = base + lane;
-      float f = 0.f;
-      if (sp < a.splits) {
-        const float* ml = a.mlpart + ((blk0 + sp) * kAttnRows + rl) * 2;
-        f = (ml[0] == -INFINITY) ? 0.f : exp2f(ml[0] - M);
-        den += f * ml[1];
-      }
-      const int n = min(64, a.splits - base);
-      for (int j0 = 0; j0 < n; j0 += 8) {
-        float o[8][PL], fw[8];
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int jj = j0 + u < n ? j0 + u : n - 1;
-          fw[u] = __shfl(f, jj, 64) * (j0 + u < n ? 1.f : 0.f);
-          const float* op = a.opart + ((blk0 + base + jj) * kAttnRows + rl) * HD;
+    for (int e = 0; e < PL; ++e) ob[j][e] = j < S ? opp[(size_t)j * kAttnRows * HD + 64 * e] : 0.f;
+  float mj = -INFINITY, lj = 0.f;
+  if (lane < S) {
+    const float2 v = *reinterpret_cast<const float2*>(mlp + (size_t)lane * kAttnRows * 2);
+    mj = v.x;
+    lj = v.y;
+  }
+  const float M = warp_max(mj);
+  const float f = (M == -INFINITY || mj == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj - M);
+  const float den = warp_sum(f * lj);
+  float num[PL];
 #pragma unroll
-          for (int j = 0; j < PL; ++j) o[u][j] = op[lane + 64 * j];
-        }
+  for (int e = 0; e < PL; ++e) num[e] = 0.f;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+  for (int j = 0; j < NB; ++j) {
+    const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j));
 #pragma unroll
-          for (int j = 0; j < PL; ++j) num[j] += fw[u] * o[u][j];
-      }
+    for (int e = 0; e < PL; ++e) num[e] += fj * ob[j][e];
+  }
+  for (int j0 = NB; j0 < S; j0 += NB) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int e = 0; e < PL; ++e) ob[j][e] = j0 + j < S ? opp[(size_t)(j0 + j) * kAttnRows * HD + 64 * e] : 0.f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j0 + j));
+#pragma unroll
+      for (int e = 0; e < PL; ++e) num[e] += (j0 + j < S ? fj : 0.f) * ob[j][e];
     }
   }
-  den = warp_sum(den);
   const int tok = r / G, h = kvh * G + r % G;
   T* out = (T*)a.out;
   const int orow = s * a.rows_per_seq + tok;
   const float inv = den > 0.f ? 1.f / den : 0.f;
 #pragma unroll
-  for (int j = 0; j < PL; ++j) out[pa_index(orow, h * HD + lane + 64 * j, a.ldo)] = Elem<T>::from_f32(num[j] * inv);
+  for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane + 64 * e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
+constexpr int kStages = 2;   // direct-to-LDS pipeline depth (64 KB of LDS per workgroup at hd 128)
+
 template <typename T>
-hipError_t attention(const AttnArgs& a, hipStream_t s) {
+hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.splits, a.n_kv_heads, a.n_seqs * a.row_blocks);
-  if (a.head_dim == 128) {
-    hipLaunchKernelGGL((attn_kernel<T, 128>), grid, dim3(256), 0, s, a);
-    if (a.splits > 1)
-      hipLaunchKernelGGL((attn_merge_kernel<T, 128>), dim3(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks),
-                         dim3(256), 0, s, a);
-  } else if (a.head_dim == 64) {
-    hipLaunchKernelGGL((attn_kernel<T, 64>), grid, dim3(256), 0, s, a);
-    if (a.splits > 1)
-      hipLaunchKernelGGL((attn_merge_kernel<T, 64>), dim3(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks),
-                         dim3(256), 0, s, a);
+  if constexpr (sizeof(T) == 2) {
+    if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages>), grid, dim3(256), 0, s, a);
+    else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages>), grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
   } else {
-    return hipErrorInvalidValue;
+    if (a.head_dim == 128) RT_LAUNCH((attn_staged_kernel<T, 128>), grid, dim3(256), 0, s, a);
+    else if (a.head_dim == 64) RT_LAUNCH((attn_staged_kernel<T, 64>), grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
+template <typename T>
+hipError_t attention_merge(const AttnArgs& a, hipStream_t s) {
+  if (a.splits <= 1) return hipSuccess;
+  dim3 grid(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks);
+  if (a.head_dim == 128) RT_LAUNCH((attn_merge_kernel<T, 128>), grid, dim3(256), 0, s, a);
+  else if (a.head_dim == 64) RT_LAUNCH((attn_merge_kernel<T, 64>), grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+template <typename T>
+hipError_t attention(const AttnArgs& a, hipStream_t s) {
+  hipError_t e = attention_partials<T>(a, s);
+  return e != hipSuccess ? e : attention_merge<T>(a, s);
+}
 template hipError_t attention<bf16_t>(const AttnArgs&, hipStream_t);
 template hipError_t attention<float>(const AttnArgs&, hipStream_t);
+template hipError_t attention_partials<bf16_t>(const AttnArgs&, hipStream_t);
+template hipError_t attention_partials<float>(const AttnArgs&, hipStream_t);
+template hipError_t attention_merge<bf16_t>(const AttnArgs&, hipStream_t);
+template hipError_t attention_merge<float>(const AttnArgs&, hipStream_t);
 
 }  // namespace rt

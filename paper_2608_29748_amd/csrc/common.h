@@ -1,9 +1,33 @@
 // Device-side helpers shared by the ReTrace round kernels (gfx950, wave64).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace rt {
+
+// Profiling hook of the host launchers: when a pair of HIP events is armed for the next
+// launch on this thread, that launch goes through hipExtLaunchKernel, which records the
+// events at the kernel's own start and end, so their elapsed time is the kernel's
+// execution time without queueing gaps.
+// A launch marked `skip` is not issued (kernel replay records only one launch class).
+struct LaunchEvents {
+  hipEvent_t b = nullptr, e = nullptr;
+  bool used = false;
+  bool skip = false;
+};
+LaunchEvents& launch_events();   // thread-local
+#define RT_LAUNCH(kernel, grid, block, shmem, stream, ...)                                        \
+  do {                                                                                            \
+    ::rt::LaunchEvents& ev_ = ::rt::launch_events();                                              \
+    if (ev_.skip) {                                                                               \
+    } else if (ev_.b && !ev_.used) {                                                              \
+      ev_.used = true;                                                                            \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev_.b, ev_.e, 0, __VA_ARGS__);    \
+    } else {                                                                                      \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                        \
+    }                                                                                             \
+  } while (0)
 
 typedef uint16_t bf16_t;                                   // bfloat16 bit pattern
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;

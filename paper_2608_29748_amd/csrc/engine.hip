@@ -14,6 +14,10 @@
 
 namespace rt {
 const char* last_error();
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
 
 #define HIPCHK(x)                                                                          \
   do {                                                                                     \
@@ -46,16 +50,34 @@ struct EngineBase {
   hipEvent_t stage_ev[RT_PROF_STAGES + 1] = {};
   std::vector<int32_t> prof_ctx;   // host copy of each sequence's context length
   size_t ev_next = 0;
+  // kernel replay: only launches of this class are issued (and counted)
+  int only_kind = -1;
+  int only_launches = 0;
+  double only_bytes = 0, only_flops = 0;
+  bool instrumented() const { return profiling || only_kind >= 0; }
+  // The next launch records the pair at its own start and end (see RT_LAUNCH).
   void prof_begin(int kind, double bytes, double flops) {
+    if (only_kind >= 0) {
+      const bool take = kind == only_kind;
+      launch_events().skip = !take;
+      if (take) { only_launches += 1; only_bytes += bytes; only_flops += flops; }
+      return;
+    }
     if (!profiling) return;
     ProfRec r{kind, ev_pool[ev_next], ev_pool[ev_next + 1], bytes, flops};
     ev_next += 2;
-    (void)hipEventRecord(r.b, stream);
     prof.push_back(r);
+    launch_events() = LaunchEvents{r.b, r.e, false};
   }
   void prof_end() {
+    if (only_kind >= 0) { launch_events().skip = true; return; }
     if (!profiling) return;
-    (void)hipEventRecord(prof.back().e, stream);
+    LaunchEvents& le = launch_events();
+    if (!le.used) {   // nothing was launched: a zero-length record
+      (void)hipEventRecord(prof.back().b, stream);
+      (void)hipEventRecord(prof.back().e, stream);
+    }
+    le = LaunchEvents{};
   }
   void stage(int i) {
     if (profiling) (void)hipEventRecord(stage_ev[i], stream);
@@ -79,6 +101,7 @@ struct EngineBase {
   virtual int run_round(bool forced) = 0;
   int round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
+  int time_kernel(int kind, int reps, rt_kernel_stat* out);
   int debug_read(int id, int seq, void* dst, size_t bytes);
   int debug_write(int id, int seq, const void* src, size_t bytes);
 };
@@ -88,7 +111,22 @@ struct Engine : EngineBase {
   const char* tlayer(int l) const { return ws + p.t_layers + (size_t)l * p.layer_bytes; }
   const char* dlayer(int l) const { return ws + p.d_layers + (size_t)l * p.layer_bytes; }
 
-  int gemm_call(const void* A, int lda, int a_rows, bool af32, const void* B, int N, int Kp, int M,
+  // Algorithmic bytes an epilogue moves for an M x N result (outputs written, side
+  // inputs read).
+  static double epi_bytes(const EpiArgs& e, int M, int N) {
+    const double mn = (double)M * N;
+    switch (e.kind) {
+      case EPI_STORE_F32: return mn * 4;
+      case EPI_STORE_ACT: return mn * sizeof(T);
+      case EPI_RESID: return mn * 8 + (e.cap ? mn * sizeof(T) : 0);
+      case EPI_SWIGLU: return mn / 2 * sizeof(T);
+      case EPI_COND_R: return mn * 8;
+      case EPI_COND_GATE: return mn * 4;
+      default: return mn * (12 + sizeof(T));   // EPI_COND_OUT: gate, e rows, x and etilde
+    }
+  }
+
+  int gemm_call(int kind, const void* A, int lda, int a_rows, bool af32, const void* B, int N, int Kp, int M,
                 EpiArgs e, int k_logical = 0) {
     if (M <= 0) return RT_OK;
     if (k_logical <= 0) k_logical = Kp;
@@ -113,10 +151,9 @@ struct Engine : EngineBase {
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
     a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
-    if (profiling) {
+    if (instrumented()) {
       const double Kl = (double)k_logical;
-      const int kind = (shape == SHAPE_SKINNY ? RT_K_GEMM_SKINNY : RT_K_GEMM_WIDE) + (af32 ? 1 : 0);
-      prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + (double)M * N * 4,
+      prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + epi_bytes(e, M, N),
                  2.0 * M * N * Kl);
     }
     HIPCHK(gemm<T>(a, shape, af32, stream));
@@ -145,7 +182,7 @@ struct Engine : EngineBase {
     prof_end();
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
-    CHK(gemm_call(xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
+    CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
     QkvPostArgs qp{};
     qp.src = at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
     qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
@@ -164,7 +201,7 @@ struct Engine : EngineBase {
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
-    if (profiling) {
+    if (instrumented()) {
       // keys read: every sequence's context plus the block, K and V, once per KV head
       double keys = 0;
       for (int s = 0; s < c.n_seqs; ++s) keys += (double)(c.prof_ctx[s] + c.rows_per_seq);
@@ -172,20 +209,26 @@ struct Engine : EngineBase {
       const double rows = (double)c.n_seqs * c.rows_per_seq;
       prof_begin(RT_K_ATTENTION, kvb + rows * q.qN * sizeof(T) * 2, 4.0 * keys * c.rows_per_seq * q.Hq * q.hd);
     }
-    HIPCHK(attention<T>(a, stream));
+    HIPCHK(attention_partials<T>(a, stream));
     prof_end();
+    if (a.splits > 1) {
+      // partials: unnormalised O plus (max, sum) per (row, split), read once
+      prof_begin(RT_K_ATTN_MERGE, (double)a.splits * q.Hkv * c.rb * c.n_seqs * kAttnRows * (q.hd + 2) * 4.0, 0);
+      HIPCHK(attention_merge<T>(a, stream));
+      prof_end();
+    }
     e = EpiArgs{};
     e.kind = EPI_RESID; e.resid = x; e.ldr = q.d;
-    CHK(gemm_call(at<T>(q.attn), 16 * q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e, q.qN));
+    CHK(gemm_call(RT_K_GEMM_O, at<T>(q.attn), 16 * q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e, q.qN));
     prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, 16 * q.Kp_d, nullptr, 0, stream);
     prof_end();
     e = EpiArgs{};
     e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = 16 * q.Kp_F;
-    CHK(gemm_call(xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e, q.d));
+    CHK(gemm_call(RT_K_GEMM_GATE_UP, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e, q.d));
     e = EpiArgs{};
     e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = 16 * q.Kp_nc; e.cap_k0 = c.cap_k0;
-    CHK(gemm_call(at<T>(q.mlp), 16 * q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
+    CHK(gemm_call(RT_K_GEMM_DOWN, at<T>(q.mlp), 16 * q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
     return RT_OK;
   }
 
@@ -222,14 +265,14 @@ struct Engine : EngineBase {
     const Plan& q = p;
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.fcout); e.ldo = q.d;
-    CHK(gemm_call(at<T>(q.g), 16 * q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
+    CHK(gemm_call(RT_K_GEMM_CONTEXT, at<T>(q.g), 16 * q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
     prof_begin(RT_K_NORM, (double)M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), 16 * q.Kp_d,
                   nullptr, 0, stream);
     prof_end();
     e = EpiArgs{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.LD * 2 * q.kvN;
-    CHK(gemm_call(at<T>(q.fa), 16 * q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e, q.d));
+    CHK(gemm_call(RT_K_GEMM_CONTEXT, at<T>(q.fa), 16 * q.Kp_d, q.Mrows, false, at<T>(q.ctxkv), q.LD * 2 * q.kvN, q.Kp_d, M, e, q.d));
     QkvPostArgs qp{};
     qp.src = at<float>(q.qkvf); qp.lds = q.LD * 2 * q.kvN; qp.M = M;
     qp.q_cols = 0; qp.kv_cols = q.kvN; qp.layer_cols = 2 * q.kvN; qp.n_layers = q.LD;
@@ -374,17 +417,17 @@ struct Engine : EngineBase {
       EpiArgs e{};
       e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er); e.ldo = ldg2; e.out_k0 = q.d;
       e.cond_m = at<float>(q.mu); e.ld_cond_m = ldg2; e.beta = cfg.beta;
-      CHK(gemm_call(at<float>(q.mu), ldg2, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e, 2 * q.d));
+      CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.mu), ldg2, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e, 2 * q.d));
       e = EpiArgs{};
       e.kind = EPI_COND_GATE; e.out_f32 = at<float>(q.gate); e.ldo = q.d;
-      CHK(gemm_call(at<float>(q.er), ldg2, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e, 2 * q.d));
+      CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.er), ldg2, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e, 2 * q.d));
       e = EpiArgs{};
       e.kind = EPI_COND_OUT; e.resid = x; e.ldr = q.d; e.etilde = at<float>(q.etilde);
       e.gate = at<float>(q.gate); e.ld_gate = q.d; e.embed = at<T>(q.embed); e.mask_token = cfg.mask_token_id;
       e.anchor = st + ST_ANCHOR; e.cond_len = st + ST_COND_LEN; e.seq_stride = kStateFields;
       e.rows_per_seq = q.bk;
       // r occupies packed k tiles d/32 .. 2d/32 of er
-      CHK(gemm_call(at<float>(q.er) + (size_t)(q.d / 32) * 512, ldg2, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e, q.d));
+      CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.er) + (size_t)(q.d / 32) * 512, ldg2, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e, q.d));
     } else {
       prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 8), 0);
       embed_block<T>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), q.d, stream);
@@ -497,6 +540,7 @@ int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* 
   profiling = true;
   int rc = run_round(false);
   profiling = false;
+  launch_events() = LaunchEvents{};
   if (rc != RT_OK) return rc;
   const size_t R = (size_t)n_seqs * q.bk;
   HIPCHK(hipMemcpyAsync(h_out, ws + q.out_tok, R * 4, hipMemcpyDeviceToHost, stream));
@@ -521,6 +565,66 @@ int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* 
     HIPCHK(hipEventElapsedTime(&ms, stage_ev[i], stage_ev[i + 1]));
     stage_ms[i] = ms;
   }
+  return RT_OK;
+}
+
+// Kernel replay: the launches of one class from a round (with the round's current
+// buffers and context lengths) are captured into a graph, replayed `reps` times between
+// two HIP events, and averaged.  Only classes whose outputs are per-round scratch are
+// allowed, so the replay changes no KV cache and no carried state.
+int EngineBase::time_kernel(int kind, int reps, rt_kernel_stat* out) {
+  if (!prefilled) return fail(RT_ERR_STATE, "rt_time_kernel called before rt_prefill");
+  switch (kind) {
+    case RT_K_GEMM_QKV: case RT_K_GEMM_O: case RT_K_GEMM_GATE_UP: case RT_K_GEMM_DOWN:
+    case RT_K_GEMM_CONTEXT: case RT_K_GEMM_COND: case RT_K_ATTENTION: case RT_K_ATTN_MERGE:
+    case RT_K_LM_HEAD: break;
+    default: return fail(RT_ERR_INVALID, "kernel class %d cannot be replayed (it writes KV or round state)", kind);
+  }
+  if (reps < 1 || reps > 1000) return fail(RT_ERR_INVALID, "reps must be in [1, 1000]");
+  const Plan& q = p;
+  std::vector<int32_t> st((size_t)n_seqs * kStateFields);
+  HIPCHK(hipStreamSynchronize(stream));
+  HIPCHK(hipMemcpy(st.data(), ws + q.state, st.size() * 4, hipMemcpyDeviceToHost));
+  prof_ctx.assign(n_seqs, 0);
+  for (int s = 0; s < n_seqs; ++s) prof_ctx[s] = st[(size_t)s * kStateFields + ST_SEQ_LEN];
+  only_kind = kind;
+  only_launches = 0;
+  only_bytes = only_flops = 0;
+  launch_events() = LaunchEvents{};
+  launch_events().skip = true;
+  hipGraph_t g = nullptr;
+  hipError_t be = hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal);
+  int rc = be == hipSuccess ? run_round(false) : RT_OK;
+  hipError_t ce = be == hipSuccess ? hipStreamEndCapture(stream, &g) : be;
+  only_kind = -1;
+  launch_events() = LaunchEvents{};
+  if (rc != RT_OK) { if (g) (void)hipGraphDestroy(g); return rc; }
+  if (ce != hipSuccess) { if (g) (void)hipGraphDestroy(g); return fail(RT_ERR_HIP, "replay capture: %s", hipGetErrorString(ce)); }
+  hipGraphExec_t ge = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  auto cleanup = [&]() {
+    if (ge) (void)hipGraphExecDestroy(ge);
+    if (g) (void)hipGraphDestroy(g);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+  };
+  hipError_t e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = hipGraphLaunch(ge, stream);          // warm-up
+  if (e == hipSuccess) e = hipEventRecord(e0, stream);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = hipGraphLaunch(ge, stream);
+  if (e == hipSuccess) e = hipEventRecord(e1, stream);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  cleanup();
+  if (e != hipSuccess) return fail(RT_ERR_HIP, "kernel replay: %s", hipGetErrorString(e));
+  out->kind = kind;
+  out->launches = only_launches;
+  out->ms = only_launches ? ms / reps : 0.0;
+  out->bytes = only_bytes;
+  out->flops = only_flops;
   return RT_OK;
 }
 
@@ -732,6 +836,16 @@ int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32
     return m->e->profile_round(stats, stage_ms, tokens, n_committed, accept_len);
   } catch (...) {
     return fail(RT_ERR_INVALID, "unexpected exception in rt_profile_round");
+  }
+}
+
+int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    if (!stat) return fail(RT_ERR_INVALID, "null pointer argument");
+    return m->e->time_kernel(kind, reps, stat);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_time_kernel");
   }
 }
 

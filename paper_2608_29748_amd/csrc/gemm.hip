@@ -41,14 +41,14 @@ void pack_weights(const T* W, int N, int K, int Kp, T* out, hipStream_t s) {
   size_t total = (size_t)(N / kTileN) * (Kp / kTileK) * kWave;
   int grid = (int)((total + 255) / 256);
   if (grid > 65535 * 4) grid = 65535 * 4;
-  hipLaunchKernelGGL(pack_kernel<T>, dim3(grid), dim3(256), 0, s, W, (const T*)nullptr, N, K, Kp, out);
+  RT_LAUNCH(pack_kernel<T>, dim3(grid), dim3(256), 0, s, W, (const T*)nullptr, N, K, Kp, out);
 }
 template <typename T>
 void pack_interleaved(const T* Wa, const T* Wb, int N, int K, int Kp, T* out, hipStream_t s) {
   size_t total = (size_t)2 * (N / kTileN) * (Kp / kTileK) * kWave;
   int grid = (int)((total + 255) / 256);
   if (grid > 65535 * 4) grid = 65535 * 4;
-  hipLaunchKernelGGL(pack_kernel<T>, dim3(grid), dim3(256), 0, s, Wa, Wb, N, K, Kp, out);
+  RT_LAUNCH(pack_kernel<T>, dim3(grid), dim3(256), 0, s, Wa, Wb, N, K, Kp, out);
 }
 template void pack_weights<bf16_t>(const bf16_t*, int, int, int, bf16_t*, hipStream_t);
 template void pack_weights<float>(const float*, int, int, int, float*, hipStream_t);
@@ -336,20 +336,20 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
     if (M > 32) return hipErrorInvalidValue;
     dim3 grid((N + 15) / 16, 1, 1);
     if (a_f32) {
-      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
     } else if (N >= 5120) {        // 32-column tiles: half the activation re-reads, >= 160 workgroups
       dim3 g2((N + 31) / 32, 1, 1);
-      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, false, 2, 2, 8, 8>), g2, dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((gemm16_kernel<T, false, 1, 2, 8, 8>), g2, dim3(512), 0, s, a);
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 2, 8, 8>), g2, dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 2, 8, 8>), g2, dim3(512), 0, s, a);
     } else {
-      if (M > 16) hipLaunchKernelGGL((gemm16_kernel<T, false, 2, 1, 8, 8>), grid, dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 8>), grid, dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);
     }
   } else {
     dim3 grid((N + 127) / 128, (M + 127) / 128, a.ksplit);
-    if (a_f32) hipLaunchKernelGGL((gemm_wide_kernel<T, true, 4, 4, 2, 2, 1>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((gemm_wide_kernel<T, false, 4, 4, 2, 2, 2>), grid, dim3(256), 0, s, a);
+    if (a_f32) RT_LAUNCH((gemm_wide_kernel<T, true, 4, 4, 2, 2, 1>), grid, dim3(256), 0, s, a);
+    else RT_LAUNCH((gemm_wide_kernel<T, false, 4, 4, 2, 2, 2>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -415,7 +415,7 @@ hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s) {
   const int heads = (a.layer_cols / a.head_dim) * a.n_layers;
   const long long items = (long long)a.M * heads;
   if (items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s, a);
+  RT_LAUNCH(qkv_post_kernel<T>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 template hipError_t qkv_post<bf16_t>(const QkvPostArgs&, hipStream_t);
@@ -537,8 +537,8 @@ hipError_t lm_head(const LmHeadArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.M > 32) return hipErrorInvalidValue;
   dim3 grid(lmhead_grid(a.N));
-  if (a.M > 16) hipLaunchKernelGGL((lmhead_kernel<T, 2, 8>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((lmhead_kernel<T, 1, 8>), grid, dim3(256), 0, s, a);
+  if (a.M > 16) RT_LAUNCH((lmhead_kernel<T, 2, 8>), grid, dim3(256), 0, s, a);
+  else RT_LAUNCH((lmhead_kernel<T, 1, 8>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 template hipError_t lm_head<bf16_t>(const LmHeadArgs&, hipStream_t);
@@ -567,7 +567,7 @@ __global__ __launch_bounds__(256) void argmax_reduce_kernel(const uint64_t* __re
 }
 hipError_t argmax_reduce(const uint64_t* part_keys, int nparts, int M, uint64_t* keys, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(M), dim3(256), 0, s, part_keys, nparts, M, keys);
+  RT_LAUNCH(argmax_reduce_kernel, dim3(M), dim3(256), 0, s, part_keys, nparts, M, keys);
   return hipGetLastError();
 }
 

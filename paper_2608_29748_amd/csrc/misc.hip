@@ -57,7 +57,7 @@ template <typename T, typename K>
 void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
              K* keep, int ldk, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg,
+  RT_LAUNCH((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg,
                      keep, ldk);
 }
 template void rmsnorm<bf16_t, uint16_t>(const float*, int, const bf16_t*, int, float, int, bf16_t*, int,
@@ -76,7 +76,7 @@ __global__ void embed_rows_kernel(const T* __restrict__ E, int d, const int32_t*
 template <typename T>
 void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL((embed_rows_kernel<T>), dim3(rows), dim3(256), 0, s, embed, d, tokens, x, ldx);
+  RT_LAUNCH((embed_rows_kernel<T>), dim3(rows), dim3(256), 0, s, embed, d, tokens, x, ldx);
 }
 
 template <typename T>
@@ -94,7 +94,7 @@ __global__ void embed_block_kernel(const T* __restrict__ E, int d, const int32_t
 template <typename T>
 void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk,
                  float* x, float* etilde, int ldx, hipStream_t s) {
-  hipLaunchKernelGGL((embed_block_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
+  RT_LAUNCH((embed_block_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
                      mask_token, bk, x, etilde, ldx);
 }
 
@@ -114,7 +114,7 @@ __global__ void embed_verify_kernel(const T* __restrict__ E, int d, const int32_
 template <typename T>
 void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* dkeys, int forced,
                   int32_t* dtok, int n_seqs, int bk, float* x, int ldx, hipStream_t s) {
-  hipLaunchKernelGGL((embed_verify_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state, dkeys,
+  RT_LAUNCH((embed_verify_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state, dkeys,
                      forced, dtok, bk, x, ldx);
 }
 
@@ -144,7 +144,7 @@ __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* 
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
                int n_seqs, int bk, float* mu, float* er, int ldg, hipStream_t s) {
-  hipLaunchKernelGGL((cond_prep_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
+  RT_LAUNCH((cond_prep_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
                      mask_token, hD, hT, bk, mu, er, ldg);
 }
 
@@ -192,7 +192,7 @@ __global__ void accept_kernel(int32_t* st_all, const int32_t* __restrict__ dtok,
 }
 void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs, int bk,
             int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s) {
-  hipLaunchKernelGGL(accept_kernel, dim3(n_seqs), dim3(64), 0, s, state, dtok, tkeys, ttok, bk, out_tokens,
+  RT_LAUNCH(accept_kernel, dim3(n_seqs), dim3(64), 0, s, state, dtok, tkeys, ttok, bk, out_tokens,
                      out_n, out_a);
 }
 
@@ -201,7 +201,7 @@ __global__ void set_ints_kernel(int32_t* dst, int n, int v0, int v1, int v2, int
   if (threadIdx.x < n && threadIdx.x < 4) dst[threadIdx.x] = v[threadIdx.x];
 }
 void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s) {
-  hipLaunchKernelGGL(set_ints_kernel, dim3(1), dim3(64), 0, s, dst, n, v0, v1, v2, v3);
+  RT_LAUNCH(set_ints_kernel, dim3(1), dim3(64), 0, s, dst, n, v0, v1, v2, v3);
 }
 
 __global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys, int plen, int budget,
@@ -221,7 +221,7 @@ __global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys
 }
 void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
                  int32_t* first_out, hipStream_t s) {
-  hipLaunchKernelGGL(first_token_kernel, dim3(1), dim3(64), 0, s, state, seq, keys, prompt_len, budget,
+  RT_LAUNCH(first_token_kernel, dim3(1), dim3(64), 0, s, state, seq, keys, prompt_len, budget,
                      first_out);
 }
 
@@ -234,7 +234,7 @@ void fill_zero(void* p, size_t bytes, hipStream_t s) {
   if (n16 == 0) return;
   size_t g = (n16 + 255) / 256;
   if (g > 8192) g = 8192;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)g), dim3(256), 0, s, (uint4*)p, n16);
+  RT_LAUNCH(fill_zero_kernel, dim3((unsigned)g), dim3(256), 0, s, (uint4*)p, n16);
 }
 
 template void embed_rows<bf16_t>(const bf16_t*, int, const int32_t*, int, float*, int, hipStream_t);

@@ -59,6 +59,8 @@ int validate_config(const rt_config* c) {
   if (c->max_batch < 1 || c->max_batch > 1024) return fail(RT_ERR_INVALID, "max_batch must be in [1, 1024]");
   if (c->max_seq_len < c->block_size + 1 || c->max_seq_len > (1 << 20))
     return fail(RT_ERR_INVALID, "max_seq_len must be in [block_size + 1, 2^20]");
+  if (c->dtype == RT_F32 && c->max_seq_len > 16384)   // fp32 attention keeps a split's page ids in LDS
+    return fail(RT_ERR_INVALID, "fp32 storage supports max_seq_len up to 16384");
   if (c->page_size != 16) return fail(RT_ERR_INVALID, "page_size must be 16");
   return RT_OK;
 }
@@ -85,11 +87,13 @@ int make_plan(const rt_config* c, Plan* p) {
   q.Mrows = (int)rup((size_t)(q.R > q.PF ? q.R : q.PF), 128);
   q.attn_rb = (q.bk * q.G + 63) / 64;
   {
-    // key splits: about two workgroups per compute unit, each split at least 64 keys
+    // key splits: about one workgroup per compute unit, at most 64 (one per lane of the
+    // merge), and no more than the 64-key chunks of the longest sequence
     const int base = q.bmax * q.Hkv * q.attn_rb;
-    int sp = (512 + base - 1) / base;
+    int sp = (256 + base - 1) / base;
     const int maxsp = (q.T + 63) / 64;
     if (sp > maxsp) sp = maxsp;
+    if (sp > 64) sp = 64;
     if (sp < 1) sp = 1;
     q.attn_splits = sp;
   }

@@ -74,6 +74,9 @@ class RoundEngine:
     def profile_round(self):
         return B.rt_profile_round(self.h, self.n_seqs, self.cfg.block_size)
 
+    def time_kernel(self, kind: int, reps: int = 20) -> dict:
+        return B.rt_time_kernel(self.h, kind, reps)
+
     def set_debug(self, flags: int) -> None:
         B.rt_set_debug(self.h, flags)
 

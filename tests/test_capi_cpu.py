@@ -69,6 +69,7 @@ def test_workspace_and_weight_count(B):
     (dict(cond_mode=5), "cond_mode"),
     (dict(max_seq_len=4), "max_seq_len"),
     (dict(max_batch=0), "max_batch"),
+    (dict(dtype=0, max_seq_len=16385), "fp32 storage"),
 ])
 def test_invalid_configs_are_rejected(B, over, msg):
     c = cfg(B, **over)

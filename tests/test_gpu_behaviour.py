@@ -1,7 +1,8 @@
 """Round semantics on the GPU through the C ABI: planted drafts with known
 acceptance lengths, the carry / reset rule, losslessness against the oracle's
 target-only greedy decode, budget clipping, graph replay, the W_v = 0 and
-conditioning-off reductions, and error statuses."""
+conditioning-off reductions, error statuses, and measurement calls that leave the
+rounds unchanged."""
 import numpy as np
 import pytest
 
@@ -138,3 +139,47 @@ def test_error_statuses(tiny):
         eng.spec_round_forced(np.full((1, wl.B), -1, np.int32))
     assert ex.value.code == B.RT_ERR_TOKEN
     eng.close()
+
+
+def test_measurement_calls_leave_the_rounds_unchanged():
+    """A profiled round is an ordinary round (same outputs, every launch counted once),
+    and kernel replays of the scratch-writing classes change no KV and no carried state:
+    the rounds that follow match an engine that was never measured, bit for bit."""
+    wl = get("mini-bf16-ragged", norm_init="perturbed")
+    W = make_weights(wl)
+    prompts = make_prompts(wl)
+    L, LD = wl.target.n_layers, wl.draft_layers
+    runs = []
+    for measured in (False, True):
+        eng = engine_for(wl, W)
+        eng.prefill(prompts, wl.new_tokens)
+        out = _run(eng, 2)
+        if measured:
+            stats, stages, tok, n, a = eng.profile_round()
+            by = {s["kind"]: s for s in stats}
+            assert by["gemm_qkv"]["launches"] == L + LD
+            assert by["gemm_gate_up"]["launches"] == L + LD
+            assert by["attention"]["launches"] == L + LD
+            assert by["gemm_cond"]["launches"] == 3
+            assert all(s["ms"] > 0 for s in stats if s["launches"]), stats
+            assert len(stages) == 7 and all(x >= 0 for x in stages)
+            out.append((tok.copy(), n.copy(), a.copy(), eng.read(B.RT_T_HD, 0, (wl.block_size, wl.target.hidden),
+                                                                 np.uint16).copy()))
+            for kind in (B.RT_K_GEMM_QKV, B.RT_K_GEMM_O, B.RT_K_GEMM_GATE_UP, B.RT_K_GEMM_DOWN,
+                         B.RT_K_GEMM_CONTEXT, B.RT_K_GEMM_COND, B.RT_K_ATTENTION, B.RT_K_ATTN_MERGE,
+                         B.RT_K_LM_HEAD):
+                r = eng.time_kernel(kind, 2)
+                assert r["launches"] > 0 and r["ms"] > 0 and r["bytes"] > 0, r
+            for kind in (B.RT_K_NORM, B.RT_K_QKV_POST, B.RT_K_MISC):
+                with pytest.raises(B.RetraceError) as ex:
+                    eng.time_kernel(kind, 2)
+                assert ex.value.code == B.RT_ERR_INVALID
+        else:
+            out += _run(eng, 1)
+        out += _run(eng, 3)
+        runs.append(out)
+        eng.close()
+    for (t0, n0, a0, h0), (t1, n1, a1, h1) in zip(*runs):
+        np.testing.assert_array_equal(t0, t1)
+        np.testing.assert_array_equal(n0, n1)
+        np.testing.assert_array_equal(h0, h1)
