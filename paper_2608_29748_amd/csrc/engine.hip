@@ -122,6 +122,7 @@ struct Engine : EngineBase {
       case EPI_SWIGLU: return mn / 2 * sizeof(T);
       case EPI_COND_R: return mn * 8;
       case EPI_COND_GATE: return mn * 4;
+      case EPI_PARTIAL: return mn * 4 * kResidSplits;
       default: return mn * (12 + sizeof(T));   // EPI_COND_OUT: gate, e rows, x and etilde
     }
   }
@@ -148,6 +149,7 @@ struct Engine : EngineBase {
       while (ks > 1 && (size_t)tiles * ks * 128 * 128 > kPartialFloats) --ks;
       if (tiles > kMaxTiles) ks = 1;
     }
+    if (shape == SHAPE_SKINNY && e.kind == EPI_PARTIAL) ks = kResidSplits;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
     a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
@@ -171,15 +173,42 @@ struct Engine : EngineBase {
     T* cap;                      // packed capture buffer of the updated residual (null: none)
     int cap_k0;                  // column offset of this layer's slot in the capture
     const int32_t* prof_ctx;     // host copy of each sequence's context length (profiling only)
+    int defer;                   // o / down (<= 32 rows): k-slab partials, added by the next norm
   };
+  // partials of the last deferred residual GEMM, consumed by the next norm of x
+  NormFold pend{};
+  // RMSNorm of x (rows of the residual stream) into the packed xa operand, folding in
+  // any deferred residual partials first
+  void norm_x(const T* w, int rows, K* keep, int ldk) {
+    const Plan& q = p;
+    prof_begin(RT_K_NORM, (double)rows * q.d * (4 + sizeof(T) + (keep ? q.ksz : 0)) +
+                              (pend.n_part ? (double)rows * q.d * 4 * (pend.n_part + 1) : 0.0), 0);
+    rmsnorm<T, K>(at<float>(q.x), q.d, w, q.d, cfg.rms_eps, rows, at<T>(q.xa), 16 * q.Kp_d, keep, ldk, pend, stream);
+    prof_end();
+    pend = NormFold{};
+  }
+  // o / down projection with the residual add, deferred (k slabs) or in the epilogue
+  int resid_gemm(int kind, const LayerCtx& c, const void* A, int lda, const char* W, int Kp, int k_logical,
+                 bool capture) {
+    const Plan& q = p;
+    EpiArgs e{};
+    if (c.defer && c.M <= 32) {
+      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.rpart); e.ldo = q.d; e.part_stride = (size_t)32 * q.d;
+      CHK(gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical));
+      pend = NormFold{at<float>(q.rpart), kResidSplits, (size_t)32 * q.d, capture ? (void*)c.cap : nullptr,
+                      16 * q.Kp_nc, c.cap_k0};
+      return RT_OK;
+    }
+    e.kind = EPI_RESID; e.resid = at<float>(q.x); e.ldr = q.d;
+    if (capture) { e.cap = c.cap; e.ldcap = 16 * q.Kp_nc; e.cap_k0 = c.cap_k0; }
+    return gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical);
+  }
 
   int layer(const char* lw, const LayerCtx& c) {
     const Plan& q = p;
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
-    prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
-    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_in), q.d, cfg.rms_eps, c.M, xa, 16 * q.Kp_d, nullptr, 0, stream);
-    prof_end();
+    norm_x((const T*)(lw + q.lo_in), c.M, nullptr, 0);
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
     CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
@@ -217,18 +246,12 @@ struct Engine : EngineBase {
       HIPCHK(attention_merge<T>(a, stream));
       prof_end();
     }
-    e = EpiArgs{};
-    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d;
-    CHK(gemm_call(RT_K_GEMM_O, at<T>(q.attn), 16 * q.Kp_q, q.Mrows, false, lw + q.lo_o, q.d, q.Kp_q, c.M, e, q.qN));
-    prof_begin(RT_K_NORM, (double)c.M * q.d * (4 + sizeof(T)), 0);
-    rmsnorm<T, K>(x, q.d, (const T*)(lw + q.lo_post), q.d, cfg.rms_eps, c.M, xa, 16 * q.Kp_d, nullptr, 0, stream);
-    prof_end();
+    CHK(resid_gemm(RT_K_GEMM_O, c, at<T>(q.attn), 16 * q.Kp_q, lw + q.lo_o, q.Kp_q, q.qN, false));
+    norm_x((const T*)(lw + q.lo_post), c.M, nullptr, 0);
     e = EpiArgs{};
     e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = 16 * q.Kp_F;
     CHK(gemm_call(RT_K_GEMM_GATE_UP, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e, q.d));
-    e = EpiArgs{};
-    e.kind = EPI_RESID; e.resid = x; e.ldr = q.d; e.cap = c.cap; e.ldcap = 16 * q.Kp_nc; e.cap_k0 = c.cap_k0;
-    CHK(gemm_call(RT_K_GEMM_DOWN, at<T>(q.mlp), 16 * q.Kp_F, q.Mrows, false, lw + q.lo_down, q.d, q.Kp_F, c.M, e, q.F));
+    CHK(resid_gemm(RT_K_GEMM_DOWN, c, at<T>(q.mlp), 16 * q.Kp_F, lw + q.lo_down, q.Kp_F, q.F, c.cap != nullptr));
     return RT_OK;
   }
 
@@ -268,7 +291,7 @@ struct Engine : EngineBase {
     CHK(gemm_call(RT_K_GEMM_CONTEXT, at<T>(q.g), 16 * q.Kp_nc, q.Mrows, false, at<T>(q.fc), q.d, q.Kp_nc, M, e, q.nc * q.d));
     prof_begin(RT_K_NORM, (double)M * q.d * (4 + sizeof(T)), 0);
     rmsnorm<T, K>(at<float>(q.fcout), q.d, at<T>(q.hidden_norm), q.d, cfg.rms_eps, M, at<T>(q.fa), 16 * q.Kp_d,
-                  nullptr, 0, stream);
+                  nullptr, 0, NormFold{}, stream);
     prof_end();
     e = EpiArgs{};
     e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.LD * 2 * q.kvN;
@@ -380,7 +403,7 @@ struct Engine : EngineBase {
         CHK(context_append(n, q.PF, pf, nullptr, 0, pt));
         if (c0 + n == len) {
           rmsnorm<T, K>(at<float>(q.x) + (size_t)(n - 1) * q.d, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, 1,
-                        at<T>(q.xa), 16 * q.Kp_d, nullptr, 0, stream);
+                        at<T>(q.xa), 16 * q.Kp_d, nullptr, 0, NormFold{}, stream);
           CHK(lm_head_argmax(1, at<uint64_t>(q.tkeys), nullptr));
           first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), len, budget, at<int32_t>(q.first_tok), stream);
         }
@@ -438,14 +461,11 @@ struct Engine : EngineBase {
     for (int l = 0; l < q.LD; ++l) {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
-                 nullptr, 0, prof_ctx.data()};
+                 nullptr, 0, prof_ctx.data(), 1};
       CHK(layer(dlayer(l), c));
     }
     stage(2);
-    prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
-    rmsnorm<T, K>(x, q.d, at<T>(q.d_final_norm), q.d, cfg.rms_eps, R, xa, 16 * q.Kp_d, at<K>(q.hd_keep), q.d,
-                  stream);
-    prof_end();
+    norm_x(at<T>(q.d_final_norm), R, at<K>(q.hd_keep), q.d);
     CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (flags & 1) ? at<float>(q.dlogits) : nullptr));
     // (3) verify: [anchor, drafts] at P..P+B, causal over the target cache
     stage(3);
@@ -457,14 +477,11 @@ struct Engine : EngineBase {
       const int slot = cond_slot(l);
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
-                 slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data()};
+                 slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data(), 1};
       CHK(layer(tlayer(l), c));
     }
     stage(4);
-    prof_begin(RT_K_NORM, (double)R * q.d * (4 + sizeof(T) + q.ksz), 0);
-    rmsnorm<T, K>(x, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, R, xa, 16 * q.Kp_d, at<K>(q.ht_keep), q.d,
-                  stream);
-    prof_end();
+    norm_x(at<T>(q.t_final_norm), R, at<K>(q.ht_keep), q.d);
     CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
     // (4) acceptance, commit, rollback, carry / reset
     stage(5);

@@ -21,6 +21,7 @@ enum EpiKind : int {
   EPI_COND_R,          // r = m + beta * y  -> out_f32 (the corrected signal, Eq.8)
   EPI_COND_GATE,       // out_f32 = sigmoid(y)                               (Eq.9 gate)
   EPI_COND_OUT,        // x = e + y * gate on conditioned rows, e elsewhere  (Eq.9)
+  EPI_PARTIAL,         // k slab z of a split reduction: out_f32[z * part_stride + m * ldo + n] = y
 };
 
 struct EpiArgs {
@@ -29,6 +30,7 @@ struct EpiArgs {
   // generic outputs: out_f32 row-major with ldo, except EPI_COND_R (packed, ldo = group
   // stride, columns offset by out_k0); out_act always packed (ldo = group stride)
   float* out_f32; void* out_act; int ldo; int out_k0;
+  size_t part_stride;            // EPI_PARTIAL: elements between the slabs of consecutive k splits
   float* resid; int ldr;
   void* cap; int ldcap; int cap_k0;   // packed capture of the updated residual (act type), may be null
   // per-row sequence mapping
@@ -48,7 +50,8 @@ struct EpiArgs {
 struct GemmArgs {
   const void* A; int lda; int a_rows;     // packed A: lda = group stride (elements); rows allocated
   const void* B; int Kp;                  // packed weights, K padded to a multiple of 32
-  int ksplit;
+  int ksplit;                             // wide: k splits summed by the last workgroup; skinny:
+                                          // k slabs, only with EPI_PARTIAL (one slab per grid z)
   float* partial; uint32_t* counters;
   EpiArgs e;
 };

@@ -124,6 +124,7 @@ __device__ void run_epilogue(const EpiArgs& e, float (*t)[LDT], int m0, int n0) 
         e.out_f32[pa_index(m, e.out_k0 + n, e.ldo)] = e.cond_m[pa_index(m, n, e.ld_cond_m)] + e.beta * y;
         break;
       case EPI_COND_GATE: e.out_f32[(size_t)m * e.ldo + n] = 1.0f / (1.0f + expf(-y)); break;
+      case EPI_PARTIAL: e.out_f32[(size_t)blockIdx.z * e.part_stride + (size_t)m * e.ldo + n] = y; break;
       default: {  // EPI_COND_OUT
         const int s = m / e.rows_per_seq, j = m % e.rows_per_seq;
         const int tok = (j == 0) ? e.anchor[s * e.seq_stride] : e.mask_token;
@@ -152,7 +153,9 @@ __global__ __launch_bounds__(NW * 64) void gemm16_kernel(GemmArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m0 = blockIdx.y * ROWS, n0 = blockIdx.x * COLS;
   const int KT = a.Kp / kTileK;
-  const int kb = KT * w / NW, ke = KT * (w + 1) / NW;
+  // k slab blockIdx.z of gridDim.z, split again over the waves
+  const int part = blockIdx.z * NW + w, parts = gridDim.z * NW;
+  const int kb = KT * part / parts, ke = KT * (part + 1) / parts;
   const int n_tiles_valid = a.e.N / kTileN;
   const T* bptr[NT];
 #pragma unroll
@@ -326,7 +329,9 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
 }
 
 int gemm_tile_rows(int shape, int M) { return shape == SHAPE_SKINNY ? (M > 16 ? 32 : 16) : 128; }
-int gemm_tile_cols(int shape, int N) { return shape == SHAPE_SKINNY ? (N >= 5120 ? 32 : 16) : 128; }
+int gemm_tile_cols(int shape, int N) {
+  return shape == SHAPE_SKINNY ? (N >= 5120 && N < 16384 ? 32 : 16) : 128;
+}
 
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
@@ -334,14 +339,24 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (shape == SHAPE_SKINNY) {
     if (M > 32) return hipErrorInvalidValue;
-    dim3 grid((N + 15) / 16, 1, 1);
+    // tile width, waves and loads in flight per shape class (measured on the Qwen3 layer
+    // shapes): split reductions 16 columns x 4 waves per slab; N >= 16384 (gate|up) 16
+    // columns; N >= 5120 32 columns; otherwise 16 columns with 8 loads in flight
+    if ((a.e.kind == EPI_PARTIAL) != (a.ksplit > 1) || a.ksplit < 1) return hipErrorInvalidValue;
+    dim3 grid((N + 15) / 16, 1, a.ksplit);
     if (a_f32) {
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
       else RT_LAUNCH((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
-    } else if (N >= 5120) {        // 32-column tiles: half the activation re-reads, >= 160 workgroups
+    } else if (a.ksplit > 1) {
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 4, 4>), grid, dim3(256), 0, s, a);
+    } else if (N >= 16384) {
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 4>), grid, dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 8, 4>), grid, dim3(512), 0, s, a);
+    } else if (N >= 5120) {
       dim3 g2((N + 31) / 32, 1, 1);
-      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 2, 8, 8>), g2, dim3(512), 0, s, a);
-      else RT_LAUNCH((gemm16_kernel<T, false, 1, 2, 8, 8>), g2, dim3(512), 0, s, a);
+      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 2, 8, 4>), g2, dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 2, 8, 4>), g2, dim3(512), 0, s, a);
     } else {
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 8>), grid, dim3(512), 0, s, a);
       else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);

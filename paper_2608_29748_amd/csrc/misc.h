@@ -18,10 +18,18 @@ enum StateField : int {
   kStateFields
 };
 
+// Pending k-slab partials of a GEMM whose residual add was deferred to the next norm:
+// slab z of row r is part[z * part_stride + r * ldx ..]; cap (optional) receives the
+// updated row, packed, at column offset cap_k0 (group stride ldcap).
+struct NormFold {
+  const float* part; int n_part; size_t part_stride;
+  void* cap; int ldcap; int cap_k0;
+};
 // out: packed GEMM-operand layout with group stride ldg; keep: optional row-major copy.
+// With fold.n_part > 0 the partials are summed and added to x first (x is updated).
 template <typename T, typename K>
-void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
-             K* keep, int ldk, hipStream_t s);
+void rmsnorm(float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
+             K* keep, int ldk, const NormFold& fold, hipStream_t s);
 template <typename T>
 void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s);
 // Drafter input without conditioning: row (s, 0) = E[anchor], rows (s, j>0) = E[mask].

@@ -9,25 +9,52 @@ template <> struct KeepT<float> { __device__ static float of(float v) { return v
 
 // One workgroup per row, single pass: each thread keeps its 8-element chunks of the row
 // in registers (hidden <= 8192), and writes the normalised row in the packed GEMM-operand
-// layout (one 8-element run per chunk) plus an optional row-major retained copy.
+// layout (one 8-element run per chunk) plus an optional row-major retained copy.  With a
+// fold, the pending k-slab partials of the producing GEMM are first summed (slab order)
+// and added to the row, which is written back (and optionally captured, packed).
 template <typename T, typename K>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, int ldx,
                                                       const T* __restrict__ w, int d, float eps,
-                                                      T* __restrict__ out, int ldg, K* keep, int ldk) {
+                                                      T* __restrict__ out, int ldg, K* keep, int ldk,
+                                                      NormFold fold) {
   __shared__ float red[4];
   const int row = blockIdx.x;
-  const float* xr = x + (size_t)row * ldx;
+  float* xr = x + (size_t)row * ldx;
   const int nch = d / 8;
   float v[4][8];
+  Frag<T> wf[4];
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int c = threadIdx.x + j * 256;
     if (c < nch) {
+      wf[j].load(w + 8 * c);
       const float4 a = *reinterpret_cast<const float4*>(xr + 8 * c);
       const float4 b = *reinterpret_cast<const float4*>(xr + 8 * c + 4);
       v[j][0] = a.x; v[j][1] = a.y; v[j][2] = a.z; v[j][3] = a.w;
       v[j][4] = b.x; v[j][5] = b.y; v[j][6] = b.z; v[j][7] = b.w;
+      if (fold.n_part > 0) {
+        float t[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[e] = 0.f;
+        for (int z = 0; z < fold.n_part; ++z) {
+          const float* pz = fold.part + z * fold.part_stride + (size_t)row * ldx + 8 * c;
+          const float4 p0 = *reinterpret_cast<const float4*>(pz);
+          const float4 p1 = *reinterpret_cast<const float4*>(pz + 4);
+          t[0] += p0.x; t[1] += p0.y; t[2] += p0.z; t[3] += p0.w;
+          t[4] += p1.x; t[5] += p1.y; t[6] += p1.z; t[7] += p1.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[j][e] += t[e];
+        *reinterpret_cast<float4*>(xr + 8 * c) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+        *reinterpret_cast<float4*>(xr + 8 * c + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+        if (fold.cap) {
+          Frag<T> cf;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) cf.set(e, v[j][e]);
+          cf.store((T*)fold.cap + pa_index(row, fold.cap_k0 + 8 * c, (size_t)fold.ldcap));
+        }
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) ss += v[j][e] * v[j][e];
     }
@@ -44,7 +71,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
       Frag<T> f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float y = v[j][e] * inv * Elem<T>::to_f32(w[8 * c + e]);
+        const float y = v[j][e] * inv * wf[j].get(e);
         f.set(e, y);
         if (keep) keep[(size_t)row * ldk + 8 * c + e] = KeepT<K>::of(y);
       }
@@ -54,16 +81,16 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 }
 
 template <typename T, typename K>
-void rmsnorm(const float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
-             K* keep, int ldk, hipStream_t s) {
+void rmsnorm(float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
+             K* keep, int ldk, const NormFold& fold, hipStream_t s) {
   if (rows <= 0) return;
   RT_LAUNCH((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg,
-                     keep, ldk);
+            keep, ldk, fold);
 }
-template void rmsnorm<bf16_t, uint16_t>(const float*, int, const bf16_t*, int, float, int, bf16_t*, int,
-                                        uint16_t*, int, hipStream_t);
-template void rmsnorm<float, float>(const float*, int, const float*, int, float, int, float*, int,
-                                    float*, int, hipStream_t);
+template void rmsnorm<bf16_t, uint16_t>(float*, int, const bf16_t*, int, float, int, bf16_t*, int,
+                                        uint16_t*, int, const NormFold&, hipStream_t);
+template void rmsnorm<float, float>(float*, int, const float*, int, float, int, float*, int,
+                                    float*, int, const NormFold&, hipStream_t);
 
 // ------------------------------------------------------------------ embeddings
 template <typename T>

@@ -141,6 +141,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.first_tok = take((size_t)q.bmax * 4);
   q.counters = take((size_t)kMaxTiles * 4);
   q.partial = take(kPartialFloats * 4);
+  q.rpart = take((size_t)kResidSplits * 32 * q.d * 4);
   {
     size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
     size_t blocks = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits;
