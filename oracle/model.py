@@ -92,9 +92,12 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray,
 # ---------------------------------------------------------------- weights
 
 class Weights:
-    """Float64 views of the stored tensors, converted on first use."""
+    """Float64 views of the stored tensors, converted on first use.  cache=True keeps
+    the float64 copies; cache="f32" keeps float32 copies (exact for bf16 and fp32
+    storage) and widens them on every use, at half the memory; cache=False keeps
+    nothing."""
 
-    def __init__(self, stored: Dict[str, np.ndarray], cache: bool = True):
+    def __init__(self, stored: Dict[str, np.ndarray], cache=True):
         self.stored = stored
         self.cache = cache
         self._f64: Dict[str, np.ndarray] = {}
@@ -102,9 +105,15 @@ class Weights:
     def __getitem__(self, name: str) -> np.ndarray:
         w = self._f64.get(name)
         if w is None:
-            w = as_f32(self.stored[name]).astype(np.float64)
+            w32 = as_f32(self.stored[name])
+            if self.cache == "f32":
+                self._f64[name] = w32
+                return w32.astype(np.float64)
+            w = w32.astype(np.float64)
             if self.cache:
                 self._f64[name] = w
+        elif w.dtype != np.float64:
+            return w.astype(np.float64)
         return w
 
     def rows(self, name: str, idx) -> np.ndarray:
@@ -154,7 +163,7 @@ class VerifyOut:
 
 class OracleModel:
     def __init__(self, wl: Workload, stored: Dict[str, np.ndarray],
-                 prec: Optional[Precision] = None, cache: bool = True):
+                 prec: Optional[Precision] = None, cache=True):
         self.wl = wl
         self.s = wl.target
         self.W = Weights(stored, cache)

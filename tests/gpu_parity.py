@@ -123,20 +123,22 @@ def kv_check(rep, name, g, ref, tol, wl, what, exact=None):
     assert rel <= rel_bound and e <= abs_bound, f"{what}: relative error {rel} (bound {rel_bound}), max abs {e}"
 
 
-def compare_prefill(eng, R, wl, prompts, seq_states, tol, layers=None, exact_states=None):
+def compare_prefill(eng, R, wl, prompts, seq_states, tol, layers=None, exact_states=None, gpu_seqs=None):
     """Target and drafter-context KV of every prompt position (exact_states: the same
-    prefill by the float64 oracle, which calibrates the bf16 bound)."""
+    prefill by the float64 oracle, which calibrates the bf16 bound).  gpu_seqs[i] is
+    the GPU sequence that prompts[i] / seq_states[i] describe (default: i)."""
     s = wl.target
     et = np.uint16 if wl.dtype == "bf16" else np.float32
     rep = Report()
-    for b, st in enumerate(seq_states):
-        n = len(prompts[b])
+    for i, st in enumerate(seq_states):
+        b = gpu_seqs[i] if gpu_seqs is not None else i
+        n = len(prompts[i])
         for l in (layers if layers is not None else range(s.n_layers)):
             for tid, ref in ((B.RT_T_TARGET_K + l, st.tgt_k[l]), (B.RT_T_TARGET_V + l, st.tgt_v[l])):
                 g = store_to_f64(eng.read(tid, b, (n, s.n_kv_heads, s.head_dim), et), wl)
                 ex = None
                 if exact_states is not None:
-                    xs = exact_states[b]
+                    xs = exact_states[i]
                     ex = (xs.tgt_k if tid < B.RT_T_TARGET_V else xs.tgt_v)[l][:n]
                 kv_check(rep, "target_kv", g, ref[:n], tol, wl, f"seq {b} layer {l} target kv", ex)
         for l in range(wl.draft_layers):
@@ -144,7 +146,7 @@ def compare_prefill(eng, R, wl, prompts, seq_states, tol, layers=None, exact_sta
                 g = store_to_f64(eng.read(tid, b, (n, s.n_kv_heads, s.head_dim), et), wl)
                 ex = None
                 if exact_states is not None:
-                    xs = exact_states[b]
+                    xs = exact_states[i]
                     ex = (xs.ctx_k if tid < B.RT_T_DRAFT_V else xs.ctx_v)[l][:n]
                 kv_check(rep, "draft_ctx_kv", g, ref[:n], tol, wl, f"seq {b} drafter layer {l} ctx kv", ex)
     return rep
@@ -179,6 +181,7 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
     against the oracle continuing from the same decisions.  With inject, every
     round starts the oracle from the GPU's carried state, so each comparison
     measures one round.  forced: optional list (per round) of [n_seqs][B] drafts.
+    seq_states[b] = None leaves GPU sequence b unchecked (sampled batches).
 
     exact: a float64 runner of the same model.  The absolute tolerance then widens,
     per tensor, to twice the mixed-precision oracle's own distance from float64
@@ -192,12 +195,14 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
     kd = keep_dtype(wl)
     ns = len(seq_states)
     for t in range(n_rounds):
-        carried = [carried_state(eng, b, wl) if inject else None for b in range(ns)]
+        carried = [carried_state(eng, b, wl) if inject and seq_states[b] is not None else None for b in range(ns)]
         if forced is not None:
             tok, n_c, acc = eng.spec_round_forced(forced[t])
         else:
             tok, n_c, acc = eng.spec_round()
         for b, st in enumerate(seq_states):
+            if st is None:        # sequence not sampled
+                continue
             if st.done:
                 assert n_c[b] == 0
                 continue

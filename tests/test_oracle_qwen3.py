@@ -105,3 +105,18 @@ def test_incremental_decode_matches_full_forward(tiny):
     b = m.target_forward(st, prompt[40:56], 40).logits
     c = m.target_forward(st, prompt[56:57], 56).logits
     np.testing.assert_allclose(np.concatenate([a, b, c]), full[:57], atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16"])
+def test_weight_cache_modes_are_bit_identical(name):
+    """The float32 weight cache (used for the largest shapes) widens stored bf16 / fp32
+    values exactly, so every result equals the float64-cache oracle bit for bit."""
+    wl = get(name, norm_init="perturbed")
+    W = make_weights(wl)
+    prompt = make_prompts(wl)[0][:24]
+    outs = []
+    for cache in (True, "f32", False):
+        m = OracleModel(wl, W, cache=cache)
+        outs.append(m.target_forward(m.new_state(prompt, 0), prompt, 0).logits)
+    np.testing.assert_array_equal(outs[0], outs[1])
+    np.testing.assert_array_equal(outs[0], outs[2])
