@@ -17,14 +17,17 @@ struct AttnArgs {
   int causal;                    // 1: key position <= query position; 0: every key below pos0+nq
   int n_q_heads, n_kv_heads, head_dim;
   int splits;                    // key-range splits per (seq, kv head, row block)
-  int row_blocks;                // row blocks of 64 (token, head) rows per sequence
+  int row_blocks;                // row blocks of rb_rows (token, head) rows per sequence
+  int rb_rows;                   // rows per block: 64, or 96 (bf16) when a sequence has 65..96 rows
   float* opart; float* mlpart;   // split partials
   void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)
 };
 
-// Number of query (token, head) rows handled by one workgroup.
+// Query (token, head) rows handled by one workgroup: 64, or 96 for bf16 blocks of 65..96
+// rows (a GQA group of 5 over a 16-token block), so that every KV head is read once.
 constexpr int kAttnRows = 64;
+constexpr int kAttnRowsMax = 96;
 
 // attention = attention_partials (per key split) then attention_merge (splits > 1).
 template <typename T>
@@ -33,6 +36,6 @@ template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s);
 template <typename T>
 hipError_t attention_merge(const AttnArgs& a, hipStream_t s);
-size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim);
+size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim, int rb_rows);
 
 }  // namespace rt

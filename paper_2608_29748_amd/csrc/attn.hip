@@ -18,8 +18,8 @@ namespace rt {
 constexpr int kChunk = 64;      // keys per LDS chunk (four pages)
 constexpr int kMaxSplitPages = 1024;   // fp32 path: page ids of one split held in LDS (16384 keys)
 
-size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim) {
-  return (size_t)n_seqs * n_kv_heads * row_blocks * splits * kAttnRows * head_dim;
+size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim, int rb_rows) {
+  return (size_t)n_seqs * n_kv_heads * row_blocks * splits * rb_rows * head_dim;
 }
 
 // Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
@@ -238,23 +238,8 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
   }
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(4))) const int32_t const_i32_t;
 
-// Workgroup barrier that orders LDS accesses for the compiler but does not wait for
-// outstanding vector-memory operations (the direct-to-LDS copies are waited for
-// explicitly with wait_vm, so that later stages stay in flight).
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
-}
 __device__ __forceinline__ short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
 __device__ __forceinline__ float bf16_value(short b) { return __uint_as_float(((uint32_t)(uint16_t)b) << 16); }
 
@@ -263,8 +248,8 @@ __device__ __forceinline__ float bf16_value(short b) { return __uint_as_float(((
 template <int NPR>
 __device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)) & (NPR - 1); }
 
-// Work split of a workgroup: wave w owns query rows rh*32..rh*32+31 of the row block
-// (rh = w/2, two 16-row MFMA tiles) and keys kh*32..kh*32+31 of every 64-key chunk
+// Work split of a workgroup: wave w owns query rows rh*16*NRT .. +16*NRT-1 of the row
+// block (rh = w/2, NRT 16-row MFMA tiles) and keys kh*32..kh*32+31 of every 64-key chunk
 // (kh = w%2, two pages); the two key halves of the same rows are merged through LDS at
 // the end.  Every K / V byte staged in LDS is read by two waves.
 //
@@ -273,7 +258,7 @@ __device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)
 // consecutive keys 8g..8g+7 (tau = 0: 8g..8g+3, tau = 1: 8g+4..8g+7).  Those eight
 // probabilities are exactly the lane's B operand of O^T += V^T P^T, and its V^T operand
 // is one contiguous 16-byte piece of a V page row.
-template <int HD, int NSTAGE>
+template <int HD, int NSTAGE, int NRT>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int ROWB = HD * 2;                 // bytes of one K row (one token)
   constexpr int NPR = ROWB / 16;               // 16-byte pieces per K row
@@ -283,7 +268,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int STG = 2 * PAGES * PGB;         // one stage: 4 K slices, then 4 V slices
   constexpr int NHT = HD / 16, NKS = HD / 32;
   constexpr int OPITCH = HD + 4;               // fp32 row pitch of the key-half merge buffer
-  constexpr int MERGE = 2 * 32 * OPITCH * 4 + 2 * 32 * 2 * 4;
+  constexpr int RH = 16 * NRT;                 // rows per wave
+  constexpr int RBR = 2 * RH;                  // rows per workgroup (row block)
+  constexpr int MERGE = 2 * RH * OPITCH * 4 + 2 * RH * 2 * 4;
   constexpr int SMEM = NSTAGE * STG > MERGE ? NSTAGE * STG : MERGE;
   static_assert(PAGES == 4, "one page per wave");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -297,9 +284,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int P = a.pos0[s * a.seq_stride];
   const int nrows = nq * G;
-  const int row0 = rb * kAttnRows;
+  const int row0 = rb * RBR;
   if (row0 >= nrows) return;
-  const int last_tok = min(nrows, row0 + kAttnRows) - 1;
+  const int last_tok = min(nrows, row0 + RBR) - 1;
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end), kv_end >= 1
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
   // chunks spread evenly over the splits (counts differ by at most one)
@@ -333,13 +320,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
   };
 
-  // this wave's queries: tile t2 (0, 1) column c16 is row row0 + rh*32 + t2*16 + c16
-  const int nrt = min(2, max(0, (nrows - row0 - rh * 32 + 15) / 16));   // tiles with valid rows
-  Frag<bf16_t> qf[2][NKS];
-  int qpos[2];
+  // this wave's queries: tile t2 (0..NRT-1) column c16 is row row0 + rh*RH + t2*16 + c16
+  const int nrt = min(NRT, max(0, (nrows - row0 - rh * RH + 15) / 16));   // tiles with valid rows
+  Frag<bf16_t> qf[NRT][NKS];
+  int qpos[NRT];
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
-    const int qrow = row0 + rh * 32 + t2 * 16 + c16;
+  for (int t2 = 0; t2 < NRT; ++t2) {
+    const int qrow = row0 + rh * RH + t2 * 16 + c16;
     const int r = min(qrow, nrows - 1);
     qpos[t2] = P + r / G;
     const int tok = r / G, h = kvh * G + r % G;
@@ -348,11 +335,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].load(qp + ks * 32 + g4 * 8);
   }
   const float sl2 = a.scale * 1.4426950408889634f;
-  float mref[2] = {-INFINITY, -INFINITY};   // reference max (log2 units); raised lazily
-  float lsum[2] = {0.f, 0.f};               // this lane's share of the softmax denominator
-  f32x4 o[2][NHT];
+  float mref[NRT], lsum[NRT];   // reference max (log2 units), raised lazily; this lane's share of the sum
+  f32x4 o[NRT][NHT];
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2)
+  for (int t2 = 0; t2 < NRT; ++t2) {
+    mref[t2] = -INFINITY;
+    lsum[t2] = 0.f;
+  }
+#pragma unroll
+  for (int t2 = 0; t2 < NRT; ++t2)
 #pragma unroll
     for (int t = 0; t < NHT; ++t) o[t2][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -396,7 +387,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       vf[t].v = *reinterpret_cast<const bf16x8*>(sv + pg * PGB + h * 32 + ((g4 & 1) ^ ((h >> 3) & 1)) * 16);
     }
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
+    for (int t2 = 0; t2 < NRT; ++t2) {
       if (t2 >= nrt) break;
       // S^T = K Q^T: two 16-key tiles of this query tile
       f32x4 st[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
@@ -451,7 +442,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     }
   }
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
+  for (int t2 = 0; t2 < NRT; ++t2) {
     lsum[t2] += __shfl_xor(lsum[t2], 16, 64);
     lsum[t2] += __shfl_xor(lsum[t2], 32, 64);
   }
@@ -459,11 +450,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   // merge the two key halves of each row pair of waves through LDS (stages are free
   // once every wave has passed this barrier)
   lds_barrier();
-  float* mo = reinterpret_cast<float*>(smem) + rh * 32 * OPITCH;             // [32][OPITCH] O^T rows
-  float* mml = reinterpret_cast<float*>(smem) + 2 * 32 * OPITCH + rh * 64;    // [32][2] (m, l)
+  float* mo = reinterpret_cast<float*>(smem) + rh * RH * OPITCH;             // [RH][OPITCH] O^T rows
+  float* mml = reinterpret_cast<float*>(smem) + 2 * RH * OPITCH + rh * RH * 2;  // [RH][2] (m, l)
   if (kh == 1) {
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
+    for (int t2 = 0; t2 < NRT; ++t2) {
       const int rl = t2 * 16 + c16;
 #pragma unroll
       for (int t = 0; t < NHT; ++t)
@@ -475,7 +466,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   lds_barrier();
   if (kh == 1) return;
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
+  for (int t2 = 0; t2 < NRT; ++t2) {
     const int rl = t2 * 16 + c16;
     const float m1 = mml[rl * 2], l1 = mml[rl * 2 + 1];
     const float m0 = mref[t2];
@@ -491,7 +482,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       o[t2][t][2] = f0 * o[t2][t][2] + f1 * v1.z;
       o[t2][t][3] = f0 * o[t2][t][3] + f1 * v1.w;
     }
-    const int qrow = row0 + rh * 32 + rl;
+    const int qrow = row0 + rh * RH + rl;
     if (a.splits == 1) {
       if (qrow < nrows) {
         const int tok = qrow / G, h = kvh * G + qrow % G;
@@ -506,9 +497,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       }
     } else {
       const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
-      float* op = a.opart + blk * kAttnRows * HD;
-      float* ml = a.mlpart + blk * kAttnRows * 2;
-      const int rw = rh * 32 + rl;
+      float* op = a.opart + blk * RBR * HD;
+      float* ml = a.mlpart + blk * RBR * 2;
+      const int rw = rh * RH + rl;
 #pragma unroll
       for (int t = 0; t < NHT; ++t)
         *reinterpret_cast<float4*>(op + (size_t)rw * HD + t * 16 + 4 * g4) =
@@ -531,20 +522,22 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks, kvh = blockIdx.y;
   const int G = a.n_q_heads / a.n_kv_heads;
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
-  const int r = rb * kAttnRows + rl;
+  const int RBR = a.rb_rows;
+  if (rl >= RBR) return;
+  const int r = rb * RBR + rl;
   if (r >= nq * G) return;
   const int S = a.splits;                     // <= 64
   const size_t blk0 = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * S;
-  const float* opp = a.opart + (blk0 * kAttnRows + rl) * HD + lane;   // split j: + j * kAttnRows * HD
-  const float* mlp = a.mlpart + (blk0 * kAttnRows + rl) * 2;          // split j: + j * kAttnRows * 2
+  const float* opp = a.opart + (blk0 * RBR + rl) * HD + lane;   // split j: + j * RBR * HD
+  const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;          // split j: + j * RBR * 2
   float ob[NB][PL];
 #pragma unroll
   for (int j = 0; j < NB; ++j)
 #pragma unroll
-    for (int e = 0; e < PL; ++e) ob[j][e] = j < S ? opp[(size_t)j * kAttnRows * HD + 64 * e] : 0.f;
+    for (int e = 0; e < PL; ++e) ob[j][e] = j < S ? opp[(size_t)j * RBR * HD + 64 * e] : 0.f;
   float mj = -INFINITY, lj = 0.f;
   if (lane < S) {
-    const float2 v = *reinterpret_cast<const float2*>(mlp + (size_t)lane * kAttnRows * 2);
+    const float2 v = *reinterpret_cast<const float2*>(mlp + (size_t)lane * RBR * 2);
     mj = v.x;
     lj = v.y;
   }
@@ -564,7 +557,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
-      for (int e = 0; e < PL; ++e) ob[j][e] = j0 + j < S ? opp[(size_t)(j0 + j) * kAttnRows * HD + 64 * e] : 0.f;
+      for (int e = 0; e < PL; ++e) ob[j][e] = j0 + j < S ? opp[(size_t)(j0 + j) * RBR * HD + 64 * e] : 0.f;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j0 + j));
@@ -586,10 +579,19 @@ template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.splits, a.n_kv_heads, a.n_seqs * a.row_blocks);
   if constexpr (sizeof(T) == 2) {
-    if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages>), grid, dim3(256), 0, s, a);
-    else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages>), grid, dim3(256), 0, s, a);
-    else return hipErrorInvalidValue;
+    if (a.rb_rows == 96) {
+      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages, 3>), grid, dim3(256), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages, 3>), grid, dim3(256), 0, s, a);
+      else return hipErrorInvalidValue;
+    } else if (a.rb_rows == 64) {
+      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages, 2>), grid, dim3(256), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages, 2>), grid, dim3(256), 0, s, a);
+      else return hipErrorInvalidValue;
+    } else {
+      return hipErrorInvalidValue;
+    }
   } else {
+    if (a.rb_rows != kAttnRows) return hipErrorInvalidValue;
     if (a.head_dim == 128) RT_LAUNCH((attn_staged_kernel<T, 128>), grid, dim3(256), 0, s, a);
     else if (a.head_dim == 64) RT_LAUNCH((attn_staged_kernel<T, 64>), grid, dim3(256), 0, s, a);
     else return hipErrorInvalidValue;
@@ -599,7 +601,7 @@ hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
 template <typename T>
 hipError_t attention_merge(const AttnArgs& a, hipStream_t s) {
   if (a.splits <= 1) return hipSuccess;
-  dim3 grid(kAttnRows / 4, a.n_kv_heads, a.n_seqs * a.row_blocks);
+  dim3 grid(kAttnRowsMax / 4, a.n_kv_heads, a.n_seqs * a.row_blocks);
   if (a.head_dim == 128) RT_LAUNCH((attn_merge_kernel<T, 128>), grid, dim3(256), 0, s, a);
   else if (a.head_dim == 64) RT_LAUNCH((attn_merge_kernel<T, 64>), grid, dim3(256), 0, s, a);
   else return hipErrorInvalidValue;

@@ -132,6 +132,23 @@ __device__ __forceinline__ float warp_max(float v, int width = 64) {
   return v;
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Workgroup barrier that orders LDS accesses for the compiler but does not wait for
+// outstanding vector-memory operations (direct-to-LDS copies are waited for explicitly
+// with wait_vm, so that later pipeline stages stay in flight).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
 // Fragment-ordered ("packed") layout of GEMM A operands: element (m, k) of an [M][Kp]
 // operand lives at (m/16)*ldg + (k/32)*512 + ((m%16) + 16*((k%32)/8))*8 + k%8 with
 // ldg = 16*Kp, so the fragment one wave needs for a 16-row group and a 32-wide k tile is

@@ -136,7 +136,12 @@ struct Engine : EngineBase {
     const int shape = M > 32 ? SHAPE_WIDE : SHAPE_SKINNY;
     const int KT = Kp / 32;
     int ks = 1;
-    if (shape == SHAPE_WIDE) {
+    // bf16 GEMMs of 33..512 rows go to the mid-size kernel (no cross-workgroup split);
+    // the test hook (flags & 4) keeps them on the 128x128 split-k path instead
+    const bool mid = shape == SHAPE_WIDE && sizeof(T) == 2 && !af32 && M <= 512 && !(flags & 4) &&
+                     (e.kind == EPI_STORE_F32 || e.kind == EPI_STORE_ACT || e.kind == EPI_RESID ||
+                      e.kind == EPI_SWIGLU || e.kind == EPI_PARTIAL);
+    if (shape == SHAPE_WIDE && !mid) {
       const int tiles = ((N + 127) / 128) * ((M + 127) / 128);
       if (flags & 4) {                       // test hook: force a k split wherever possible
         ks = KT < 4 ? KT : 4;
@@ -149,7 +154,7 @@ struct Engine : EngineBase {
       while (ks > 1 && (size_t)tiles * ks * 128 * 128 > kPartialFloats) --ks;
       if (tiles > kMaxTiles) ks = 1;
     }
-    if (shape == SHAPE_SKINNY && e.kind == EPI_PARTIAL) ks = kResidSplits;
+    if (e.kind == EPI_PARTIAL) ks = kResidSplits;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
     a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
@@ -164,7 +169,7 @@ struct Engine : EngineBase {
   }
 
   struct LayerCtx {
-    int M, rows_per_seq, n_seqs, stride, causal, splits, rb;
+    int M, rows_per_seq, n_seqs, stride, causal, splits, rb, rb_rows;
     const int32_t* pos0;
     const int32_t* nq;
     const int32_t* pt;
@@ -192,11 +197,12 @@ struct Engine : EngineBase {
                  bool capture) {
     const Plan& q = p;
     EpiArgs e{};
-    if (c.defer && c.M <= 32) {
-      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.rpart); e.ldo = q.d; e.part_stride = (size_t)32 * q.d;
+    if (c.defer && c.M <= q.rpart_rows && (c.M <= 32 || (sizeof(T) == 2 && !(flags & 4)))) {
+      const size_t stride = (size_t)q.rpart_rows * q.d;
+      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.rpart); e.ldo = q.d; e.part_stride = stride;
       CHK(gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical));
-      pend = NormFold{at<float>(q.rpart), kResidSplits, (size_t)32 * q.d, capture ? (void*)c.cap : nullptr,
-                      16 * q.Kp_nc, c.cap_k0};
+      pend = NormFold{at<float>(q.rpart), kResidSplits, stride, capture ? (void*)c.cap : nullptr, 16 * q.Kp_nc,
+                      c.cap_k0};
       return RT_OK;
     }
     e.kind = EPI_RESID; e.resid = at<float>(q.x); e.ldr = q.d;
@@ -228,7 +234,8 @@ struct Engine : EngineBase {
     a.q = at<T>(q.qbuf); a.kcache = c.kc; a.vcache = c.vc; a.page_table = c.pt; a.max_pages = q.pages_per_seq;
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
-    a.splits = c.splits; a.row_blocks = c.rb; a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
+    a.splits = c.splits; a.row_blocks = c.rb; a.rb_rows = c.rb_rows;
+    a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
     if (instrumented()) {
       // keys read: every sequence's context plus the block, K and V, once per KV head
@@ -242,7 +249,7 @@ struct Engine : EngineBase {
     prof_end();
     if (a.splits > 1) {
       // partials: unnormalised O plus (max, sum) per (row, split), read once
-      prof_begin(RT_K_ATTN_MERGE, (double)a.splits * q.Hkv * c.rb * c.n_seqs * kAttnRows * (q.hd + 2) * 4.0, 0);
+      prof_begin(RT_K_ATTN_MERGE, (double)a.splits * q.Hkv * c.rb * c.n_seqs * c.rb_rows * (q.hd + 2) * 4.0, 0);
       HIPCHK(attention_merge<T>(a, stream));
       prof_end();
     }
@@ -395,7 +402,7 @@ struct Engine : EngineBase {
         embed_rows<T>(at<T>(q.embed), q.d, tok + c0, n, at<float>(q.x), q.d, stream);
         for (int l = 0; l < q.L; ++l) {
           const int slot = cond_slot(l);
-          LayerCtx c{n, q.PF, 1, 0, 1, 1, (n * q.G + 63) / 64, pf, pf + 1, pt,
+          LayerCtx c{n, q.PF, 1, 0, 1, 1, (n * q.G + kAttnRows - 1) / kAttnRows, kAttnRows, pf, pf + 1, pt,
                      at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
                      slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, &c0};
           CHK(layer(tlayer(l), c));
@@ -459,7 +466,7 @@ struct Engine : EngineBase {
     stage(1);
     // (2) drafter: B+1 rows at P..P+B over its context cache (no causal mask in the block)
     for (int l = 0; l < q.LD; ++l) {
-      LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
+      LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, q.attn_rows, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
                  nullptr, 0, prof_ctx.data(), 1};
       CHK(layer(dlayer(l), c));
@@ -475,7 +482,7 @@ struct Engine : EngineBase {
     prof_end();
     for (int l = 0; l < q.L; ++l) {
       const int slot = cond_slot(l);
-      LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, st + ST_SEQ_LEN, nullptr, pt,
+      LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, q.attn_rows, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
                  slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data(), 1};
       CHK(layer(tlayer(l), c));

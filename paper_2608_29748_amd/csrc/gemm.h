@@ -95,8 +95,13 @@ void pack_interleaved(const T* Wa, const T* Wb, int N, int K, int Kp, T* out, hi
 enum GemmShape : int { SHAPE_SKINNY = 0, SHAPE_WIDE = 1 };
 // SHAPE_SKINNY: M <= 32, 16 or 32-row tiles, the k range split across the workgroup's
 // waves and reduced in LDS (no ksplit).  SHAPE_WIDE: 128x128 tiles, optional ksplit.
+// SHAPE_WIDE with bf16 storage and a bf16 A operand goes to the mid-size kernel
+// (gemm_mid.hip) for 33..512 rows when its epilogue allows; otherwise 128x128 tiles.
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s);
+bool gemm_mid_supports(const GemmArgs& a);
+hipError_t gemm_mid(const GemmArgs& a, hipStream_t s);
+int gemm_mid_cols(int N);
 int gemm_tile_cols(int shape, int N);
 int gemm_tile_rows(int shape, int M);
 template <typename T>

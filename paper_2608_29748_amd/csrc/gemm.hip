@@ -362,6 +362,10 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
       else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 8, 8>), grid, dim3(512), 0, s, a);
     }
   } else {
+    if constexpr (sizeof(T) == 2) {
+      if (!a_f32 && gemm_mid_supports(a)) return gemm_mid(a, s);
+    }
+    if (a.e.kind == EPI_PARTIAL) return hipErrorInvalidValue;
     dim3 grid((N + 127) / 128, (M + 127) / 128, a.ksplit);
     if (a_f32) RT_LAUNCH((gemm_wide_kernel<T, true, 4, 4, 2, 2, 1>), grid, dim3(256), 0, s, a);
     else RT_LAUNCH((gemm_wide_kernel<T, false, 4, 4, 2, 2, 2>), grid, dim3(256), 0, s, a);

@@ -22,7 +22,7 @@ inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 constexpr int kPrefillChunk = 512;     // prompt rows per prefill pass
 constexpr int kMaxTiles = 1 << 16;     // split-K arrival counters
 constexpr size_t kPartialFloats = (size_t)8 << 20;   // split-K partial capacity (32 MiB)
-constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections (<= 32 rows)
+constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections
 
 struct Plan {
   // dimensions
@@ -33,6 +33,7 @@ struct Plan {
   int pages_per_seq, n_pages;
   int R, PF, Mrows;                      // round rows, prefill rows, allocated activation rows
   int attn_rb, attn_splits;              // round attention row blocks / key splits
+  int attn_rows;                         // round attention rows per block (64, or 96)
   int pf_rb;
   size_t cache_layer_elems;
   // byte offsets into the workspace
@@ -44,7 +45,8 @@ struct Plan {
   size_t x, xa, qbuf, attn, mlp, g, fcout, fa, etilde, mu, er, gate;
   size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
   size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys
-  size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplits][32][d]
+  size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplits][rpart_rows][d]
+  int rpart_rows;                // max(32, rows of a round)
   int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init
   size_t total;

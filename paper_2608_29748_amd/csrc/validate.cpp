@@ -85,13 +85,16 @@ int make_plan(const rt_config* c, Plan* p) {
   q.R = q.bmax * q.bk;
   q.PF = kPrefillChunk;
   q.Mrows = (int)rup((size_t)(q.R > q.PF ? q.R : q.PF), 128);
-  q.attn_rb = (q.bk * q.G + 63) / 64;
+  // one row block per sequence and KV head when the block has at most 96 (token, head)
+  // rows (bf16), so each KV head's keys are read once
+  q.attn_rows = (c->dtype == RT_BF16 && q.bk * q.G > 64 && q.bk * q.G <= 96) ? 96 : 64;
+  q.attn_rb = (q.bk * q.G + q.attn_rows - 1) / q.attn_rows;
   {
-    // key splits: about one workgroup per compute unit, at most 64 (one per lane of the
-    // merge), and no more than the 64-key chunks of the longest sequence
+    // key splits: about two workgroups per compute unit, at most 64 (one per lane of the
+    // merge), and at least two 64-key chunks per split at the longest sequence
     const int base = q.bmax * q.Hkv * q.attn_rb;
-    int sp = (256 + base - 1) / base;
-    const int maxsp = (q.T + 63) / 64;
+    int sp = (512 + base - 1) / base;
+    const int maxsp = ((q.T + 63) / 64) / 2;
     if (sp > maxsp) sp = maxsp;
     if (sp > 64) sp = 64;
     if (sp < 1) sp = 1;
@@ -141,13 +144,14 @@ int make_plan(const rt_config* c, Plan* p) {
   q.first_tok = take((size_t)q.bmax * 4);
   q.counters = take((size_t)kMaxTiles * 4);
   q.partial = take(kPartialFloats * 4);
-  q.rpart = take((size_t)kResidSplits * 32 * q.d * 4);
+  q.rpart_rows = q.R > 32 ? q.R : 32;
+  q.rpart = take((size_t)kResidSplits * q.rpart_rows * q.d * 4);
   {
     size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
     size_t blocks = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits;
     (void)rb;
-    q.opart = take(blocks * 64 * q.hd * 4);
-    q.mlpart = take(blocks * 64 * 2 * 4);
+    q.opart = take(blocks * q.attn_rows * q.hd * 4);
+    q.mlpart = take(blocks * q.attn_rows * 2 * 4);
   }
   const size_t M = q.Mrows;
   q.x = take(M * q.d * 4);

@@ -169,6 +169,8 @@ def test_measurement_calls_leave_the_rounds_unchanged():
                          B.RT_K_GEMM_CONTEXT, B.RT_K_GEMM_COND, B.RT_K_ATTENTION, B.RT_K_ATTN_MERGE,
                          B.RT_K_LM_HEAD):
                 r = eng.time_kernel(kind, 2)
+                if kind == B.RT_K_ATTN_MERGE and r["launches"] == 0:   # one key split: no merge
+                    continue
                 assert r["launches"] > 0 and r["ms"] > 0 and r["bytes"] > 0, r
             for kind in (B.RT_K_NORM, B.RT_K_QKV_POST, B.RT_K_MISC):
                 with pytest.raises(B.RetraceError) as ex:

@@ -19,7 +19,7 @@ def _setup(name, **over):
     return wl, W, prompts
 
 
-@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged"])
+@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5"])
 def test_prefill_and_rounds_match_oracle(name):
     wl, W, prompts = _setup(name, norm_init="perturbed")
     log(f"[{name}] engine init")

@@ -116,6 +116,13 @@ PRESETS = {
                           head_dim=64, ffn=512),
         draft_layers=2, cond_layers=(0, 2), block_size=16, batch=3, prompt_len=(17, 70),
         new_tokens=40, seed=8),
+    # GQA group of 5 (80 query rows per 16-token block, as at the Qwen3-14B shape), hd 128
+    "mini-bf16-gqa5": Workload(
+        name="mini-bf16-gqa5", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=256, n_layers=2, n_q_heads=10, n_kv_heads=2,
+                          head_dim=128, ffn=512),
+        draft_layers=1, cond_layers=(0, 1), block_size=16, batch=2, prompt_len=(90, 150),
+        new_tokens=40, seed=9),
 }
 
 
