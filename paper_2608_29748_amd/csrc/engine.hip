@@ -265,6 +265,20 @@ struct Engine : EngineBase {
   // LM head over rows of xa with a fused argmax into keys[M] (optional fp32 logits).
   int lm_head_argmax(int M, uint64_t* keys, float* logits) {
     const Plan& q = p;
+    if (sizeof(T) == 2 && M > 32 && M <= 512) {   // mid-size rows: one pass over the vocabulary
+      GemmArgs g{};
+      g.A = at<T>(q.xa); g.lda = 16 * q.Kp_d; g.a_rows = q.Mrows; g.B = at<T>(q.lm_head); g.Kp = q.Kp_d; g.ksplit = 1;
+      g.e.kind = EPI_ARGMAX; g.e.M = M; g.e.N = q.V; g.e.out_f32 = logits; g.e.ldo = q.V;
+      g.e.part_keys = at<uint64_t>(q.part_keys);
+      const int parts = 2 * ((q.V + gemm_mid_cols(q.V) - 1) / gemm_mid_cols(q.V));
+      prof_begin(RT_K_LM_HEAD, (double)q.V * q.d * sizeof(T) + (double)M * q.d * sizeof(T), 2.0 * M * q.V * q.d);
+      HIPCHK(gemm_mid(g, stream));
+      prof_end();
+      prof_begin(RT_K_MISC, (double)parts * M * 8, 0);
+      HIPCHK(argmax_reduce(at<uint64_t>(q.part_keys), parts, M, keys, stream));
+      prof_end();
+      return RT_OK;
+    }
     const int parts = lmhead_grid(q.V);
     for (int r0 = 0; r0 < M; r0 += 32) {          // 32-row passes over the vocabulary
       const int m = M - r0 < 32 ? M - r0 : 32;

@@ -22,6 +22,8 @@ enum EpiKind : int {
   EPI_COND_GATE,       // out_f32 = sigmoid(y)                               (Eq.9 gate)
   EPI_COND_OUT,        // x = e + y * gate on conditioned rows, e elsewhere  (Eq.9)
   EPI_PARTIAL,         // k slab z of a split reduction: out_f32[z * part_stride + m * ldo + n] = y
+  EPI_ARGMAX,          // per row, (max, lowest column) key of each half workgroup -> part_keys;
+                       // optional fp32 logits out_f32[m * ldo + n] (mid-size kernel only)
 };
 
 struct EpiArgs {
@@ -31,6 +33,7 @@ struct EpiArgs {
   // stride, columns offset by out_k0); out_act always packed (ldo = group stride)
   float* out_f32; void* out_act; int ldo; int out_k0;
   size_t part_stride;            // EPI_PARTIAL: elements between the slabs of consecutive k splits
+  uint64_t* part_keys;           // EPI_ARGMAX: [2 * gridDim.x][M] keys
   float* resid; int ldr;
   void* cap; int ldcap; int cap_k0;   // packed capture of the updated residual (act type), may be null
   // per-row sequence mapping

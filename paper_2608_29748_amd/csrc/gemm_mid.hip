@@ -54,6 +54,36 @@ __device__ __forceinline__ void mid_store(const EpiArgs& e, const f32x4 (&acc)[M
     }
 }
 
+// Argmax epilogue: for every row, the (value, lowest column) key over this wave's
+// columns goes to part_keys[2 * blockIdx.x + wn][row] (reduced by argmax_reduce).
+template <int MT, int NT>
+__device__ __forceinline__ void mid_argmax(const EpiArgs& e, const f32x4 (&acc)[MT][NT], int rbase, int cbase,
+                                           int c16, int part) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = rbase + m * 16 + r;
+      uint64_t key = 0ull;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int col = cbase + n * 16 + c16;
+        const float v = acc[m][n][r];
+        if (col < e.N) {
+          const uint64_t k = argmax_key(v, (uint32_t)col);
+          key = k > key ? k : key;
+          if (e.out_f32 && row < e.M) e.out_f32[(size_t)row * e.ldo + col] = v;
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const uint64_t other = __shfl_xor(key, o, 64);
+        key = other > key ? other : key;
+      }
+      if (c16 == 0 && row < e.M) e.part_keys[(size_t)part * e.M + row] = key;
+    }
+}
+
 template <int MB, int NB, int NSTAGE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_mid_kernel(GemmArgs a) {
   constexpr int MT = MB / 32;           // 16-row tiles per wave
@@ -133,6 +163,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   const EpiArgs& e = a.e;
   const int rbase = m0 + wm * MT * 16 + 4 * g4, cbase = n0 + wn * NT * 16;
   switch (e.kind) {
+    case EPI_ARGMAX: mid_argmax<MT, NT>(e, acc, rbase, cbase, c16, 2 * blockIdx.x + wn); break;
     case EPI_SWIGLU: mid_store<EPI_SWIGLU, MT, NT>(e, acc, rbase, cbase, c16); break;
     case EPI_STORE_F32: mid_store<EPI_STORE_F32, MT, NT>(e, acc, rbase, cbase, c16); break;
     case EPI_STORE_ACT: mid_store<EPI_STORE_ACT, MT, NT>(e, acc, rbase, cbase, c16); break;
@@ -145,7 +176,8 @@ int gemm_mid_cols(int N) { return N / 128 >= 160 ? 128 : 64; }
 
 bool gemm_mid_supports(const GemmArgs& a) {
   const int k = a.e.kind;
-  return (k == EPI_STORE_F32 || k == EPI_STORE_ACT || k == EPI_RESID || k == EPI_SWIGLU || k == EPI_PARTIAL) &&
+  return (k == EPI_STORE_F32 || k == EPI_STORE_ACT || k == EPI_RESID || k == EPI_SWIGLU || k == EPI_PARTIAL ||
+          k == EPI_ARGMAX) &&
          a.e.M > 32 && a.e.M <= 512 && (a.e.kind == EPI_PARTIAL || a.ksplit == 1);
 }
 

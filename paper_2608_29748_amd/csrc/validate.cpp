@@ -176,7 +176,8 @@ int make_plan(const rt_config* c, Plan* p) {
   {
     const size_t qc = (size_t)q.qkvN > (size_t)q.LD * 2 * q.kvN ? (size_t)q.qkvN : (size_t)q.LD * 2 * q.kvN;
     q.qkvf = take(M * qc * 4);
-    q.lm_parts = (q.V + 31) / 32 / 8 + 1;
+    q.lm_parts = (q.V + 31) / 32 / 8 + 1;                 // skinny LM head workgroups
+    if (2 * ((q.V + 63) / 64) > q.lm_parts) q.lm_parts = 2 * ((q.V + 63) / 64);   // mid-size: 2 per workgroup
     q.part_keys = take((size_t)q.lm_parts * M * 8);
   }
   q.dtok = take((size_t)q.R * 4);
