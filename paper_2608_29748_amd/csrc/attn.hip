@@ -407,8 +407,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       }
       float mx = fmaxf(fmaxf(fmaxf(st[0][0], st[0][1]), fmaxf(st[0][2], st[0][3])),
                        fmaxf(fmaxf(st[1][0], st[1][1]), fmaxf(st[1][2], st[1][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mx = group4_max(mx);
       const float mxs = mx * sl2;
       // raise the reference only when a score exceeds it by more than 2^8 (exponentials
       // stay below 256; the final ratio is unchanged); rescale O and the sum then
@@ -422,13 +421,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         lsum[t2] *= alpha;
         mref[t2] = mnew;
       }
-      const bool live = mref[t2] != -INFINITY;
+      // rows that have seen no visible key yet (reference -inf) take p = 0
+      const float mr = mref[t2];
+      const bool all_live = __builtin_amdgcn_ballot_w64(mr == -INFINITY) == 0;
       Frag<bf16_t> ph, pl;
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float x = live ? __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mref[t2])) : 0.f;
+          float x = __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr));
+          if (!all_live) x = mr == -INFINITY ? 0.f : x;
           lsum[t2] += x;
           const short hb = bf16_bits(x);
           ph.v[tau * 4 + e] = hb;
@@ -442,10 +444,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     }
   }
 #pragma unroll
-  for (int t2 = 0; t2 < NRT; ++t2) {
-    lsum[t2] += __shfl_xor(lsum[t2], 16, 64);
-    lsum[t2] += __shfl_xor(lsum[t2], 32, 64);
-  }
+  for (int t2 = 0; t2 < NRT; ++t2) lsum[t2] = group4_sum(lsum[t2]);
 
   // merge the two key halves of each row pair of waves through LDS (stages are free
   // once every wave has passed this barrier)

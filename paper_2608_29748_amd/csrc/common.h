@@ -132,6 +132,22 @@ __device__ __forceinline__ float warp_max(float v, int width = 64) {
   return v;
 }
 
+// Reductions over the four lanes l, l^16, l^32, l^48 (the same MFMA column in each
+// 16-lane group) with the gfx950 lane-swap instructions: each returns the pair
+// {v[l], v[l ^ 16]} resp. {v[l], v[l ^ 32]}, no LDS round trip.
+__device__ __forceinline__ float group4_max(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group4_sum(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Workgroup barrier that orders LDS accesses for the compiler but does not wait for

@@ -90,10 +90,10 @@ int make_plan(const rt_config* c, Plan* p) {
   q.attn_rows = (c->dtype == RT_BF16 && q.bk * q.G > 64 && q.bk * q.G <= 96) ? 96 : 64;
   q.attn_rb = (q.bk * q.G + q.attn_rows - 1) / q.attn_rows;
   {
-    // key splits: about two workgroups per compute unit, at most 64 (one per lane of the
+    // key splits: about one workgroup per compute unit, at most 64 (one per lane of the
     // merge), and at least two 64-key chunks per split at the longest sequence
     const int base = q.bmax * q.Hkv * q.attn_rb;
-    int sp = (512 + base - 1) / base;
+    int sp = (256 + base - 1) / base;
     const int maxsp = ((q.T + 63) / 64) / 2;
     if (sp > maxsp) sp = maxsp;
     if (sp > 64) sp = 64;
