@@ -39,12 +39,8 @@ constexpr int kTileN = 16;        // n extent of one packed weight tile
 constexpr int kPage = 16;         // tokens per KV page
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (bf16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// Round to nearest even (gfx950 converts in hardware; NaN stays NaN, quieted).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 __device__ __forceinline__ float f16_to_f32(uint16_t h) {
   _Float16 v; __builtin_memcpy(&v, &h, 2); return (float)v;
 }
