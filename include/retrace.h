@@ -43,7 +43,15 @@ enum {
 };
 
 enum { RT_F32 = 0, RT_BF16 = 1 };                   /* weight / activation storage type */
-enum { RT_COND_OFF = 0, RT_COND_RETRACE = 1 };     /* OFF: plain block drafting (no carry) */
+/* Drafter input conditioning on the previous round's rejected suffix (Section 4.2; the
+ * component ablation of Table 3 and its appendix settings):
+ *   RT_COND_OFF        plain block drafting: anchor and mask embeddings only;
+ *   RT_COND_RETRACE    corrected signal r = m + beta W_c [m; u] (Eq.7-8) fused through the
+ *                      gated residual of Eq.9 (the method itself);
+ *   RT_COND_RAW_GATED  the same gated residual on the uncorrected signal r = m;
+ *   RT_COND_OVERWRITE  the conditioned mask rows are replaced by m_j itself.
+ * Every mode tracks r and cond_len the same way; OFF ignores them. */
+enum { RT_COND_OFF = 0, RT_COND_RETRACE = 1, RT_COND_RAW_GATED = 2, RT_COND_OVERWRITE = 3 };
 
 #define RT_MAX_COND_LAYERS 8
 
@@ -58,7 +66,7 @@ typedef struct rt_config {
   int32_t block_size;      /* rows per draft block, anchor included: B = block_size - 1 proposals */
   int32_t mask_token_id;   /* token whose embedding fills the B proposal rows */
   float beta;              /* correction strength of Eq.8 (1.0 at inference) */
-  int32_t cond_mode;       /* RT_COND_RETRACE or RT_COND_OFF */
+  int32_t cond_mode;       /* one of RT_COND_OFF / _RETRACE / _RAW_GATED / _OVERWRITE */
   int32_t dtype;           /* RT_BF16 (fp16 retained states) or RT_F32 (fp32 everywhere) */
   int32_t max_batch;       /* sequences per batch */
   int32_t max_seq_len;     /* per sequence: prompt + generation budget + block_size */

@@ -51,14 +51,25 @@ def align_rejected(hD_prev: np.ndarray, hT_prev: np.ndarray, r: int, B: int):
 
 def condition_inputs(e: np.ndarray, m: np.ndarray, u: np.ndarray, cond_len: int,
                      w_c: np.ndarray, w_v: np.ndarray, w_g: np.ndarray,
-                     beta: float) -> np.ndarray:
+                     beta: float, mode: str = "retrace") -> np.ndarray:
     """Eq.7 (correction), Eq.8 (corrected signal), Eq.9 (gated residual) for rows
     j = 1..cond_len.  Weight matrices are [out][in]; W_c's first d input columns
-    act on m and W_g's first d on e."""
+    act on m and W_g's first d on e.
+
+    The component ablation (Section 5, Table 3; Appendix "Ablation Settings") uses the
+    same aligned signal three ways: "retrace" corrects it (Eq.7-8) and adds it through
+    the gate (Eq.9); "raw_gated" adds the raw aligned drafter state r_j = m_j through
+    the same gate; "overwrite" replaces the conditioned mask inputs with m_j."""
     e_t = e.copy()
     for j in range(1, cond_len + 1):
-        c = w_c @ np.concatenate([m[j], u[j]])
-        rj = m[j] + beta * c
+        if mode == "overwrite":
+            e_t[j] = m[j]
+            continue
+        if mode == "raw_gated":
+            rj = m[j]
+        else:
+            c = w_c @ np.concatenate([m[j], u[j]])
+            rj = m[j] + beta * c
         gate = sigmoid(w_g @ np.concatenate([e[j], rj]))
         e_t[j] = e[j] + (w_v @ rj) * gate
     return e_t
@@ -117,10 +128,10 @@ class OracleRunner:
     def draft(self, st: SeqState) -> DraftOut:
         m, W = self.m, self.m.W
         e = m.block_inputs(st.anchor)
-        if st.cond_len > 0:
+        if st.cond_len > 0 and self.wl.cond_mode != "off":
             mm, uu = align_rejected(st.hD_prev, st.hT_prev, st.r, self.B)
             e_t = condition_inputs(e, mm, uu, st.cond_len, W["retrace.w_c"], W["retrace.w_v"],
-                                   W["retrace.w_g"], self.wl.beta)
+                                   W["retrace.w_g"], self.wl.beta, self.wl.cond_mode)
         else:
             e_t = e.copy()
         e_t = m.prec.r(e_t)

@@ -452,17 +452,20 @@ struct Engine : EngineBase {
     const int32_t* pt = at<int32_t>(q.page_table);
     // (1) rejected-trajectory conditioning (Eq.5-9)
     stage(0);
-    if (cfg.cond_mode == RT_COND_RETRACE) {
-      prof_begin(RT_K_MISC, (double)R * q.d * (4 * q.ksz + sizeof(T) + 16), 0);
+    if (cfg.cond_mode == RT_COND_RETRACE || cfg.cond_mode == RT_COND_RAW_GATED) {
+      const bool raw = cfg.cond_mode == RT_COND_RAW_GATED;
+      prof_begin(RT_K_MISC, (double)R * q.d * ((raw ? 2 : 4) * q.ksz + sizeof(T) + (raw ? 8 : 16)), 0);
       const int ldg2 = 16 * q.Kp_2d;
       cond_prep<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, at<K>(q.hd_keep), at<K>(q.ht_keep), n_seqs, q.bk,
-                      at<float>(q.mu), at<float>(q.er), ldg2, stream);
+                      at<float>(q.mu), at<float>(q.er), ldg2, raw ? 1 : 0, stream);
       prof_end();
       EpiArgs e{};
-      e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er); e.ldo = ldg2; e.out_k0 = q.d;
-      e.cond_m = at<float>(q.mu); e.ld_cond_m = ldg2; e.beta = cfg.beta;
-      CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.mu), ldg2, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e, 2 * q.d));
-      e = EpiArgs{};
+      if (!raw) {   // corrected signal r = m + beta W_c [m; u] (Eq.7-8); raw gated keeps r = m
+        e.kind = EPI_COND_R; e.out_f32 = at<float>(q.er); e.ldo = ldg2; e.out_k0 = q.d;
+        e.cond_m = at<float>(q.mu); e.ld_cond_m = ldg2; e.beta = cfg.beta;
+        CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.mu), ldg2, R, true, at<T>(q.wc), q.d, q.Kp_2d, R, e, 2 * q.d));
+        e = EpiArgs{};
+      }
       e.kind = EPI_COND_GATE; e.out_f32 = at<float>(q.gate); e.ldo = q.d;
       CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.er), ldg2, R, true, at<T>(q.wg), q.d, q.Kp_2d, R, e, 2 * q.d));
       e = EpiArgs{};
@@ -473,8 +476,11 @@ struct Engine : EngineBase {
       // r occupies packed k tiles d/32 .. 2d/32 of er
       CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.er) + (size_t)(q.d / 32) * 512, ldg2, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e, q.d));
     } else {
+      // plain block drafting, or the overwrite ablation (conditioned rows take m_j)
+      const bool ow = cfg.cond_mode == RT_COND_OVERWRITE;
       prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 8), 0);
-      embed_block<T>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), q.d, stream);
+      embed_block<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, ow ? at<K>(q.hd_keep) : nullptr,
+                        x, at<float>(q.etilde), q.d, stream);
       prof_end();
     }
     stage(1);

@@ -32,9 +32,11 @@ void rmsnorm(float* x, int ldx, const T* w, int d, float eps, int rows, T* out, 
              K* keep, int ldk, const NormFold& fold, hipStream_t s);
 template <typename T>
 void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x, int ldx, hipStream_t s);
-// Drafter input without conditioning: row (s, 0) = E[anchor], rows (s, j>0) = E[mask].
-template <typename T>
-void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk,
+// Drafter input without gated conditioning: row (s, 0) = E[anchor], rows (s, j>0) =
+// E[mask], except that with hD given the conditioned rows 1..cond_len take the aligned
+// drafter states m_j = hD[s][r + j] instead (the overwrite ablation of Table 3).
+template <typename T, typename K>
+void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk, const K* hD,
                  float* x, float* etilde, int ldx, hipStream_t s);
 // Verify input: row (s, 0) = E[anchor], row (s, i) = E[draft token i]; also records the
 // draft tokens (decoded from the drafter's argmax keys unless `forced`).
@@ -42,10 +44,11 @@ template <typename T>
 void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* dkeys, int forced,
                   int32_t* dtok, int n_seqs, int bk, float* x, int ldx, hipStream_t s);
 // Conditioning gather (Eq.5/6): mu = [m | u] rows, er[:, :d] = e rows (both packed fp32,
-// group stride ldg).
+// group stride ldg).  raw != 0 (gated fusion of the uncorrected signal): er[:, d:2d] = m
+// rows and mu is left untouched.
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
-               int n_seqs, int bk, float* mu, float* er, int ldg, hipStream_t s);
+               int n_seqs, int bk, float* mu, float* er, int ldg, int raw, hipStream_t s);
 void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs,
             int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
 void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s);

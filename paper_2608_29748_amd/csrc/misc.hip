@@ -93,6 +93,10 @@ template void rmsnorm<float, float>(float*, int, const float*, int, float, int, 
                                     float*, int, const NormFold&, hipStream_t);
 
 // ------------------------------------------------------------------ embeddings
+template <typename K> struct KeepRead;
+template <> struct KeepRead<uint16_t> { __device__ static float of(uint16_t v) { return f16_to_f32(v); } };
+template <> struct KeepRead<float> { __device__ static float of(float v) { return v; } };
+
 template <typename T>
 __global__ void embed_rows_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ tok,
                                   float* __restrict__ x, int ldx) {
@@ -106,10 +110,22 @@ void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x
   RT_LAUNCH((embed_rows_kernel<T>), dim3(rows), dim3(256), 0, s, embed, d, tokens, x, ldx);
 }
 
-template <typename T>
+// Rows (s, j) with 1 <= j <= cond_len take m_j = hD[s][r + j] when hD is given (the
+// overwrite ablation); every other row is E[anchor] (j = 0) or E[mask].
+template <typename T, typename K>
 __global__ void embed_block_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st,
-                                   int mask, int bk, float* x, float* et, int ldx) {
+                                   int mask, int bk, const K* __restrict__ hD, float* x, float* et, int ldx) {
   const int row = blockIdx.x, sq = row / bk, j = row % bk;
+  const bool cond = hD && j >= 1 && j <= st[sq * kStateFields + ST_COND_LEN];
+  if (cond) {
+    const K* pm = hD + ((size_t)sq * bk + st[sq * kStateFields + ST_R] + j) * d;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+      const float v = KeepRead<K>::of(pm[i]);
+      x[(size_t)row * ldx + i] = v;
+      et[(size_t)row * ldx + i] = v;
+    }
+    return;
+  }
   const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
   const T* er = E + (size_t)tok * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
@@ -118,11 +134,11 @@ __global__ void embed_block_kernel(const T* __restrict__ E, int d, const int32_t
     et[(size_t)row * ldx + i] = v;
   }
 }
-template <typename T>
-void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk,
+template <typename T, typename K>
+void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk, const K* hD,
                  float* x, float* etilde, int ldx, hipStream_t s) {
-  RT_LAUNCH((embed_block_kernel<T>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
-                     mask_token, bk, x, etilde, ldx);
+  RT_LAUNCH((embed_block_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
+                     mask_token, bk, hD, x, etilde, ldx);
 }
 
 template <typename T>
@@ -146,15 +162,13 @@ void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* d
 }
 
 // ------------------------------------------------------------------ conditioning gather
-template <typename K> struct KeepRead;
-template <> struct KeepRead<uint16_t> { __device__ static float of(uint16_t v) { return f16_to_f32(v); } };
-template <> struct KeepRead<float> { __device__ static float of(float v) { return v; } };
 
 // row (s, j): m_j = hD[s][r + j], u_j = hT[s][r + j - 1] for 1 <= j <= cond_len, else 0.
+// raw: the uncorrected signal r_j = m_j goes straight into er[:, d:2d] and mu is not used.
 template <typename T, typename K>
 __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ st, int mask,
                                  const K* __restrict__ hD, const K* __restrict__ hT, int bk,
-                                 float* __restrict__ mu, float* __restrict__ er, int ldg) {
+                                 float* __restrict__ mu, float* __restrict__ er, int ldg, int raw) {
   const int row = blockIdx.x, sq = row / bk, j = row % bk;
   const int r = st[sq * kStateFields + ST_R], cl = st[sq * kStateFields + ST_COND_LEN];
   const bool cond = j >= 1 && j <= cl;
@@ -162,6 +176,13 @@ __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* 
   const K* pu = hT + ((size_t)sq * bk + (cond ? r + j - 1 : 0)) * d;
   const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
   const T* pe = E + (size_t)tok * d;
+  if (raw) {
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+      er[pa_index(row, i, ldg)] = Elem<T>::to_f32(pe[i]);
+      er[pa_index(row, d + i, ldg)] = cond ? KeepRead<K>::of(pm[i]) : 0.f;
+    }
+    return;
+  }
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     mu[pa_index(row, i, ldg)] = cond ? KeepRead<K>::of(pm[i]) : 0.f;
     mu[pa_index(row, d + i, ldg)] = cond ? KeepRead<K>::of(pu[i]) : 0.f;
@@ -170,9 +191,9 @@ __global__ void cond_prep_kernel(const T* __restrict__ E, int d, const int32_t* 
 }
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
-               int n_seqs, int bk, float* mu, float* er, int ldg, hipStream_t s) {
+               int n_seqs, int bk, float* mu, float* er, int ldg, int raw, hipStream_t s) {
   RT_LAUNCH((cond_prep_kernel<T, K>), dim3(n_seqs * bk), dim3(256), 0, s, embed, d, state,
-                     mask_token, hD, hT, bk, mu, er, ldg);
+                     mask_token, hD, hT, bk, mu, er, ldg, raw);
 }
 
 // ------------------------------------------------------------------ acceptance / rollback
@@ -266,17 +287,17 @@ void fill_zero(void* p, size_t bytes, hipStream_t s) {
 
 template void embed_rows<bf16_t>(const bf16_t*, int, const int32_t*, int, float*, int, hipStream_t);
 template void embed_rows<float>(const float*, int, const int32_t*, int, float*, int, hipStream_t);
-template void embed_block<bf16_t>(const bf16_t*, int, const int32_t*, int, int, int, float*, float*, int,
-                                  hipStream_t);
-template void embed_block<float>(const float*, int, const int32_t*, int, int, int, float*, float*, int,
-                                 hipStream_t);
+template void embed_block<bf16_t, uint16_t>(const bf16_t*, int, const int32_t*, int, int, int, const uint16_t*,
+                                            float*, float*, int, hipStream_t);
+template void embed_block<float, float>(const float*, int, const int32_t*, int, int, int, const float*, float*,
+                                        float*, int, hipStream_t);
 template void embed_verify<bf16_t>(const bf16_t*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
                                    int, float*, int, hipStream_t);
 template void embed_verify<float>(const float*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
                                   int, float*, int, hipStream_t);
 template void cond_prep<bf16_t, uint16_t>(const bf16_t*, int, const int32_t*, int, const uint16_t*,
-                                          const uint16_t*, int, int, float*, float*, int, hipStream_t);
+                                          const uint16_t*, int, int, float*, float*, int, int, hipStream_t);
 template void cond_prep<float, float>(const float*, int, const int32_t*, int, const float*, const float*, int,
-                                      int, float*, float*, int, hipStream_t);
+                                      int, float*, float*, int, int, hipStream_t);
 
 }  // namespace rt

@@ -55,7 +55,8 @@ int validate_config(const rt_config* c) {
   if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab) return fail(RT_ERR_TOKEN, "mask_token_id out of range");
   if (!isfinite(c->beta)) return fail(RT_ERR_INVALID, "beta must be finite");
   if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(RT_ERR_INVALID, "rope_theta / rms_eps invalid");
-  if (c->cond_mode != RT_COND_OFF && c->cond_mode != RT_COND_RETRACE) return fail(RT_ERR_INVALID, "cond_mode invalid");
+  if (c->cond_mode < RT_COND_OFF || c->cond_mode > RT_COND_OVERWRITE)
+    return fail(RT_ERR_INVALID, "cond_mode must be RT_COND_OFF, _RETRACE, _RAW_GATED or _OVERWRITE");
   if (c->max_batch < 1 || c->max_batch > 1024) return fail(RT_ERR_INVALID, "max_batch must be in [1, 1024]");
   if (c->max_seq_len < c->block_size + 1 || c->max_seq_len > (1 << 20))
     return fail(RT_ERR_INVALID, "max_seq_len must be in [block_size + 1, 2^20]");

@@ -26,7 +26,9 @@ def log(*a):
     sys.stdout.flush()
 
 
-def engine_for(wl, W, max_batch=None, cond_mode=B.RT_COND_RETRACE):
+def engine_for(wl, W, max_batch=None, cond_mode=None):
+    if cond_mode is None:
+        cond_mode = B.COND_MODES[wl.cond_mode]
     cfg = config_from(wl.target, dtype=wl.dtype, draft_layers=wl.draft_layers,
                       cond_layers=wl.cond_layers, block_size=wl.block_size,
                       mask_token_id=wl.mask_token_id, max_batch=max_batch or wl.batch,

@@ -66,7 +66,8 @@ def test_workspace_and_weight_count(B):
     (dict(cond_layer_ids=[1, 0]), "increase"),
     (dict(draft_layers=0), "draft_layers"),
     (dict(dtype=7), "dtype"),
-    (dict(cond_mode=5), "cond_mode"),
+    (dict(cond_mode=4), "cond_mode"),
+    (dict(cond_mode=-1), "cond_mode"),
     (dict(max_seq_len=4), "max_seq_len"),
     (dict(max_batch=0), "max_batch"),
     (dict(dtype=0, max_seq_len=16385), "fp32 storage"),

@@ -38,6 +38,24 @@ def test_prefill_and_rounds_match_oracle(name):
     eng.close()
 
 
+@pytest.mark.parametrize("name,mode", [("tiny-f32", "raw_gated"), ("tiny-f32", "overwrite"),
+                                       ("mini-bf16", "raw_gated"), ("mini-bf16", "overwrite"),
+                                       ("mini-bf16-ragged", "off")])
+def test_ablation_conditioning_matches_oracle(name, mode):
+    """The component-ablation drafters of Table 3 (raw gated fusion, overwrite) and
+    plain block drafting, round by round against the oracle run in the same mode."""
+    wl, W, prompts = _setup(name, norm_init="perturbed", cond_mode=mode)
+    log(f"[{name} {mode}] prefill")
+    eng = engine_for(wl, W)
+    R = OracleRunner(OracleModel(wl, W))
+    first = eng.prefill(prompts, wl.new_tokens)
+    states = [R.prefill(p, wl.new_tokens) for p in prompts]
+    assert list(first) == [st.anchor for st in states]
+    rep = run_teacher_forced(eng, R, wl, states, 6, TOL[wl.dtype])
+    log(f"[{name} {mode}] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}")
+    eng.close()
+
+
 def test_forced_split_k_matches_oracle():
     """Prefill GEMMs (128-row tiles) with every reduction split four ways across
     workgroups (last-arriver fixup)."""

@@ -2,7 +2,9 @@
 forms of the conditioning under special weights, its stated reductions (W_v = 0,
 beta = 0), losslessness against target-only greedy decoding, brute-force
 recomputation, planted drafts with known acceptance lengths, the reset rule,
-budget clipping, and the drafter's internal consistency."""
+budget clipping, the component-ablation conditioning variants (Table 3), and the
+drafter's internal consistency."""
+import dataclasses
 import json
 import os
 
@@ -141,6 +143,49 @@ def test_beta_zero_is_raw_gated():
                                    rtol=1e-13)
 
 
+def check_raw_gated_ignores_correction(cond=condition_inputs):
+    """Raw gated fusion (Table 3): r_j = m_j, so W_c, u and beta drop out and the result
+    equals the corrected form at beta = 0; hand-worked d = 2 row with W_v = I,
+    W_g = [0 | I]: e~ = e + m * sigmoid(m)."""
+    rng = np.random.default_rng(5)
+    e, m, u = _rows(rng), _rows(rng), _rows(rng)
+    wv, wg = rng.standard_normal((D, D)), rng.standard_normal((D, 2 * D))
+    ref = condition_inputs(e, m, u, 4, np.zeros((D, 2 * D)), wv, wg, 1.0)   # W_c = 0: r = m
+    for wc, uu, beta in ((rng.standard_normal((D, 2 * D)), u, 1.0), (np.eye(D, 2 * D), 3 * m, 0.5)):
+        np.testing.assert_allclose(cond(e, m, uu, 4, wc, wv, wg, beta, "raw_gated"), ref, rtol=1e-13)
+    e2 = np.array([[9.0, 9.0], [0.5, -1.0]])
+    m2 = np.array([[0.0, 0.0], [2.0, -3.0]])
+    u2 = np.array([[0.0, 0.0], [7.0, 5.0]])
+    I, Z = np.eye(2), np.zeros((2, 2))
+    s = lambda x: 1 / (1 + np.exp(-x))
+    out = cond(e2, m2, u2, 1, np.hstack([I, I]), I, np.hstack([Z, I]), 1.0, "raw_gated")
+    np.testing.assert_allclose(out[1], [0.5 + 2 * s(2.0), -1.0 - 3 * s(-3.0)], rtol=1e-14)
+    np.testing.assert_array_equal(out[0], e2[0])
+
+
+def check_overwrite_replaces_rows(cond=condition_inputs):
+    """Overwrite (Table 3): conditioned rows 1..n become m_j exactly, whatever the
+    weights; the anchor row and rows past n keep e."""
+    rng = np.random.default_rng(6)
+    e, m, u = _rows(rng, 8), _rows(rng, 8), _rows(rng, 8)
+    w = lambda *s: rng.standard_normal(s)
+    out = cond(e, m, u, 5, w(D, 2 * D), w(D, D), w(D, 2 * D), 1.0, "overwrite")
+    np.testing.assert_array_equal(out[1:6], m[1:6])
+    np.testing.assert_array_equal(out[0], e[0])
+    np.testing.assert_array_equal(out[6:], e[6:])
+
+
+def test_ablation_conditioning_closed_forms():
+    check_raw_gated_ignores_correction()
+    check_overwrite_replaces_rows()
+    for mode in ("retrace", "raw_gated", "overwrite"):   # nothing conditioned: inputs unchanged
+        rng = np.random.default_rng(7)
+        e, m, u = _rows(rng), _rows(rng), _rows(rng)
+        out = condition_inputs(e, m, u, 0, w := rng.standard_normal((D, 2 * D)), rng.standard_normal((D, D)), w,
+                               1.0, mode)
+        np.testing.assert_array_equal(out, e)
+
+
 # ------------------------------------------------------------ planted mistakes must be caught
 
 def _align_off_by_one(hD, hT, r, B):
@@ -167,6 +212,16 @@ def _cond_gate_on_r_only(e, m, u, n, wc, wv, wg, beta):
     (check_gate_inputs, {"cond": _cond_gate_on_r_only}),
     (check_beta_scales_correction, {"cond": lambda e, m, u, n, wc, wv, wg, b:
                                     condition_inputs(e, m, u, n, wc, wv, wg, 1.0)}),
+    # raw gated fusion fed the target state instead of the drafter's, or still corrected
+    (check_raw_gated_ignores_correction, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode:
+                                          condition_inputs(e, u, m, n, wc, wv, wg, 0.0)}),
+    (check_raw_gated_ignores_correction, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode:
+                                          condition_inputs(e, m, u, n, wc, wv, wg, b)}),
+    # overwrite that adds m to e, or shifts the aligned rows by one
+    (check_overwrite_replaces_rows, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode:
+                                     np.concatenate([e[:1], e[1:n + 1] + m[1:n + 1], e[n + 1:]])}),
+    (check_overwrite_replaces_rows, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode:
+                                     np.concatenate([e[:1], m[:n], e[n + 1:]])}),
 ])
 def test_pins_catch_planted_mistakes(check, kw):
     with pytest.raises(AssertionError):
@@ -189,9 +244,13 @@ def mini():
     return wl, W, make_prompts(wl)[0]
 
 
-@pytest.mark.parametrize("which", ["tiny", "mini"])
-def test_lossless_against_target_greedy(which, tiny, mini):
+@pytest.mark.parametrize("which,mode", [("tiny", "retrace"), ("mini", "retrace"), ("mini", "raw_gated"),
+                                        ("mini", "overwrite"), ("mini", "off")])
+def test_lossless_against_target_greedy(which, mode, tiny, mini):
+    """Whatever the drafter's conditioning, greedy verification commits exactly the
+    target's own greedy continuation (Section 3, lossless acceptance)."""
     wl, W, prompt = tiny if which == "tiny" else mini
+    wl = dataclasses.replace(wl, cond_mode=mode)
     R = OracleRunner(OracleModel(wl, W))
     gen, recs, _ = R.spec_decode(prompt, wl.new_tokens)
     assert len(gen) == wl.new_tokens
@@ -268,6 +327,38 @@ def test_wv_zero_run_is_plain_dflash(mini):
         d = R.draft(st)
         np.testing.assert_array_equal(d.e_tilde, d.e)
         R.round(st)
+
+
+@pytest.mark.parametrize("mode", ["overwrite", "raw_gated", "off"])
+def test_ablation_rounds_condition_the_drafter_input(mini, mode):
+    """Within whole rounds: overwrite puts the previous round's aligned drafter states on
+    the conditioned rows (Eq.5 alignment), raw gated and off leave the anchor and the
+    unconditioned rows at their embeddings, and off leaves every row there."""
+    wl, W, prompt = mini
+    wl = dataclasses.replace(wl, cond_mode=mode)
+    R = OracleRunner(OracleModel(wl, W))
+    truth = R.ar_decode(prompt, 60)
+    st = R.prefill(prompt, 50)
+    seen = 0
+    for k in (2, 5, None, 1, 3):
+        r, n, hD = st.r, st.cond_len, None if st.hD_prev is None else st.hD_prev.copy()
+        d = R.draft(st)
+        if mode == "off" or n == 0:
+            np.testing.assert_array_equal(d.e_tilde, d.e)
+        else:
+            seen += 1
+            np.testing.assert_array_equal(d.e_tilde[0], d.e[0])
+            np.testing.assert_array_equal(d.e_tilde[n + 1:], d.e[n + 1:])
+            if mode == "overwrite":
+                np.testing.assert_array_equal(d.e_tilde[1:n + 1], hD[r + 1:r + n + 1])
+            else:
+                assert not np.array_equal(d.e_tilde[1:n + 1], d.e[1:n + 1])
+        done = len(st.generated)
+        draft = list(truth[done:done + wl.B])
+        if k is not None:
+            draft[k - 1] = (draft[k - 1] + 1) % wl.target.vocab
+        R.round(st, forced_draft=draft)
+    assert mode == "off" or seen >= 3
 
 
 def test_context_pathway_incremental_equals_recomputed(tiny):

@@ -50,6 +50,7 @@ class Workload:
     rms_eps: float = 1.0e-6
     page_size: int = 16
     beta: float = 1.0
+    cond_mode: str = "retrace"      # "retrace" (corrected, gated), "raw_gated", "overwrite", "off"
     init_std: float = 0.02
     norm_init: str = "ones"         # "ones" or "perturbed" (1 + 0.1 N(0,1)); tests use both
 
