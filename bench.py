@@ -8,7 +8,11 @@ HBM.  `value` is committed tokens per second over exactly `--steps` rounds after
 `--warmup` rounds.  A profiled phase then times every kernel launch with HIP
 events on the library's stream to give the per-stage breakdown and the roofline
 of the dominant kernel (the fused gate|up projection GEMM).  The CPU baseline is the
-float64 oracle, started from the GPU's state, timed on this host.
+float64 oracle, started from the GPU's state, timed on this host.  Last, the same
+prompts are decoded target-only (one row per sequence per step, same kernels, graph
+replay) for the speedup of speculative over target-only decoding.  --cond-mode runs
+the component-ablation drafters (raw gated fusion, overwrite) or plain block drafting
+in place of the method's conditioning.
 
 Random-initialised weights and uniform-random prompts of the workload's shapes
 stand in for the trained checkpoints and the benchmark prompts.
@@ -36,11 +40,13 @@ def log(*a):
 
 
 def build_engine(wl, W):
+    from paper_2608_29748_amd import binding as B
     from paper_2608_29748_amd.engine import RoundEngine, config_from
     from workloads import weight_specs
     cfg = config_from(wl.target, dtype=wl.dtype, draft_layers=wl.draft_layers, cond_layers=wl.cond_layers,
                       block_size=wl.block_size, mask_token_id=wl.mask_token_id, max_batch=wl.batch,
-                      max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps, beta=wl.beta)
+                      max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps, beta=wl.beta,
+                      cond_mode=B.COND_MODES[wl.cond_mode])
     return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
 
 
@@ -139,6 +145,27 @@ def cpu_baseline(eng, wl, W, prompts, seconds: float):
             "seconds_per_round": el / rounds}
 
 
+def target_only(eng, wl, prompts, steps: int, spec_value: float, warmup: int = 4):
+    """Target-only greedy decoding of the same prompts on the same kernels, one row per
+    sequence per step, graph-replayed: committed tokens per second over `steps` steps."""
+    import torch
+    steps = min(steps, wl.new_tokens - 1 - warmup)
+    eng.prefill(prompts, wl.new_tokens)
+    eng.ar_steps(warmup)
+    torch.cuda.synchronize()
+    done, left = 0, steps
+    t0 = time.perf_counter()
+    while left:
+        c = min(left, 256)
+        _, n = eng.ar_steps(c)
+        done += int(n.sum())
+        left -= c
+    el = time.perf_counter() - t0
+    tps = done / el
+    return {"tokens_per_s": tps, "ms_per_step": el * 1e3 / steps, "steps": steps, "warmup": warmup,
+            "speedup_of_speculative": spec_value / tps}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +176,9 @@ def main():
     ap.add_argument("--replay-reps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ar-steps", type=int, default=64, help="timed target-only greedy steps (0: skip)")
+    ap.add_argument("--cond-mode", choices=["retrace", "raw_gated", "overwrite", "off"], default="retrace",
+                    help="drafter conditioning: the method, a component-ablation variant, or none")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB copies (reference reading for the HBM byte counters)")
     args = ap.parse_args()
@@ -160,7 +190,7 @@ def main():
     import torch
     from workloads import get, make_prompts, make_weights
 
-    wl = get(args.workload)
+    wl = get(args.workload, cond_mode=args.cond_mode)
     need = args.warmup + args.steps + args.profile_rounds + 2
     if need > wl.new_tokens - 1:
         raise SystemExit(f"{need} rounds exceed the workload's generation budget of {wl.new_tokens} tokens")
@@ -249,7 +279,7 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "prompt_len": list(wl.prompt_len),
                    "block_size": wl.block_size, "new_tokens": wl.new_tokens, "hidden": wl.target.hidden,
                    "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
-                   "cond_layers": list(wl.cond_layers), "parallelism": "single GPU"},
+                   "cond_layers": list(wl.cond_layers), "cond_mode": wl.cond_mode, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": DOMINANT_DESC,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",
@@ -269,6 +299,11 @@ def main():
             out["cpu_baseline"] = cpu_baseline(eng, wl, W, prompts, args.cpu_seconds)
         except MemoryError as e:   # pragma: no cover
             out["cpu_baseline"] = {"error": f"oracle did not fit in host memory: {e}"}
+    if args.ar_steps > 0:
+        out["target_only"] = target_only(eng, wl, prompts, args.ar_steps, value)
+        log(f"target-only: {out['target_only']['ms_per_step']:.3f} ms/step, "
+            f"{out['target_only']['tokens_per_s']:.1f} tokens/s, "
+            f"speedup {out['target_only']['speedup_of_speculative']:.2f}x")
     eng.close()
     print(json.dumps(out), flush=True)
 

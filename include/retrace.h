@@ -124,6 +124,21 @@ int rt_prefill(rt_model* m, int32_t n_seqs, const int32_t* prompt_lens, const in
  * round.  Blocks until the outputs are on the host. */
 int rt_spec_round(rt_model* m, int32_t* tokens, int32_t* n_committed, int32_t* accept_len);
 
+/* Target-only greedy decoding on the same kernels (the autoregressive baseline that
+ * speculative decoding is measured against; Section 5, speedup over target-only
+ * decoding).  Each of the n_steps steps (1..RT_AR_MAX_STEPS) runs the target over
+ * one row per prefilled sequence -- its last committed token at the next position --
+ * appends that row's K/V to the paged cache and commits the argmax of the target's
+ * logits.  Outputs (host):
+ *   tokens[n_seqs][n_steps]: the committed tokens, -1 once a sequence's budget is spent;
+ *   n_generated[n_seqs]: tokens committed by this call.
+ * The drafter's context cache is not extended, so after rt_ar_steps only further
+ * rt_ar_steps calls are allowed until the next rt_prefill (rt_spec_round returns
+ * RT_ERR_STATE).  With debug flag 1 the last step's fp32 logits are kept
+ * (RT_T_AR_LOGITS).  Blocks until the outputs are on the host. */
+#define RT_AR_MAX_STEPS 256
+int rt_ar_steps(rt_model* m, int32_t n_steps, int32_t* tokens, int32_t* n_generated);
+
 /* Releases the handle (the workspace stays the caller's). */
 int rt_destroy(rt_model* m);
 
@@ -202,6 +217,7 @@ enum {
   RT_T_TARGET_TOKENS = 6,  /* [block] int32: target argmax of verify rows 0..B */
   RT_T_STATE = 7,          /* [8] int32: seq_len, anchor, r, cond_len, budget, round_pos, append, A */
   RT_T_G = 8,              /* [block][n_cond*d] captured conditioning-layer states (storage type) */
+  RT_T_AR_LOGITS = 9,      /* [V] f32 logits of the last rt_ar_steps step (needs debug flag 1) */
   RT_T_TARGET_K = 100,     /* + layer: [pos][Hkv][hd] storage type, positions 0.. */
   RT_T_TARGET_V = 200,     /* + layer */
   RT_T_DRAFT_K = 300,      /* + drafter layer: context keys */

@@ -25,7 +25,8 @@ COND_MODES = {"off": RT_COND_OFF, "retrace": RT_COND_RETRACE, "raw_gated": RT_CO
               "overwrite": RT_COND_OVERWRITE}
 RT_MAX_COND_LAYERS = 8
 (RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
- RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G) = range(9)
+ RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G, RT_T_AR_LOGITS) = range(10)
+RT_AR_MAX_STEPS = 256
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
 (RT_K_GEMM_QKV, RT_K_GEMM_O, RT_K_GEMM_GATE_UP, RT_K_GEMM_DOWN, RT_K_GEMM_CONTEXT, RT_K_GEMM_COND,
  RT_K_ATTENTION, RT_K_ATTN_MERGE, RT_K_NORM, RT_K_QKV_POST, RT_K_LM_HEAD, RT_K_MISC) = range(12)
@@ -37,7 +38,7 @@ RT_PROF_STAGES = 7
 
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
-           "rt_debug_write", "rt_profile_round", "rt_time_kernel"]
+           "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps"]
 
 
 class RetraceError(RuntimeError):
@@ -86,8 +87,10 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_debug_write.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_profile_round.argtypes = [P, C.POINTER(rt_kernel_stat), C.POINTER(C.c_double), i32p, i32p, i32p]
     lib.rt_time_kernel.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(rt_kernel_stat)]
+    lib.rt_ar_steps.argtypes = [P, C.c_int32, i32p, i32p]
     for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
-                 "rt_set_debug", "rt_debug_read", "rt_debug_write", "rt_profile_round"):
+                 "rt_set_debug", "rt_debug_read", "rt_debug_write", "rt_profile_round", "rt_time_kernel",
+                 "rt_ar_steps"):
         getattr(lib, name).restype = C.c_int
     return lib
 
@@ -165,6 +168,16 @@ def rt_spec_round_forced(h: int, drafts: np.ndarray, block_size: int):
                                      n.ctypes.data_as(C.POINTER(C.c_int32)),
                                      a.ctypes.data_as(C.POINTER(C.c_int32))))
     return tok, n, a
+
+
+def rt_ar_steps(h: int, n_seqs: int, n_steps: int):
+    """Target-only greedy steps: (tokens [n_seqs][n_steps] with -1 past the budget,
+    tokens generated per sequence)."""
+    tok = np.full((n_seqs, n_steps), -1, np.int32)
+    n = np.zeros(n_seqs, np.int32)
+    _check(_lib.rt_ar_steps(C.c_void_p(h), n_steps, tok.ctypes.data_as(C.POINTER(C.c_int32)),
+                            n.ctypes.data_as(C.POINTER(C.c_int32))))
+    return tok, n
 
 
 def rt_profile_round(h: int, n_seqs: int, block_size: int):

@@ -41,6 +41,9 @@ struct EngineBase {
   int flags = 0;
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
+  hipGraph_t ar_graph = nullptr;       // one target-only step
+  hipGraphExec_t ar_gexec = nullptr;
+  bool ar_mode = false;                // target-only steps ran since the last prefill
   int32_t* h_out = nullptr;      // pinned: tokens [R], n [bmax], a [bmax], first [bmax]
   // profiling: an event pair around every launch, aggregated per kernel kind
   bool profiling = false;
@@ -92,14 +95,34 @@ struct EngineBase {
   void drop_graph() {
     if (gexec) (void)hipGraphExecDestroy(gexec);
     if (graph) (void)hipGraphDestroy(graph);
+    if (ar_gexec) (void)hipGraphExecDestroy(ar_gexec);
+    if (ar_graph) (void)hipGraphDestroy(ar_graph);
     gexec = nullptr;
     graph = nullptr;
+    ar_gexec = nullptr;
+    ar_graph = nullptr;
+  }
+  // Captures body() (which enqueues on `stream`) into a graph once; later calls reuse it.
+  template <class F>
+  int capture_once(hipGraph_t& g_out, hipGraphExec_t& ge, F&& body) {
+    if (ge) return RT_OK;
+    HIPCHK(hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal));
+    int st = body();
+    hipGraph_t g = nullptr;
+    hipError_t ce = hipStreamEndCapture(stream, &g);
+    if (st != RT_OK) { if (g) (void)hipGraphDestroy(g); return st; }
+    if (ce != hipSuccess) return fail(RT_ERR_HIP, "graph capture: %s", hipGetErrorString(ce));
+    g_out = g;
+    HIPCHK(hipGraphInstantiate(&ge, g_out, nullptr, nullptr, 0));
+    return RT_OK;
   }
   template <class X> X* at(size_t off) const { return reinterpret_cast<X*>(ws + off); }
   virtual int init(const void* const* w) = 0;
   virtual int prefill(int ns, const int32_t* lens, const int32_t* ids, int budget, int32_t* first) = 0;
   virtual int run_round(bool forced) = 0;
+  virtual int run_ar_step() = 0;
   int round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc);
+  int ar_steps(int n, int32_t* tokens, int32_t* n_gen);
   int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int time_kernel(int kind, int reps, rt_kernel_stat* out);
   int debug_read(int id, int seq, void* dst, size_t bytes);
@@ -403,6 +426,7 @@ struct Engine : EngineBase {
     const Plan& q = p;
     drop_graph();
     prefilled = false;
+    ar_mode = false;
     size_t off = 0;
     int32_t* pf = at<int32_t>(q.pf_ints);
     int32_t* tok = at<int32_t>(q.tokbuf);
@@ -523,10 +547,72 @@ struct Engine : EngineBase {
     HIPCHK(hipGetLastError());
     return RT_OK;
   }
+
+  // One target-only greedy step: the anchor row of every sequence at position seq_len.
+  int run_ar_step() override {
+    const Plan& q = p;
+    static_assert(kAttnRowsAr == kAttnRows, "target-only steps use the 64-row attention blocks");
+    const int M = n_seqs;
+    int32_t* st = at<int32_t>(q.state);
+    const int32_t* pt = at<int32_t>(q.page_table);
+    prof_begin(RT_K_MISC, (double)M * q.d * (sizeof(T) + 4), 0);
+    embed_block<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, 1, nullptr, at<float>(q.x), nullptr,
+                      q.d, stream);
+    prof_end();
+    for (int l = 0; l < q.L; ++l) {
+      LayerCtx c{M, 1, n_seqs, kStateFields, 1, q.ar_splits, q.ar_rb, kAttnRows, st + ST_SEQ_LEN, nullptr, pt,
+                 at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
+                 nullptr, 0, prof_ctx.data(), 1};
+      CHK(layer(tlayer(l), c));
+    }
+    norm_x(at<T>(q.t_final_norm), M, nullptr, 0);
+    CHK(lm_head_argmax(M, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
+    prof_begin(RT_K_MISC, (double)M * 16, 0);
+    ar_commit(st, at<uint64_t>(q.tkeys), n_seqs, at<int32_t>(q.ar_tok), kArMaxSteps, at<int32_t>(q.pf_ints) + 8,
+              stream);
+    prof_end();
+    HIPCHK(hipGetLastError());
+    return RT_OK;
+  }
 };
+
+static int ar_state_error() {
+  return fail(RT_ERR_STATE, "target-only steps ran since rt_prefill (the drafter context was not extended); "
+                            "call rt_prefill before the next round");
+}
+
+int EngineBase::ar_steps(int n, int32_t* tokens, int32_t* n_gen) {
+  if (!prefilled) return fail(RT_ERR_STATE, "rt_ar_steps called before rt_prefill");
+  if (!tokens || !n_gen) return fail(RT_ERR_INVALID, "null output pointer");
+  if (n < 1 || n > kArMaxSteps) return fail(RT_ERR_INVALID, "n_steps must be in [1, %d]", kArMaxSteps);
+  const Plan& q = p;
+  ar_mode = true;
+  set_ints(at<int32_t>(q.pf_ints) + 8, 1, 0, 0, 0, 0, stream);   // step counter (outside the graph)
+  HIPCHK(hipGetLastError());
+  if (flags & 2) {
+    for (int i = 0; i < n; ++i) CHK(run_ar_step());
+  } else {
+    CHK(capture_once(ar_graph, ar_gexec, [&] { return run_ar_step(); }));
+    for (int i = 0; i < n; ++i) HIPCHK(hipGraphLaunch(ar_gexec, stream));
+  }
+  std::vector<int32_t> h((size_t)n_seqs * kArMaxSteps);
+  HIPCHK(hipMemcpyAsync(h.data(), ws + q.ar_tok, h.size() * 4, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  for (int s = 0; s < n_seqs; ++s) {
+    int cnt = 0;
+    for (int i = 0; i < n; ++i) {
+      const int32_t t = h[(size_t)s * kArMaxSteps + i];
+      tokens[(size_t)s * n + i] = t;
+      cnt += t >= 0;
+    }
+    n_gen[s] = cnt;
+  }
+  return RT_OK;
+}
 
 int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc) {
   if (!prefilled) return fail(RT_ERR_STATE, "rt_spec_round called before rt_prefill");
+  if (ar_mode) return ar_state_error();
   if (!tokens || !n_comm || !acc) return fail(RT_ERR_INVALID, "null output pointer");
   const Plan& q = p;
   if (forced) {
@@ -542,16 +628,7 @@ int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, i
   } else if (flags & 2) {
     CHK(run_round(false));
   } else {
-    if (!gexec) {
-      HIPCHK(hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal));
-      int st = run_round(false);
-      hipGraph_t g = nullptr;
-      hipError_t ce = hipStreamEndCapture(stream, &g);
-      if (st != RT_OK) { if (g) (void)hipGraphDestroy(g); return st; }
-      if (ce != hipSuccess) return fail(RT_ERR_HIP, "graph capture: %s", hipGetErrorString(ce));
-      graph = g;
-      HIPCHK(hipGraphInstantiate(&gexec, graph, nullptr, nullptr, 0));
-    }
+    CHK(capture_once(graph, gexec, [&] { return run_round(false); }));
     HIPCHK(hipGraphLaunch(gexec, stream));
   }
   const size_t R = (size_t)n_seqs * q.bk;
@@ -568,6 +645,7 @@ int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, i
 int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm,
                               int32_t* acc) {
   if (!prefilled) return fail(RT_ERR_STATE, "rt_profile_round called before rt_prefill");
+  if (ar_mode) return ar_state_error();
   const Plan& q = p;
   if (ev_pool.empty()) {
     ev_pool.resize(8192);
@@ -618,6 +696,7 @@ int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* 
 // allowed, so the replay changes no KV cache and no carried state.
 int EngineBase::time_kernel(int kind, int reps, rt_kernel_stat* out) {
   if (!prefilled) return fail(RT_ERR_STATE, "rt_time_kernel called before rt_prefill");
+  if (ar_mode) return ar_state_error();
   switch (kind) {
     case RT_K_GEMM_QKV: case RT_K_GEMM_O: case RT_K_GEMM_GATE_UP: case RT_K_GEMM_DOWN:
     case RT_K_GEMM_CONTEXT: case RT_K_GEMM_COND: case RT_K_ATTENTION: case RT_K_ATTN_MERGE:
@@ -713,6 +792,7 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
     case RT_T_DRAFT_TOKENS: off = q.dtok + seq * bk * 4; cap = bk * 4; break;
     case RT_T_TARGET_TOKENS: off = q.ttok + seq * bk * 4; cap = bk * 4; break;
     case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
+    case RT_T_AR_LOGITS: off = q.vlogits + seq * (size_t)q.V * 4; cap = (size_t)q.V * 4; break;
     case RT_T_G: {
       // packed [group][k tile][lane][8] -> row-major [bk][n_cond * d]
       const size_t ncd = (size_t)q.nc * q.d, ldg = (size_t)16 * q.Kp_nc;
@@ -880,6 +960,15 @@ int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32
     return m->e->profile_round(stats, stage_ms, tokens, n_committed, accept_len);
   } catch (...) {
     return fail(RT_ERR_INVALID, "unexpected exception in rt_profile_round");
+  }
+}
+
+int rt_ar_steps(rt_model* m, int32_t n_steps, int32_t* tokens, int32_t* n_generated) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    return m->e->ar_steps(n_steps, tokens, n_generated);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_ar_steps");
   }
 }
 

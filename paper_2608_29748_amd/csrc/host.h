@@ -23,6 +23,8 @@ constexpr int kPrefillChunk = 512;     // prompt rows per prefill pass
 constexpr int kMaxTiles = 1 << 16;     // split-K arrival counters
 constexpr size_t kPartialFloats = (size_t)8 << 20;   // split-K partial capacity (32 MiB)
 constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections
+constexpr int kArMaxSteps = RT_AR_MAX_STEPS;   // target-only greedy steps per rt_ar_steps call
+constexpr int kAttnRowsAr = 64;   // attention rows per block in target-only steps (the 64-row kernel)
 
 struct Plan {
   // dimensions
@@ -34,6 +36,7 @@ struct Plan {
   int R, PF, Mrows;                      // round rows, prefill rows, allocated activation rows
   int attn_rb, attn_splits;              // round attention row blocks / key splits
   int attn_rows;                         // round attention rows per block (64, or 96)
+  int ar_rb, ar_splits;                  // target-only steps: 64-row attention blocks / key splits
   int pf_rb;
   size_t cache_layer_elems;
   // byte offsets into the workspace
@@ -46,6 +49,7 @@ struct Plan {
   size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
   size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys
   size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplits][rpart_rows][d]
+  size_t ar_tok;                 // target-only step tokens [bmax][kArMaxSteps]
   int rpart_rows;                // max(32, rows of a round)
   int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init

@@ -35,6 +35,7 @@ void embed_rows(const T* embed, int d, const int32_t* tokens, int rows, float* x
 // Drafter input without gated conditioning: row (s, 0) = E[anchor], rows (s, j>0) =
 // E[mask], except that with hD given the conditioned rows 1..cond_len take the aligned
 // drafter states m_j = hD[s][r + j] instead (the overwrite ablation of Table 3).
+// etilde (a second copy of the rows) may be null.
 template <typename T, typename K>
 void embed_block(const T* embed, int d, const int32_t* state, int mask_token, int n_seqs, int bk, const K* hD,
                  float* x, float* etilde, int ldx, hipStream_t s);
@@ -51,6 +52,10 @@ void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, cons
                int n_seqs, int bk, float* mu, float* er, int ldg, int raw, hipStream_t s);
 void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs,
             int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
+// Target-only greedy step commit for n_seqs (<= 1024) sequences: tokens go to column
+// *step of out (row stride ld_out), then *step is advanced.
+void ar_commit(int32_t* state, const uint64_t* tkeys, int n_seqs, int32_t* out, int ld_out, int32_t* step,
+               hipStream_t s);
 void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s);
 void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
                  int32_t* first_out, hipStream_t s);

@@ -11,39 +11,57 @@ template <> struct KeepT<float> { __device__ static float of(float v) { return v
 // in registers (hidden <= 8192), and writes the normalised row in the packed GEMM-operand
 // layout (one 8-element run per chunk) plus an optional row-major retained copy.  With a
 // fold, the pending k-slab partials of the producing GEMM are first summed (slab order)
-// and added to the row, which is written back (and optionally captured, packed).
-template <typename T, typename K>
+// and added to the row, which is written back (and optionally captured, packed).  Every
+// load of the row (x, partials, weight) is issued before the first use, so the row costs
+// one memory latency; NP is the partial count when known at compile time (-1: runtime,
+// at most 8).
+template <typename T, typename K, int NP>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, int ldx,
                                                       const T* __restrict__ w, int d, float eps,
                                                       T* __restrict__ out, int ldg, K* keep, int ldk,
                                                       NormFold fold) {
+  constexpr int MAXP = NP >= 0 ? NP : 8;
   __shared__ float red[4];
   const int row = blockIdx.x;
   float* xr = x + (size_t)row * ldx;
   const int nch = d / 8;
-  float v[4][8];
+  const int np = NP >= 0 ? NP : fold.n_part;
+  float4 xa[4][2], pa[4][MAXP > 0 ? MAXP : 1][2];
   Frag<T> wf[4];
-  float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int c = threadIdx.x + j * 256;
     if (c < nch) {
       wf[j].load(w + 8 * c);
-      const float4 a = *reinterpret_cast<const float4*>(xr + 8 * c);
-      const float4 b = *reinterpret_cast<const float4*>(xr + 8 * c + 4);
-      v[j][0] = a.x; v[j][1] = a.y; v[j][2] = a.z; v[j][3] = a.w;
-      v[j][4] = b.x; v[j][5] = b.y; v[j][6] = b.z; v[j][7] = b.w;
-      if (fold.n_part > 0) {
+      xa[j][0] = *reinterpret_cast<const float4*>(xr + 8 * c);
+      xa[j][1] = *reinterpret_cast<const float4*>(xr + 8 * c + 4);
+#pragma unroll
+      for (int z = 0; z < MAXP; ++z)
+        if (z < np) {
+          const float* pz = fold.part + z * fold.part_stride + (size_t)row * ldx + 8 * c;
+          pa[j][z][0] = *reinterpret_cast<const float4*>(pz);
+          pa[j][z][1] = *reinterpret_cast<const float4*>(pz + 4);
+        }
+    }
+  }
+  float v[4][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = threadIdx.x + j * 256;
+    if (c < nch) {
+      v[j][0] = xa[j][0].x; v[j][1] = xa[j][0].y; v[j][2] = xa[j][0].z; v[j][3] = xa[j][0].w;
+      v[j][4] = xa[j][1].x; v[j][5] = xa[j][1].y; v[j][6] = xa[j][1].z; v[j][7] = xa[j][1].w;
+      if (np > 0) {
         float t[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) t[e] = 0.f;
-        for (int z = 0; z < fold.n_part; ++z) {
-          const float* pz = fold.part + z * fold.part_stride + (size_t)row * ldx + 8 * c;
-          const float4 p0 = *reinterpret_cast<const float4*>(pz);
-          const float4 p1 = *reinterpret_cast<const float4*>(pz + 4);
-          t[0] += p0.x; t[1] += p0.y; t[2] += p0.z; t[3] += p0.w;
-          t[4] += p1.x; t[5] += p1.y; t[6] += p1.z; t[7] += p1.w;
-        }
+#pragma unroll
+        for (int z = 0; z < MAXP; ++z)
+          if (z < np) {
+            t[0] += pa[j][z][0].x; t[1] += pa[j][z][0].y; t[2] += pa[j][z][0].z; t[3] += pa[j][z][0].w;
+            t[4] += pa[j][z][1].x; t[5] += pa[j][z][1].y; t[6] += pa[j][z][1].z; t[7] += pa[j][z][1].w;
+          }
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[j][e] += t[e];
         *reinterpret_cast<float4*>(xr + 8 * c) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
@@ -84,8 +102,12 @@ template <typename T, typename K>
 void rmsnorm(float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
              K* keep, int ldk, const NormFold& fold, hipStream_t s) {
   if (rows <= 0) return;
-  RT_LAUNCH((rmsnorm_kernel<T, K>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg,
-            keep, ldk, fold);
+  if (fold.n_part == 0)
+    RT_LAUNCH((rmsnorm_kernel<T, K, 0>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
+  else if (fold.n_part == 4)
+    RT_LAUNCH((rmsnorm_kernel<T, K, 4>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
+  else
+    RT_LAUNCH((rmsnorm_kernel<T, K, -1>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
 }
 template void rmsnorm<bf16_t, uint16_t>(float*, int, const bf16_t*, int, float, int, bf16_t*, int,
                                         uint16_t*, int, const NormFold&, hipStream_t);
@@ -131,7 +153,7 @@ __global__ void embed_block_kernel(const T* __restrict__ E, int d, const int32_t
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     const float v = Elem<T>::to_f32(er[i]);
     x[(size_t)row * ldx + i] = v;
-    et[(size_t)row * ldx + i] = v;
+    if (et) et[(size_t)row * ldx + i] = v;
   }
 }
 template <typename T, typename K>
@@ -242,6 +264,40 @@ void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t*
             int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s) {
   RT_LAUNCH(accept_kernel, dim3(n_seqs), dim3(64), 0, s, state, dtok, tkeys, ttok, bk, out_tokens,
                      out_n, out_a);
+}
+
+// Target-only greedy step: one thread per sequence commits the argmax of its row (the
+// K/V of the anchor row were written at position seq_len by this step's layers).  The
+// token goes to out[s * ld_out + k], k = *step, which the last thread advances.
+__global__ __launch_bounds__(1024) void ar_commit_kernel(int32_t* st_all, const uint64_t* __restrict__ tkeys,
+                                                         int n_seqs, int32_t* out, int ld_out, int32_t* step) {
+  const int k = *step;
+  const int sq = threadIdx.x;
+  if (sq < n_seqs) {
+    int32_t* st = st_all + sq * kStateFields;
+    const int budget = st[ST_BUDGET];
+    int v = -1;
+    if (budget > 0) {
+      v = key_index(tkeys[sq]);
+      const int P = st[ST_SEQ_LEN] + 1;
+      st[ST_SEQ_LEN] = P;
+      st[ST_ANCHOR] = v;
+      st[ST_BUDGET] = budget - 1;
+      st[ST_ROUND_POS] = P;
+      st[ST_APPEND] = 0;
+      st[ST_ACCEPT] = 0;
+      st[ST_R] = 0;
+      st[ST_COND_LEN] = 0;
+    }
+    out[(size_t)sq * ld_out + k] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) *step = k + 1;
+}
+void ar_commit(int32_t* state, const uint64_t* tkeys, int n_seqs, int32_t* out, int ld_out, int32_t* step,
+               hipStream_t s) {
+  const int threads = (n_seqs + 63) / 64 * 64;
+  RT_LAUNCH(ar_commit_kernel, dim3(1), dim3(threads), 0, s, state, tkeys, n_seqs, out, ld_out, step);
 }
 
 __global__ void set_ints_kernel(int32_t* dst, int n, int v0, int v1, int v2, int v3) {

@@ -90,17 +90,20 @@ int make_plan(const rt_config* c, Plan* p) {
   // rows (bf16), so each KV head's keys are read once
   q.attn_rows = (c->dtype == RT_BF16 && q.bk * q.G > 64 && q.bk * q.G <= 96) ? 96 : 64;
   q.attn_rb = (q.bk * q.G + q.attn_rows - 1) / q.attn_rows;
-  {
-    // key splits: about one workgroup per compute unit, at most 64 (one per lane of the
-    // merge), and at least two 64-key chunks per split at the longest sequence
-    const int base = q.bmax * q.Hkv * q.attn_rb;
+  // key splits: about one workgroup per compute unit, at most 64 (one per lane of the
+  // merge), and at least two 64-key chunks per split at the longest sequence
+  auto key_splits = [&](int row_blocks) {
+    const int base = q.bmax * q.Hkv * row_blocks;
     int sp = (256 + base - 1) / base;
     const int maxsp = ((q.T + 63) / 64) / 2;
     if (sp > maxsp) sp = maxsp;
     if (sp > 64) sp = 64;
     if (sp < 1) sp = 1;
-    q.attn_splits = sp;
-  }
+    return sp;
+  };
+  q.attn_splits = key_splits(q.attn_rb);
+  q.ar_rb = (q.G + kAttnRowsAr - 1) / kAttnRowsAr;   // one query token: G rows per KV head
+  q.ar_splits = key_splits(q.ar_rb);
   q.pf_rb = (q.PF * q.G + 63) / 64;
   q.cache_layer_elems = (size_t)q.n_pages * q.Hkv * 16 * q.hd;
 
@@ -149,10 +152,12 @@ int make_plan(const rt_config* c, Plan* p) {
   q.rpart = take((size_t)kResidSplits * q.rpart_rows * q.d * 4);
   {
     size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
-    size_t blocks = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits;
     (void)rb;
-    q.opart = take(blocks * q.attn_rows * q.hd * 4);
-    q.mlpart = take(blocks * q.attn_rows * 2 * 4);
+    size_t rows = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits * q.attn_rows;
+    const size_t ar_rows = (size_t)q.bmax * q.Hkv * q.ar_rb * q.ar_splits * kAttnRowsAr;
+    if (ar_rows > rows) rows = ar_rows;
+    q.opart = take(rows * q.hd * 4);
+    q.mlpart = take(rows * 2 * 4);
   }
   const size_t M = q.Mrows;
   q.x = take(M * q.d * 4);
@@ -187,6 +192,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.out_n = take((size_t)q.bmax * 4);
   q.out_a = take((size_t)q.bmax * 4);
   q.tokbuf = take((size_t)q.T * 4);
+  q.ar_tok = take((size_t)q.bmax * kArMaxSteps * 4);
   q.total = off;
   return RT_OK;
 }

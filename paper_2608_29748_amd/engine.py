@@ -71,6 +71,9 @@ class RoundEngine:
     def spec_round_forced(self, drafts: np.ndarray):
         return B.rt_spec_round_forced(self.h, drafts, self.cfg.block_size)
 
+    def ar_steps(self, n_steps: int):
+        return B.rt_ar_steps(self.h, self.n_seqs, n_steps)
+
     def profile_round(self):
         return B.rt_profile_round(self.h, self.n_seqs, self.cfg.block_size)
 

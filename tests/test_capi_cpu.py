@@ -112,6 +112,7 @@ def test_calls_on_null_handle(B):
     assert B._lib.rt_prefill(None, 1, p, p, 4, p) == B.RT_ERR_INVALID
     assert B._lib.rt_spec_round(None, p, p, p) == B.RT_ERR_INVALID
     assert B._lib.rt_spec_round_forced(None, p, p, p, p) == B.RT_ERR_INVALID
+    assert B._lib.rt_ar_steps(None, 1, p, p) == B.RT_ERR_INVALID
     assert B._lib.rt_set_debug(None, 0) == B.RT_ERR_INVALID
     assert B._lib.rt_debug_read(None, 0, 0, None, 0) == B.RT_ERR_INVALID
     assert B._lib.rt_debug_write(None, 0, 0, None, 0) == B.RT_ERR_INVALID
