@@ -172,6 +172,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3-4b-shape")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload's batch (concurrency sweep)")
     ap.add_argument("--profile-rounds", type=int, default=5)
     ap.add_argument("--replay-reps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -190,7 +191,10 @@ def main():
     import torch
     from workloads import get, make_prompts, make_weights
 
-    wl = get(args.workload, cond_mode=args.cond_mode)
+    over = {"cond_mode": args.cond_mode}
+    if args.batch is not None:
+        over["batch"] = args.batch
+    wl = get(args.workload, **over)
     need = args.warmup + args.steps + args.profile_rounds + 2
     if need > wl.new_tokens - 1:
         raise SystemExit(f"{need} rounds exceed the workload's generation budget of {wl.new_tokens} tokens")

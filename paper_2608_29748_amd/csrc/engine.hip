@@ -159,11 +159,9 @@ struct Engine : EngineBase {
     const int shape = M > 32 ? SHAPE_WIDE : SHAPE_SKINNY;
     const int KT = Kp / 32;
     int ks = 1;
-    // bf16 GEMMs of 33..512 rows go to the mid-size kernel (no cross-workgroup split);
+    // bf16 GEMMs of 33..512 rows go to the mid-size kernel (which picks its own k slabs);
     // the test hook (flags & 4) keeps them on the 128x128 split-k path instead
-    const bool mid = shape == SHAPE_WIDE && sizeof(T) == 2 && !af32 && M <= 512 && !(flags & 4) &&
-                     (e.kind == EPI_STORE_F32 || e.kind == EPI_STORE_ACT || e.kind == EPI_RESID ||
-                      e.kind == EPI_SWIGLU || e.kind == EPI_PARTIAL);
+    const bool mid = shape == SHAPE_WIDE && sizeof(T) == 2 && M <= 512 && !(flags & 4);
     if (shape == SHAPE_WIDE && !mid) {
       const int tiles = ((N + 127) / 128) * ((M + 127) / 128);
       if (flags & 4) {                       // test hook: force a k split wherever possible
@@ -180,7 +178,8 @@ struct Engine : EngineBase {
     if (e.kind == EPI_PARTIAL) ks = kResidSplits;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
-    a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.e = e;
+    a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.partial_floats = kPartialFloats;
+    a.e = e;
     if (instrumented()) {
       const double Kl = (double)k_logical;
       prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + epi_bytes(e, M, N),
@@ -295,7 +294,8 @@ struct Engine : EngineBase {
       g.e.part_keys = at<uint64_t>(q.part_keys);
       const int parts = 2 * ((q.V + gemm_mid_cols(q.V) - 1) / gemm_mid_cols(q.V));
       prof_begin(RT_K_LM_HEAD, (double)q.V * q.d * sizeof(T) + (double)M * q.d * sizeof(T), 2.0 * M * q.V * q.d);
-      HIPCHK(gemm_mid(g, stream));
+      g.partial = at<float>(q.partial); g.partial_floats = kPartialFloats;
+      HIPCHK(gemm_mid(g, false, stream));
       prof_end();
       prof_begin(RT_K_MISC, (double)parts * M * 8, 0);
       HIPCHK(argmax_reduce(at<uint64_t>(q.part_keys), parts, M, keys, stream));

@@ -56,6 +56,7 @@ struct GemmArgs {
   int ksplit;                             // wide: k splits summed by the last workgroup; skinny:
                                           // k slabs, only with EPI_PARTIAL (one slab per grid z)
   float* partial; uint32_t* counters;
+  size_t partial_floats;                  // capacity of `partial`
   EpiArgs e;
 };
 
@@ -98,13 +99,17 @@ void pack_interleaved(const T* Wa, const T* Wb, int N, int K, int Kp, T* out, hi
 enum GemmShape : int { SHAPE_SKINNY = 0, SHAPE_WIDE = 1 };
 // SHAPE_SKINNY: M <= 32, 16 or 32-row tiles, the k range split across the workgroup's
 // waves and reduced in LDS (no ksplit).  SHAPE_WIDE: 128x128 tiles, optional ksplit.
-// SHAPE_WIDE with bf16 storage and a bf16 A operand goes to the mid-size kernel
-// (gemm_mid.hip) for 33..512 rows when its epilogue allows; otherwise 128x128 tiles.
+// SHAPE_WIDE with bf16 storage goes to the mid-size kernel (gemm_mid.hip) for 33..512
+// rows; otherwise (fp32 storage, more rows) 128x128 tiles.
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s);
 bool gemm_mid_supports(const GemmArgs& a);
-hipError_t gemm_mid(const GemmArgs& a, hipStream_t s);
+hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s);
 int gemm_mid_cols(int N);
+// Sums ks fp32 slabs part[z][M][N] (row-major, slab stride M*N) in slab order and runs
+// epilogue e on the result.
+template <typename T>
+hipError_t gemm_split_epilogue(const EpiArgs& e, const float* part, int ks, hipStream_t s);
 int gemm_tile_cols(int shape, int N);
 int gemm_tile_rows(int shape, int M);
 template <typename T>

@@ -138,6 +138,37 @@ __device__ void run_epilogue(const EpiArgs& e, float (*t)[LDT], int m0, int n0) 
   }
 }
 
+// ------------------------------------------------------------------ split-slab epilogue
+// One workgroup per 16 x 64 output tile: sums the k slabs in slab order into LDS, then
+// runs the epilogue on the complete tile.
+template <typename T>
+__global__ __launch_bounds__(256) void split_epilogue_kernel(EpiArgs e, const float* __restrict__ part, int ks) {
+  __shared__ float tile[16][65];
+  const int m0 = blockIdx.y * 16, n0 = blockIdx.x * 64;
+  const size_t slab = (size_t)e.M * e.N;
+  for (int idx = threadIdx.x; idx < 16 * 64; idx += 256) {
+    const int r = idx / 64, c = idx % 64;
+    const int m = m0 + r, n = n0 + c;
+    float sum = 0.f;
+    if (m < e.M && n < e.N) {
+      const float* p = part + (size_t)m * e.N + n;
+      for (int z = 0; z < ks; ++z) sum += p[z * slab];
+    }
+    tile[r][c] = sum;
+  }
+  __syncthreads();
+  run_epilogue<T, 16, 64, 65, 256>(e, tile, m0, n0);
+}
+template <typename T>
+hipError_t gemm_split_epilogue(const EpiArgs& e, const float* part, int ks, hipStream_t s) {
+  if (e.M <= 0 || e.N <= 0) return hipSuccess;
+  if (e.kind == EPI_PARTIAL || e.kind == EPI_ARGMAX || ks < 1) return hipErrorInvalidValue;
+  RT_LAUNCH((split_epilogue_kernel<T>), dim3((e.N + 63) / 64, (e.M + 15) / 16), dim3(256), 0, s, e, part, ks);
+  return hipGetLastError();
+}
+template hipError_t gemm_split_epilogue<bf16_t>(const EpiArgs&, const float*, int, hipStream_t);
+template hipError_t gemm_split_epilogue<float>(const EpiArgs&, const float*, int, hipStream_t);
+
 // ------------------------------------------------------------------ skinny GEMM (M <= 32)
 // Workgroup tile (MT*16) x (NT*16); its NW waves split the reduction into contiguous
 // k ranges (each streams its own run of packed weight tiles) and the partial tiles are
@@ -363,7 +394,7 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
     }
   } else {
     if constexpr (sizeof(T) == 2) {
-      if (!a_f32 && gemm_mid_supports(a)) return gemm_mid(a, s);
+      if (gemm_mid_supports(a)) return gemm_mid(a, a_f32, s);
     }
     if (a.e.kind == EPI_PARTIAL) return hipErrorInvalidValue;
     dim3 grid((N + 127) / 128, (M + 127) / 128, a.ksplit);

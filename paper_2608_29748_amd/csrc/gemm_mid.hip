@@ -9,6 +9,13 @@
 // split the tile 2 x 2: wave (wm, wn) accumulates MB/2 rows x NB/2 columns, reading its
 // fragments from LDS at consecutive 16-byte lane offsets (conflict free).  The
 // epilogue runs on the accumulators in registers.
+//
+// An fp32 A operand (AF32) is copied as 2 KiB fragments and split in registers into a
+// bf16 high part and a bf16 remainder, each multiplied by the weight tile (two MFMAs),
+// as in the other GEMM kernels.  When the output tiles alone would leave the chip
+// underfilled, or the epilogue is one the register epilogue does not cover, the k range
+// is split over grid z into fp32 slabs that a second kernel sums in slab order before
+// running the epilogue.
 #include "gemm.h"
 
 namespace rt {
@@ -84,15 +91,17 @@ __device__ __forceinline__ void mid_argmax(const EpiArgs& e, const f32x4 (&acc)[
     }
 }
 
-template <int MB, int NB, int NSTAGE>
+template <int MB, int NB, int NSTAGE, bool AF32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_mid_kernel(GemmArgs a) {
   constexpr int MT = MB / 32;           // 16-row tiles per wave
   constexpr int NT = NB / 32;           // 16-column tiles per wave
-  constexpr int AG = MB / 16;           // packed A groups per k tile (1 KiB each)
+  constexpr int AG = MB / 16;           // packed A groups per k tile
+  constexpr int AB = AF32 ? 2048 : 1024;   // bytes of one A group's k tile
+  constexpr int AI = AG * AB / 1024;    // A copy items (1 KiB) per k tile
   constexpr int BT = NB / 16;           // packed weight tiles per k tile (1 KiB each)
-  constexpr int LPW = (AG + BT) / 4;    // direct-to-LDS copies per wave per k tile
-  constexpr int STG = (AG + BT) * 1024;
-  static_assert((AG + BT) % 4 == 0, "copies must spread evenly over the four waves");
+  constexpr int LPW = (AI + BT) / 4;    // direct-to-LDS copies per wave per k tile
+  constexpr int STG = (AI + BT) * 1024;
+  static_assert((AI + BT) % 4 == 0, "copies must spread evenly over the four waves");
   __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STG];
 
   const int lane = threadIdx.x & 63, g4 = lane >> 4, c16 = lane & 15;
@@ -104,23 +113,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   const int max_group = (a.a_rows - 1) >> 4;
   const int n_tiles_valid = a.e.N / kTileN;
 
-  // copy j of this wave per k tile: item it = w + 4 j (A groups first, then weight
+  // copy j of this wave per k tile: item it = w + 4 j (A items first, then weight
   // tiles); sources and destinations are uniform per wave
-  auto item_src = [&](int j) -> const bf16_t* {
+  constexpr size_t AE = AF32 ? 4 : 2;   // bytes per A element
+  auto item_src = [&](int j, int kt) -> const char* {
     const int it = w + 4 * j;
-    if (it < AG) {
-      int grp = (m0 >> 4) + it;
+    if (it < AI) {
+      int grp = (m0 >> 4) + it * 1024 / AB;
       if (grp > max_group) grp = max_group;
-      return (const bf16_t*)a.A + (size_t)grp * a.lda;
+      return (const char*)a.A + (size_t)grp * a.lda * AE + (size_t)kt * AB + (it * 1024) % AB;
     }
-    int nt = (n0 >> 4) + (it - AG);
+    int nt = (n0 >> 4) + (it - AI);
     if (nt >= n_tiles_valid) nt = n_tiles_valid - 1;
-    return (const bf16_t*)a.B + (size_t)nt * KT * 512;
+    return (const char*)a.B + ((size_t)nt * KT + kt) * 1024;
   };
   auto issue = [&](int kt, int stg) {
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(item_src(j) + (size_t)kt * 512 + lane * 8),
+      __builtin_amdgcn_global_load_lds((const void*)(item_src(j, kt) + lane * 16),
                                        (lds_void_t*)(smem + stg * STG + (w + 4 * j) * 1024), 16, 0, 0);
   };
 
@@ -146,16 +156,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     lds_barrier();   // every wave's copies of tile kt are visible; tile kt-1's stage is free
     if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
     const char* st = smem + (i % NSTAGE) * STG;
-    Frag<bf16_t> af[MT], bf[NT];
-#pragma unroll
-    for (int m = 0; m < MT; ++m) af[m].v = *reinterpret_cast<const bf16x8*>(st + (wm * MT + m) * 1024 + lane * 16);
+    Frag<bf16_t> bf[NT];
 #pragma unroll
     for (int n = 0; n < NT; ++n)
-      bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AG + wn * NT + n) * 1024 + lane * 16);
+      bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AI + wn * NT + n) * 1024 + lane * 16);
+    if constexpr (AF32) {
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+      for (int m = 0; m < MT; ++m) {
+        const float4* pa = reinterpret_cast<const float4*>(st + (wm * MT + m) * 2048 + lane * 32);
+        const float4 x0 = pa[0], x1 = pa[1];
+        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        Frag<bf16_t> hi, lo;
 #pragma unroll
-      for (int n = 0; n < NT; ++n) mma(acc[m][n], af[m], bf[n]);
+        for (int e = 0; e < 8; ++e) {
+          const bf16_t h = f32_to_bf16(xs[e]);
+          hi.v[e] = (short)h;
+          lo.v[e] = (short)f32_to_bf16(xs[e] - bf16_to_f32(h));
+        }
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          mma(acc[m][n], hi, bf[n]);
+          mma(acc[m][n], lo, bf[n]);
+        }
+      }
+    } else {
+      Frag<bf16_t> af[MT];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) af[m].v = *reinterpret_cast<const bf16x8*>(st + (wm * MT + m) * 1024 + lane * 16);
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int n = 0; n < NT; ++n) mma(acc[m][n], af[m], bf[n]);
+    }
   }
 
   // epilogue from the accumulators: lane (g4, c16) of tile (m, n) holds rows
@@ -176,22 +208,61 @@ int gemm_mid_cols(int N) { return N / 128 >= 160 ? 128 : 64; }
 
 bool gemm_mid_supports(const GemmArgs& a) {
   const int k = a.e.kind;
-  return (k == EPI_STORE_F32 || k == EPI_STORE_ACT || k == EPI_RESID || k == EPI_SWIGLU || k == EPI_PARTIAL ||
-          k == EPI_ARGMAX) &&
-         a.e.M > 32 && a.e.M <= 512 && (a.e.kind == EPI_PARTIAL || a.ksplit == 1);
+  if (a.e.M <= 32 || a.e.M > 512) return false;
+  if (k == EPI_PARTIAL) return a.ksplit >= 1;
+  return a.ksplit == 1;
 }
 
-hipError_t gemm_mid(const GemmArgs& a, hipStream_t s) {
+// The register epilogue covers these kinds; the others always take the slab path.
+static bool mid_direct_kind(int k) {
+  return k == EPI_STORE_F32 || k == EPI_STORE_ACT || k == EPI_RESID || k == EPI_SWIGLU || k == EPI_PARTIAL ||
+         k == EPI_ARGMAX;
+}
+
+template <bool AF32>
+static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t s) {
+  if (MB == 128 && NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4, AF32>), grid, dim3(256), 0, s, a);
+  else if (MB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32>), grid, dim3(256), 0, s, a);
+  else if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32>), grid, dim3(256), 0, s, a);
+  else RT_LAUNCH((gemm_mid_kernel<256, 128, 3, AF32>), grid, dim3(256), 0, s, a);
+}
+
+hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s) {
   if (!gemm_mid_supports(a)) return hipErrorInvalidValue;
-  const int M = a.e.M, N = a.e.N;
+  const int M = a.e.M, N = a.e.N, KT = a.Kp / kTileK;
   const int NB = gemm_mid_cols(N);
   const int MB = M <= 128 ? 128 : 256;
-  dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, a.ksplit);
-  if (MB == 128 && NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4>), grid, dim3(256), 0, s, a);
-  else if (MB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4>), grid, dim3(256), 0, s, a);
-  else if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3>), grid, dim3(256), 0, s, a);
-  else RT_LAUNCH((gemm_mid_kernel<256, 128, 3>), grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  const int tiles = ((N + NB - 1) / NB) * ((M + MB - 1) / MB);
+  if (a.e.kind == EPI_PARTIAL || a.e.kind == EPI_ARGMAX) {   // slabs or keys chosen by the caller
+    const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, a.ksplit);
+    if (a_f32) mid_launch<true>(a, MB, NB, grid, s);
+    else mid_launch<false>(a, MB, NB, grid, s);
+    return hipGetLastError();
+  }
+  // k slabs: about two workgroups per compute unit, at least eight k tiles per slab,
+  // and the slabs must fit the partial buffer
+  int ks = 1;
+  if (tiles < 256) ks = (512 + tiles - 1) / tiles;
+  if (ks > KT / 8) ks = KT / 8;
+  const size_t slab = (size_t)M * N;
+  if (a.partial_floats / slab < (size_t)ks) ks = (int)(a.partial_floats / slab);
+  if (ks < 1) ks = 1;
+  if (ks == 1 && mid_direct_kind(a.e.kind)) {
+    const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, 1);
+    if (a_f32) mid_launch<true>(a, MB, NB, grid, s);
+    else mid_launch<false>(a, MB, NB, grid, s);
+    return hipGetLastError();
+  }
+  if (!a.partial || a.partial_floats < slab * ks) return hipErrorInvalidValue;
+  GemmArgs g = a;
+  g.ksplit = ks;
+  g.e.kind = EPI_PARTIAL; g.e.out_f32 = a.partial; g.e.ldo = N; g.e.part_stride = slab;
+  const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, ks);
+  if (a_f32) mid_launch<true>(g, MB, NB, grid, s);
+  else mid_launch<false>(g, MB, NB, grid, s);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  return gemm_split_epilogue<bf16_t>(a.e, a.partial, ks, s);
 }
 
 }  // namespace rt

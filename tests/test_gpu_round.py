@@ -2,7 +2,7 @@
 import numpy as np
 import pytest
 
-from oracle import OracleModel, OracleRunner
+from oracle import OracleModel, OracleRunner, Precision
 from workloads import get, make_prompts, make_weights
 
 from gpu_parity import compare_prefill, engine_for, log, run_teacher_forced
@@ -19,7 +19,19 @@ def _setup(name, **over):
     return wl, W, prompts
 
 
-@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5"])
+def _exact(wl, W, R):
+    """A float64 runner sharing R's weights, for bf16 models of width >= 1024: their
+    bf16 rounding noise exceeds the fixed tolerance, so the bounds are calibrated by
+    the mixed-precision oracle's own distance from float64 arithmetic (as at the
+    measured shapes)."""
+    if wl.dtype != "bf16" or wl.target.hidden < 1024:
+        return None
+    RX = OracleRunner(OracleModel(wl, W, prec=Precision.for_dtype("f64")))
+    RX.m.W = R.m.W
+    return RX
+
+
+@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5", "mini-bf16-b4"])
 def test_prefill_and_rounds_match_oracle(name):
     wl, W, prompts = _setup(name, norm_init="perturbed")
     log(f"[{name}] engine init")
@@ -32,7 +44,7 @@ def test_prefill_and_rounds_match_oracle(name):
     tol = TOL[wl.dtype]
     rep = compare_prefill(eng, R, wl, prompts, states, tol)
     log(f"[{name}] prefill max err {rep.max_err}")
-    rep = run_teacher_forced(eng, R, wl, states, 6, tol)
+    rep = run_teacher_forced(eng, R, wl, states, 6, tol, exact=_exact(wl, W, R))
     log(f"[{name}] rounds {rep.rounds} max err {rep.max_err} p99.9 {rep.p999} "
         f"near-ties {rep.near_ties}/{rep.decisions}")
     eng.close()
@@ -40,7 +52,7 @@ def test_prefill_and_rounds_match_oracle(name):
 
 @pytest.mark.parametrize("name,mode", [("tiny-f32", "raw_gated"), ("tiny-f32", "overwrite"),
                                        ("mini-bf16", "raw_gated"), ("mini-bf16", "overwrite"),
-                                       ("mini-bf16-ragged", "off")])
+                                       ("mini-bf16-ragged", "off"), ("mini-bf16-b4", "raw_gated")])
 def test_ablation_conditioning_matches_oracle(name, mode):
     """The component-ablation drafters of Table 3 (raw gated fusion, overwrite) and
     plain block drafting, round by round against the oracle run in the same mode."""
@@ -51,7 +63,7 @@ def test_ablation_conditioning_matches_oracle(name, mode):
     first = eng.prefill(prompts, wl.new_tokens)
     states = [R.prefill(p, wl.new_tokens) for p in prompts]
     assert list(first) == [st.anchor for st in states]
-    rep = run_teacher_forced(eng, R, wl, states, 6, TOL[wl.dtype])
+    rep = run_teacher_forced(eng, R, wl, states, 6, TOL[wl.dtype], exact=_exact(wl, W, R))
     log(f"[{name} {mode}] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}")
     eng.close()
 

@@ -104,6 +104,13 @@ PRESETS = {
         name="qwen3-14b-shape-b16", dtype="bf16", target=_qwen(151936, 5120, 40, 40, 8, 17408),
         draft_layers=5, cond_layers=cond_layer_ids(40, 5), block_size=16, batch=16,
         prompt_len=(8192, 16384), new_tokens=128, seed=4),
+    # Concurrent serving at the Qwen3-4B shape (Appendix, concurrent serving): short
+    # math-word-problem prompts (96..320 tokens), up to 1024 new tokens, 16-token blocks;
+    # the batch (client concurrency 1..32) is set per run.
+    "qwen3-4b-serve": Workload(
+        name="qwen3-4b-serve", dtype="bf16", target=_qwen(151936, 2560, 36, 32, 8, 9728),
+        draft_layers=5, cond_layers=cond_layer_ids(36, 5), block_size=16, batch=1,
+        prompt_len=(96, 320), new_tokens=1024, seed=5),
     # Small bf16 models for fast CPU/GPU tests (not measured workloads).
     "mini-bf16": Workload(
         name="mini-bf16", dtype="bf16",
@@ -117,6 +124,14 @@ PRESETS = {
                           head_dim=64, ffn=512),
         draft_layers=2, cond_layers=(0, 2), block_size=16, batch=3, prompt_len=(17, 70),
         new_tokens=40, seed=8),
+    # Four sequences (64 round rows) over a 1024-wide model: the mid-size GEMM path with
+    # k slabs (reductions of 32..64 k tiles), including the fp32-operand conditioning GEMMs
+    "mini-bf16-b4": Workload(
+        name="mini-bf16-b4", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=1024, n_layers=2, n_q_heads=8, n_kv_heads=2,
+                          head_dim=128, ffn=2048),
+        draft_layers=1, cond_layers=(0, 1), block_size=16, batch=4, prompt_len=(30, 90),
+        new_tokens=40, seed=10),
     # GQA group of 5 (80 query rows per 16-token block, as at the Qwen3-14B shape), hd 128
     "mini-bf16-gqa5": Workload(
         name="mini-bf16-gqa5", dtype="bf16",
