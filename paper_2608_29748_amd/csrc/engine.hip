@@ -156,7 +156,10 @@ struct Engine : EngineBase {
     if (k_logical <= 0) k_logical = Kp;
     e.M = M;
     e.N = N;
-    const int shape = M > 32 ? SHAPE_WIDE : SHAPE_SKINNY;
+    // skinny up to 32 rows, and up to 64 rows with bf16 operands; the test hook (flags & 4)
+    // keeps 33..64 rows on the wide split-k path
+    const bool skinny = M <= 32 || (M <= 64 && sizeof(T) == 2 && !af32 && !(flags & 4));
+    const int shape = skinny ? SHAPE_SKINNY : SHAPE_WIDE;
     const int KT = Kp / 32;
     int ks = 1;
     // bf16 GEMMs of 33..512 rows go to the mid-size kernel (which picks its own k slabs);

@@ -97,8 +97,9 @@ template <typename T>
 void pack_interleaved(const T* Wa, const T* Wb, int N, int K, int Kp, T* out, hipStream_t s);
 
 enum GemmShape : int { SHAPE_SKINNY = 0, SHAPE_WIDE = 1 };
-// SHAPE_SKINNY: M <= 32, 16 or 32-row tiles, the k range split across the workgroup's
-// waves and reduced in LDS (no ksplit).  SHAPE_WIDE: 128x128 tiles, optional ksplit.
+// SHAPE_SKINNY: M <= 32 (and 33..64 with bf16 operands), 16, 32 or 64-row tiles, the k
+// range split across the workgroup's waves and reduced in LDS (no ksplit except k slabs
+// with EPI_PARTIAL).  SHAPE_WIDE: 128x128 tiles, optional ksplit.
 // SHAPE_WIDE with bf16 storage goes to the mid-size kernel (gemm_mid.hip) for 33..512
 // rows; otherwise (fp32 storage, more rows) 128x128 tiles.
 template <typename T>
@@ -110,8 +111,6 @@ int gemm_mid_cols(int N);
 // epilogue e on the result.
 template <typename T>
 hipError_t gemm_split_epilogue(const EpiArgs& e, const float* part, int ks, hipStream_t s);
-int gemm_tile_cols(int shape, int N);
-int gemm_tile_rows(int shape, int M);
 template <typename T>
 hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s);
 template <typename T>

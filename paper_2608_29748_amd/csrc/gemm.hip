@@ -359,17 +359,21 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
   run_epilogue<T, ROWS, COLS, LDT, 256>(a.e, tile, m0, n0);
 }
 
-int gemm_tile_rows(int shape, int M) { return shape == SHAPE_SKINNY ? (M > 16 ? 32 : 16) : 128; }
-int gemm_tile_cols(int shape, int N) {
-  return shape == SHAPE_SKINNY ? (N >= 5120 && N < 16384 ? 32 : 16) : 128;
-}
-
 template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
   const int M = a.e.M, N = a.e.N;
   if (M <= 0 || N <= 0) return hipSuccess;
   if (shape == SHAPE_SKINNY) {
-    if (M > 32) return hipErrorInvalidValue;
+    if (M > 32) {
+      // 33..64 rows (bf16 operands): 64-row tiles, eight waves over k, two k tiles in
+      // flight per wave; 32 columns, or 64 per k slab of a split reduction
+      if constexpr (sizeof(T) != 2) return hipErrorInvalidValue;
+      if (M > 64 || a_f32) return hipErrorInvalidValue;
+      if ((a.e.kind == EPI_PARTIAL) != (a.ksplit > 1) || a.ksplit < 1) return hipErrorInvalidValue;
+      if (a.ksplit > 1) RT_LAUNCH((gemm16_kernel<T, false, 4, 4, 8, 2>), dim3((N + 63) / 64, 1, a.ksplit), dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 4, 2, 8, 2>), dim3((N + 31) / 32, 1, 1), dim3(512), 0, s, a);
+      return hipGetLastError();
+    }
     // tile width, waves and loads in flight per shape class (measured on the Qwen3 layer
     // shapes): split reductions 16 columns x 4 waves per slab; N >= 16384 (gate|up) 16
     // columns; N >= 5120 32 columns; otherwise 16 columns with 8 loads in flight
