@@ -221,43 +221,78 @@ static bool mid_direct_kind(int k) {
 
 template <bool AF32>
 static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t s) {
-  if (MB == 128 && NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4, AF32>), grid, dim3(256), 0, s, a);
-  else if (MB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32>), grid, dim3(256), 0, s, a);
-  else if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32>), grid, dim3(256), 0, s, a);
-  else RT_LAUNCH((gemm_mid_kernel<256, 128, 3, AF32>), grid, dim3(256), 0, s, a);
+  if (MB == 128) {
+    if (NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4, AF32>), grid, dim3(256), 0, s, a);
+    else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32>), grid, dim3(256), 0, s, a);
+    else if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<128, 192, 4, false>), grid, dim3(256), 0, s, a);
+  } else {
+    if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32>), grid, dim3(256), 0, s, a);
+    else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, 3, AF32>), grid, dim3(256), 0, s, a);
+    else if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<256, 192, 4, false>), grid, dim3(256), 0, s, a);
+  }
+}
+
+// Tile width and k slabs.  A workgroup streams (MB + NB) / 16 KiB through LDS per k
+// tile, about one workgroup per compute unit is resident for the wide tiles, and the
+// grid runs in rounds of 256 workgroups, so the estimated time of a choice is
+// rounds x (MB + NB) / 16 x k tiles per slab (slabs cost an extra pass over the
+// output).  Outputs of fewer than 128 tiles take k slabs to fill the chip.  The choices
+// reproduce the fastest measured configuration at the Qwen3-8B and 14B layer shapes.
+struct MidPlan { int NB, ks; };
+static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
+  const int M = a.e.M, N = a.e.N, KT = a.Kp / kTileK;
+  const int ai = (MB / 16) * (a_f32 ? 2 : 1);
+  const size_t slab = (size_t)M * N;
+  MidPlan best{64, 1};
+  double best_cost = 1e30;
+  for (int NB : {64, 128, 192}) {
+    if (NB == 192 && a_f32) continue;
+    const long tiles = (long)((N + NB - 1) / NB) * ((M + MB - 1) / MB);
+    int ks = 1;
+    if (a.e.kind == EPI_PARTIAL) {
+      ks = a.ksplit;
+    } else if (tiles < 128) {
+      ks = (int)(256 / tiles);
+      if (ks > KT / 8) ks = KT / 8;
+      if (ks > 8) ks = 8;
+      if ((size_t)ks > a.partial_floats / slab) ks = (int)(a.partial_floats / slab);
+      if (ks < 1) ks = 1;
+    }
+    if (NB == 192 && ks > 1) continue;   // the wide tile is for large outputs only
+    const double rounds = (double)((tiles * ks + 255) / 256);
+    double cost = rounds * (ai + NB / 16) * ((KT + ks - 1) / ks);
+    // slabs are written and read back once (mostly from cache): a quarter of their
+    // bytes relative to the weights'
+    if (ks > 1 && a.e.kind != EPI_PARTIAL) cost *= 1.0 + (double)ks * M / (KT * kTileK);
+    if (cost < best_cost) { best_cost = cost; best = MidPlan{NB, ks}; }
+  }
+  return best;
 }
 
 hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s) {
   if (!gemm_mid_supports(a)) return hipErrorInvalidValue;
-  const int M = a.e.M, N = a.e.N, KT = a.Kp / kTileK;
-  const int NB = gemm_mid_cols(N);
+  const int M = a.e.M, N = a.e.N;
   const int MB = M <= 128 ? 128 : 256;
-  const int tiles = ((N + NB - 1) / NB) * ((M + MB - 1) / MB);
-  if (a.e.kind == EPI_PARTIAL || a.e.kind == EPI_ARGMAX) {   // slabs or keys chosen by the caller
-    const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, a.ksplit);
-    if (a_f32) mid_launch<true>(a, MB, NB, grid, s);
-    else mid_launch<false>(a, MB, NB, grid, s);
-    return hipGetLastError();
-  }
-  // k slabs: about two workgroups per compute unit, at least eight k tiles per slab,
-  // and the slabs must fit the partial buffer
-  int ks = 1;
-  if (tiles < 256) ks = (512 + tiles - 1) / tiles;
-  if (ks > KT / 8) ks = KT / 8;
-  const size_t slab = (size_t)M * N;
-  if (a.partial_floats / slab < (size_t)ks) ks = (int)(a.partial_floats / slab);
-  if (ks < 1) ks = 1;
-  if (ks == 1 && mid_direct_kind(a.e.kind)) {
+  if (a.e.kind == EPI_ARGMAX) {   // the caller sizes its key parts by gemm_mid_cols
+    const int NB = gemm_mid_cols(N);
     const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, 1);
     if (a_f32) mid_launch<true>(a, MB, NB, grid, s);
     else mid_launch<false>(a, MB, NB, grid, s);
     return hipGetLastError();
   }
+  const MidPlan pl = mid_plan(a, MB, a_f32);
+  const int NB = pl.NB, ks = pl.ks;
+  const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, ks);
+  if (a.e.kind == EPI_PARTIAL || (ks == 1 && mid_direct_kind(a.e.kind))) {
+    if (a_f32) mid_launch<true>(a, MB, NB, grid, s);
+    else mid_launch<false>(a, MB, NB, grid, s);
+    return hipGetLastError();
+  }
+  const size_t slab = (size_t)M * N;
   if (!a.partial || a.partial_floats < slab * ks) return hipErrorInvalidValue;
   GemmArgs g = a;
   g.ksplit = ks;
   g.e.kind = EPI_PARTIAL; g.e.out_f32 = a.partial; g.e.ldo = N; g.e.part_stride = slab;
-  const dim3 grid((N + NB - 1) / NB, (M + MB - 1) / MB, ks);
   if (a_f32) mid_launch<true>(g, MB, NB, grid, s);
   else mid_launch<false>(g, MB, NB, grid, s);
   const hipError_t err = hipGetLastError();
