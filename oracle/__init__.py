@@ -14,6 +14,10 @@ Parity status per part (what pins each one lives in tests/test_oracle_*.py):
   conditioning (Eq.5-9) ............................ special-case closed forms, Fig.3 indices,
                                                      W_v = 0 and beta = 0 reductions
   acceptance / rollback / losslessness ............. target-only greedy decode, planted drafts
+  temperature sampling (sampling.py) ............... Philox4x64-10 against numpy's generator,
+                                                     filtered-distribution closed forms, the
+                                                     speculative-sampling rule's output
+                                                     distribution (chi-square), whole rounds
   drafter internals (DFlash context pathway) ....... parity unpinned against the paper (the
                                                      paper does not define the DFlash
                                                      architecture); only internal-consistency
@@ -24,6 +28,7 @@ from .numerics import Precision, round_bf16, round_f16, round_f32
 from .model import OracleModel, SeqState, DraftOut, VerifyOut
 from .retrace import (align_rejected, condition_inputs, accept_length, RoundRecord,
                       OracleRunner)
+from . import sampling
 
 __all__ = ["Precision", "round_bf16", "round_f16", "round_f32", "OracleModel", "SeqState",
            "DraftOut", "VerifyOut", "align_rejected", "condition_inputs", "accept_length",

@@ -138,6 +138,8 @@ class SeqState:
     hT_prev: Optional[np.ndarray] = None   # retained [B+1][d] target final states
     r: int = 0                   # first rejected block position of the last round
     cond_len: int = 0            # number of conditioned rows for the next draft
+    seq: int = 0                 # batch position (selects the sequence's random draws)
+    rnd: int = 0                 # rounds (or target-only steps) completed
 
     @property
     def done(self) -> bool:

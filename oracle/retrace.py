@@ -33,6 +33,8 @@ from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
 
+from . import sampling as smp
+
 from .model import DraftOut, OracleModel, SeqState, VerifyOut, sigmoid
 
 
@@ -111,11 +113,25 @@ class OracleRunner:
         self.B = model.wl.B
 
     # -- prefill: prompt rows through the target, first token, drafter context
-    def prefill(self, prompt, budget: int) -> SeqState:
+    @property
+    def sampling(self) -> bool:
+        return self.wl.temperature > 0.0
+
+    def dist(self, logits_row) -> smp.Dist:
+        return smp.filtered(logits_row, self.wl.temperature, self.wl.top_k, self.wl.top_p)
+
+    def u(self, st: SeqState, rnd: int, purpose: int, pos: int) -> float:
+        return smp.uniform(self.wl.sample_seed, rnd, st.seq, purpose, pos)
+
+    def prefill(self, prompt, budget: int, seq: int = 0) -> SeqState:
         m = self.m
         st = m.new_state(prompt, budget)
+        st.seq = seq
         out = m.target_forward(st, prompt, 0)
-        first = int(argmax_rows(out.logits[-1]))
+        if self.sampling:
+            first = smp.sample(self.dist(out.logits[-1]), self.u(st, 0, smp.U_FIRST, 0))
+        else:
+            first = int(argmax_rows(out.logits[-1]))
         m.context_append(st, out.g, 0)
         d = self.wl.target.hidden
         st.P, st.anchor, st.generated = len(prompt), first, [first]
@@ -142,9 +158,17 @@ class OracleRunner:
         return self.m.target_forward(st, [st.anchor] + [int(t) for t in y_hat], st.P)
 
     def commit(self, st: SeqState, y_hat, y_t, d: DraftOut, v: VerifyOut) -> Tuple[int, List[int]]:
+        """Greedy acceptance: the longest prefix of drafts equal to the target's argmax."""
+        A = accept_length(y_hat, y_t[: self.B])
+        return self.commit_tokens(st, y_hat, A, int(y_t[A]), d, v)
+
+    def commit_tokens(self, st: SeqState, y_hat, A: int, corr: int, d: DraftOut,
+                      v: VerifyOut) -> Tuple[int, List[int]]:
+        """Commits drafts 1..A and the correction / bonus token corr, rolls the target
+        cache back, extends the drafter context and applies the carry / reset rule."""
         B = self.B
-        A = accept_length(y_hat, y_t[:B])
-        new = [int(t) for t in y_hat[:A]] + [int(y_t[A])]
+        st.rnd += 1
+        new = [int(t) for t in y_hat[:A]] + [int(corr)]
         new = new[: max(0, st.budget - len(st.generated))]
         st.generated.extend(new)
         # rollback: target rows P+A+1..P+B were computed for rejected tokens
@@ -152,7 +176,7 @@ class OracleRunner:
         st.tgt_v[:, st.P + A + 1: st.P + B + 1] = 0.0
         self.m.context_append(st, v.g[: A + 1], st.P)
         st.P += A + 1
-        st.anchor = int(y_t[A])
+        st.anchor = int(corr)
         if A < B - 1:
             st.r = A + 1
             st.cond_len = B - st.r
@@ -165,6 +189,8 @@ class OracleRunner:
         return A, new
 
     def round(self, st: SeqState, forced_draft: Optional[Sequence[int]] = None) -> RoundRecord:
+        if self.sampling:
+            return self.sample_round(st, forced_draft)
         P, cond_len = st.P, st.cond_len
         d = self.draft(st)
         y_hat = (np.asarray(forced_draft, dtype=np.int64) if forced_draft is not None
@@ -175,6 +201,26 @@ class OracleRunner:
         return RoundRecord(draft=d, verify=v, y_hat=y_hat, y_t=y_t, A=A, committed=new,
                            cond_len=cond_len, P=P)
 
+    def sample_round(self, st: SeqState, forced_draft: Optional[Sequence[int]] = None) -> RoundRecord:
+        """A round under temperature sampling: drafts drawn from the drafter's filtered
+        distributions, speculative-sampling acceptance against the target's."""
+        P, cond_len, B = st.P, st.cond_len, self.B
+        rnd = st.rnd + 1
+        d = self.draft(st)
+        q = [self.dist(d.logits[i]) for i in range(1, B + 1)]
+        if forced_draft is not None:
+            y_hat = np.asarray(forced_draft, dtype=np.int64)
+        else:
+            y_hat = np.array([smp.sample(q[i - 1], self.u(st, rnd, smp.U_DRAFT, i)) for i in range(1, B + 1)],
+                             dtype=np.int64)
+        v = self.verify(st, y_hat)
+        p = [self.dist(v.logits[i]) for i in range(B + 1)]
+        u_acc = [self.u(st, rnd, smp.U_ACCEPT, i) for i in range(1, B + 1)]
+        A, corr = smp.speculative_accept(y_hat, q, p, u_acc, self.u(st, rnd, smp.U_RESAMPLE, 0))
+        A, new = self.commit_tokens(st, y_hat, A, corr, d, v)
+        return RoundRecord(draft=d, verify=v, y_hat=y_hat, y_t=argmax_rows(v.logits), A=A, committed=new,
+                           cond_len=cond_len, P=P)
+
     def spec_decode(self, prompt, budget: int, max_rounds: Optional[int] = None):
         st = self.prefill(prompt, budget)
         recs = []
@@ -183,16 +229,20 @@ class OracleRunner:
         return st.generated, recs, st
 
     # -- references
-    def ar_decode(self, prompt, n_new: int) -> List[int]:
-        """Target-only greedy decoding: one row per step, n_new tokens."""
+    def ar_decode(self, prompt, n_new: int, seq: int = 0) -> List[int]:
+        """Target-only decoding, one row per step, n_new tokens: greedy, or under
+        temperature sampling with the step index as the draw's round."""
         m = self.m
         st = m.new_state(prompt, n_new)
+        st.seq = seq
+        pick = ((lambda row, k: smp.sample(self.dist(row), self.u(st, k, smp.U_STEP if k else smp.U_FIRST, 0)))
+                if self.sampling else (lambda row, k: int(argmax_rows(row))))
         out = m.target_forward(st, prompt, 0)
-        tok = int(argmax_rows(out.logits[-1]))
+        tok = pick(out.logits[-1], 0)
         toks, pos = [tok], len(prompt)
         while len(toks) < n_new:
             out = m.target_forward(st, [tok], pos)
-            tok = int(argmax_rows(out.logits[-1]))
+            tok = pick(out.logits[-1], len(toks))
             toks.append(tok)
             pos += 1
         return toks

@@ -51,6 +51,10 @@ class Workload:
     page_size: int = 16
     beta: float = 1.0
     cond_mode: str = "retrace"      # "retrace" (corrected, gated), "raw_gated", "overwrite", "off"
+    temperature: float = 0.0        # 0: greedy; > 0: speculative sampling with top-k / top-p
+    top_k: int = 20
+    top_p: float = 0.95
+    sample_seed: int = 42
     init_std: float = 0.02
     norm_init: str = "ones"         # "ones" or "perturbed" (1 + 0.1 N(0,1)); tests use both
 
