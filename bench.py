@@ -46,7 +46,8 @@ def build_engine(wl, W):
     cfg = config_from(wl.target, dtype=wl.dtype, draft_layers=wl.draft_layers, cond_layers=wl.cond_layers,
                       block_size=wl.block_size, mask_token_id=wl.mask_token_id, max_batch=wl.batch,
                       max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps, beta=wl.beta,
-                      cond_mode=B.COND_MODES[wl.cond_mode])
+                      cond_mode=B.COND_MODES[wl.cond_mode], temperature=wl.temperature, top_k=wl.top_k,
+                      top_p=wl.top_p, sample_seed=wl.sample_seed)
     return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
 
 
@@ -106,7 +107,7 @@ def cpu_baseline(eng, wl, W, prompts, seconds: float):
     s = wl.target
     model = OracleModel(wl, W)
     R = OracleRunner(model)
-    st_arr = eng.read(B.RT_T_STATE, 0, (8,), np.int32)
+    st_arr = eng.read(B.RT_T_STATE, 0, (9,), np.int32)
     P = int(st_arr[0])
     st = model.new_state(prompts[0], wl.new_tokens)
     et = np.uint16 if wl.dtype == "bf16" else np.float32
@@ -123,6 +124,7 @@ def cpu_baseline(eng, wl, W, prompts, seconds: float):
     st.hD_prev = eng.read(B.RT_T_HD, 0, (wl.block_size, s.hidden), kd).astype(np.float64)
     st.hT_prev = eng.read(B.RT_T_HT, 0, (wl.block_size, s.hidden), kd).astype(np.float64)
     st.P, st.anchor, st.r, st.cond_len = P, int(st_arr[1]), int(st_arr[2]), int(st_arr[3])
+    st.rnd = int(st_arr[8])
     st.generated = [0] * (wl.new_tokens - int(st_arr[4]))
     # one-time float64 conversion of the weights (the oracle's setup) outside the sample
     t0 = time.perf_counter()
@@ -180,6 +182,8 @@ def main():
     ap.add_argument("--ar-steps", type=int, default=64, help="timed target-only greedy steps (0: skip)")
     ap.add_argument("--cond-mode", choices=["retrace", "raw_gated", "overwrite", "off"], default="retrace",
                     help="drafter conditioning: the method, a component-ablation variant, or none")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="0: greedy; > 0: speculative sampling with the workload's top-k / top-p (20 / 0.95)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB copies (reference reading for the HBM byte counters)")
     args = ap.parse_args()
@@ -191,7 +195,7 @@ def main():
     import torch
     from workloads import get, make_prompts, make_weights
 
-    over = {"cond_mode": args.cond_mode}
+    over = {"cond_mode": args.cond_mode, "temperature": args.temperature}
     if args.batch is not None:
         over["batch"] = args.batch
     wl = get(args.workload, **over)
@@ -283,7 +287,8 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "prompt_len": list(wl.prompt_len),
                    "block_size": wl.block_size, "new_tokens": wl.new_tokens, "hidden": wl.target.hidden,
                    "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
-                   "cond_layers": list(wl.cond_layers), "cond_mode": wl.cond_mode, "parallelism": "single GPU"},
+                   "cond_layers": list(wl.cond_layers), "cond_mode": wl.cond_mode, "temperature": wl.temperature,
+                   "top_k": wl.top_k, "top_p": wl.top_p, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": DOMINANT_DESC,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",

@@ -71,7 +71,24 @@ typedef struct rt_config {
   int32_t max_batch;       /* sequences per batch */
   int32_t max_seq_len;     /* per sequence: prompt + generation budget + block_size */
   int32_t page_size;       /* KV page size in tokens; must be 16 */
+  /* Decoding (Section 5 settings: temperature 0 = greedy; temperature 1 with top-k 20,
+   * top-p 0.95).  temperature > 0 selects speculative sampling: drafts are drawn from
+   * the drafter's filtered distribution q, draft i is kept with probability
+   * min(1, p_i / q_i) against the target's filtered distribution p, and the first
+   * rejection draws its correction from the normalised residual max(0, p - q) (a full
+   * block draws a bonus token from the last row), so that committed tokens follow the
+   * target's own filtered sampling.  A filtered distribution divides the logits by the
+   * temperature, keeps the top_k largest (ties to the lowest id), renormalises, and cuts
+   * to the shortest prefix whose cumulative probability reaches top_p.  Draws come from
+   * a Philox4x64-10 counter (round, sequence, purpose, position) under key
+   * (sample_seed, 0). */
+  float temperature;       /* 0 (greedy) or > 0 */
+  int32_t top_k;           /* 1..RT_MAX_TOP_K and <= vocab (used when temperature > 0) */
+  float top_p;             /* (0, 1] (used when temperature > 0) */
+  uint64_t sample_seed;
 } rt_config;
+
+#define RT_MAX_TOP_K 64
 
 typedef struct rt_model rt_model;   /* opaque handle */
 
@@ -215,9 +232,16 @@ enum {
   RT_T_ETILDE = 4,         /* [block][d] f32 conditioned drafter inputs */
   RT_T_DRAFT_TOKENS = 5,   /* [block] int32: anchor, then the B draft tokens */
   RT_T_TARGET_TOKENS = 6,  /* [block] int32: target argmax of verify rows 0..B */
-  RT_T_STATE = 7,          /* [8] int32: seq_len, anchor, r, cond_len, budget, round_pos, append, A */
+  RT_T_STATE = 7,          /* [9] int32: seq_len, anchor, r, cond_len, budget, round_pos, append, A,
+                              rounds (or target-only steps) completed */
   RT_T_G = 8,              /* [block][n_cond*d] captured conditioning-layer states (storage type) */
-  RT_T_AR_LOGITS = 9,      /* [V] f32 logits of the last rt_ar_steps step (needs debug flag 1) */
+  RT_T_AR_LOGITS = 9,      /* [V] f32 logits of the last rt_ar_steps step (needs debug flag 1 or sampling) */
+  /* sampling (temperature > 0): filtered distributions of the last round, [block][RT_MAX_TOP_K],
+   * ids in decreasing probability (-1 past the kept entries) and their probabilities */
+  RT_T_DRAFT_DIST_IDS = 10,   /* int32, drafter rows (row 0, the anchor row, is not used) */
+  RT_T_DRAFT_DIST_P = 11,     /* f32 */
+  RT_T_VERIFY_DIST_IDS = 12,  /* int32, target rows 0..B */
+  RT_T_VERIFY_DIST_P = 13,    /* f32 */
   RT_T_TARGET_K = 100,     /* + layer: [pos][Hkv][hd] storage type, positions 0.. */
   RT_T_TARGET_V = 200,     /* + layer */
   RT_T_DRAFT_K = 300,      /* + drafter layer: context keys */

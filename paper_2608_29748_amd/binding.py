@@ -25,7 +25,9 @@ COND_MODES = {"off": RT_COND_OFF, "retrace": RT_COND_RETRACE, "raw_gated": RT_CO
               "overwrite": RT_COND_OVERWRITE}
 RT_MAX_COND_LAYERS = 8
 (RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
- RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G, RT_T_AR_LOGITS) = range(10)
+ RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G, RT_T_AR_LOGITS, RT_T_DRAFT_DIST_IDS, RT_T_DRAFT_DIST_P,
+ RT_T_VERIFY_DIST_IDS, RT_T_VERIFY_DIST_P) = range(14)
+RT_MAX_TOP_K = 64
 RT_AR_MAX_STEPS = 256
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
 (RT_K_GEMM_QKV, RT_K_GEMM_O, RT_K_GEMM_GATE_UP, RT_K_GEMM_DOWN, RT_K_GEMM_CONTEXT, RT_K_GEMM_COND,
@@ -55,7 +57,8 @@ class rt_config(C.Structure):
                 ("cond_layer_ids", C.c_int32 * RT_MAX_COND_LAYERS), ("block_size", C.c_int32),
                 ("mask_token_id", C.c_int32), ("beta", C.c_float), ("cond_mode", C.c_int32),
                 ("dtype", C.c_int32), ("max_batch", C.c_int32), ("max_seq_len", C.c_int32),
-                ("page_size", C.c_int32)]
+                ("page_size", C.c_int32), ("temperature", C.c_float), ("top_k", C.c_int32),
+                ("top_p", C.c_float), ("sample_seed", C.c_uint64)]
 
 
 class rt_kernel_stat(C.Structure):

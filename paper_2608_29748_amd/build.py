@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libretrace.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["gemm.hip", "gemm_mid.hip", "attn.hip", "misc.hip", "engine.hip", "validate.cpp"]
+SOURCES = ["gemm.hip", "gemm_mid.hip", "attn.hip", "misc.hip", "sample.hip", "engine.hip", "validate.cpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          # packed fp32 vector ops stay off: hipcc otherwise forms them from float code
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -11,6 +11,7 @@
 #include "gemm.h"
 #include "host.h"
 #include "misc.h"
+#include "sample.h"
 
 namespace rt {
 const char* last_error();
@@ -323,6 +324,22 @@ struct Engine : EngineBase {
     return RT_OK;
   }
 
+  bool sampling() const { return cfg.temperature > 0.f; }
+  // Filtered distributions of `rows` rows of fp32 logits (and, per mode, one draw per row).
+  int dists(const float* logits, int rows, int32_t* ids, float* probs, int mode, int seq0, int32_t* tok_out) {
+    const Plan& q = p;
+    DistArgs d{};
+    d.logits = logits; d.ldl = q.V; d.V = q.V; d.rows = rows;
+    d.top_k = cfg.top_k; d.inv_temp = 1.0f / cfg.temperature; d.top_p = cfg.top_p;
+    d.ids = ids; d.probs = probs; d.ldd = kMaxTopK;
+    d.mode = mode; d.state = at<int32_t>(q.state); d.state_stride = kStateFields; d.bk = q.bk; d.seq0 = seq0;
+    d.seed = cfg.sample_seed; d.tok_out = tok_out;
+    prof_begin(RT_K_MISC, (double)rows * q.V * 4 * 4, 0);
+    HIPCHK(filtered_dists(d, stream));
+    prof_end();
+    return RT_OK;
+  }
+
   int cond_slot(int l) const {
     for (int i = 0; i < cfg.n_cond_layers; ++i)
       if (cfg.cond_layer_ids[i] == l) return i;
@@ -452,8 +469,13 @@ struct Engine : EngineBase {
         if (c0 + n == len) {
           rmsnorm<T, K>(at<float>(q.x) + (size_t)(n - 1) * q.d, q.d, at<T>(q.t_final_norm), q.d, cfg.rms_eps, 1,
                         at<T>(q.xa), 16 * q.Kp_d, nullptr, 0, NormFold{}, stream);
-          CHK(lm_head_argmax(1, at<uint64_t>(q.tkeys), nullptr));
-          first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), len, budget, at<int32_t>(q.first_tok), stream);
+          const bool smp = sampling();
+          CHK(lm_head_argmax(1, at<uint64_t>(q.tkeys), smp ? at<float>(q.vlogits) : nullptr));
+          if (smp)
+            CHK(dists(at<float>(q.vlogits), 1, at<int32_t>(q.dist_ids_v), at<float>(q.dist_p_v), SAMPLE_FIRST, s,
+                      at<int32_t>(q.stok)));
+          first_token(at<int32_t>(q.state), s, at<uint64_t>(q.tkeys), smp ? at<int32_t>(q.stok) : nullptr, len, budget,
+                      at<int32_t>(q.first_tok), stream);
         }
         HIPCHK(hipGetLastError());
       }
@@ -520,12 +542,17 @@ struct Engine : EngineBase {
     }
     stage(2);
     norm_x(at<T>(q.d_final_norm), R, at<K>(q.hd_keep), q.d);
-    CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (flags & 1) ? at<float>(q.dlogits) : nullptr));
+    const bool smp = sampling();
+    CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (smp || (flags & 1)) ? at<float>(q.dlogits) : nullptr));
+    // sampling: the drafter's filtered distributions, drafts drawn into dtok (unless forced)
+    if (smp)
+      CHK(dists(at<float>(q.dlogits), R, at<int32_t>(q.dist_ids_d), at<float>(q.dist_p_d), SAMPLE_DRAFT, 0,
+                forced ? nullptr : at<int32_t>(q.dtok)));
     // (3) verify: [anchor, drafts] at P..P+B, causal over the target cache
     stage(3);
     prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 4), 0);
-    embed_verify<T>(at<T>(q.embed), q.d, st, at<uint64_t>(q.dkeys), forced ? 1 : 0, at<int32_t>(q.dtok), n_seqs,
-                    q.bk, x, q.d, stream);
+    embed_verify<T>(at<T>(q.embed), q.d, st, at<uint64_t>(q.dkeys), (forced || smp) ? 1 : 0, at<int32_t>(q.dtok),
+                    n_seqs, q.bk, x, q.d, stream);
     prof_end();
     for (int l = 0; l < q.L; ++l) {
       const int slot = cond_slot(l);
@@ -536,12 +563,24 @@ struct Engine : EngineBase {
     }
     stage(4);
     norm_x(at<T>(q.t_final_norm), R, at<K>(q.ht_keep), q.d);
-    CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
+    CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (smp || (flags & 1)) ? at<float>(q.vlogits) : nullptr));
+    if (smp)
+      CHK(dists(at<float>(q.vlogits), R, at<int32_t>(q.dist_ids_v), at<float>(q.dist_p_v), SAMPLE_NONE, 0, nullptr));
     // (4) acceptance, commit, rollback, carry / reset
     stage(5);
     prof_begin(RT_K_MISC, (double)R * 16, 0);
-    accept(st, at<int32_t>(q.dtok), at<uint64_t>(q.tkeys), at<int32_t>(q.ttok), n_seqs, q.bk, at<int32_t>(q.out_tok),
-           at<int32_t>(q.out_n), at<int32_t>(q.out_a), stream);
+    if (smp) {
+      AcceptSampleArgs g{};
+      g.state = st; g.state_stride = kStateFields; g.dtok = at<int32_t>(q.dtok);
+      g.q_ids = at<int32_t>(q.dist_ids_d); g.q_p = at<float>(q.dist_p_d);
+      g.p_ids = at<int32_t>(q.dist_ids_v); g.p_p = at<float>(q.dist_p_v); g.ldd = kMaxTopK;
+      g.tkeys = at<uint64_t>(q.tkeys); g.ttok = at<int32_t>(q.ttok); g.bk = q.bk; g.seed = cfg.sample_seed;
+      g.out_tok = at<int32_t>(q.out_tok); g.out_n = at<int32_t>(q.out_n); g.out_a = at<int32_t>(q.out_a);
+      HIPCHK(accept_sampled(g, n_seqs, stream));
+    } else {
+      accept(st, at<int32_t>(q.dtok), at<uint64_t>(q.tkeys), at<int32_t>(q.ttok), n_seqs, q.bk, at<int32_t>(q.out_tok),
+             at<int32_t>(q.out_n), at<int32_t>(q.out_a), stream);
+    }
     prof_end();
     // drafter context pathway for the committed rows 0..A at P..P+A
     stage(6);
@@ -551,9 +590,11 @@ struct Engine : EngineBase {
     return RT_OK;
   }
 
-  // One target-only greedy step: the anchor row of every sequence at position seq_len.
+  // One target-only step (greedy or sampled): the anchor row of every sequence at position seq_len.
   int run_ar_step() override {
     const Plan& q = p;
+    static_assert(kStateFields <= kStateSlots, "per-sequence state exceeds its slots");
+    static_assert(kMaxTopK == RT_MAX_TOP_K, "distribution width");
     static_assert(kAttnRowsAr == kAttnRows, "target-only steps use the 64-row attention blocks");
     const int M = n_seqs;
     int32_t* st = at<int32_t>(q.state);
@@ -569,10 +610,14 @@ struct Engine : EngineBase {
       CHK(layer(tlayer(l), c));
     }
     norm_x(at<T>(q.t_final_norm), M, nullptr, 0);
-    CHK(lm_head_argmax(M, at<uint64_t>(q.tkeys), (flags & 1) ? at<float>(q.vlogits) : nullptr));
+    const bool smp = sampling();
+    CHK(lm_head_argmax(M, at<uint64_t>(q.tkeys), (smp || (flags & 1)) ? at<float>(q.vlogits) : nullptr));
+    if (smp)
+      CHK(dists(at<float>(q.vlogits), M, at<int32_t>(q.dist_ids_v), at<float>(q.dist_p_v), SAMPLE_STEP, 0,
+                at<int32_t>(q.stok)));
     prof_begin(RT_K_MISC, (double)M * 16, 0);
-    ar_commit(st, at<uint64_t>(q.tkeys), n_seqs, at<int32_t>(q.ar_tok), kArMaxSteps, at<int32_t>(q.pf_ints) + 8,
-              stream);
+    ar_commit(st, at<uint64_t>(q.tkeys), smp ? at<int32_t>(q.stok) : nullptr, n_seqs, at<int32_t>(q.ar_tok),
+              kArMaxSteps, at<int32_t>(q.pf_ints) + 8, stream);
     prof_end();
     HIPCHK(hipGetLastError());
     return RT_OK;
@@ -796,6 +841,10 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
     case RT_T_TARGET_TOKENS: off = q.ttok + seq * bk * 4; cap = bk * 4; break;
     case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
     case RT_T_AR_LOGITS: off = q.vlogits + seq * (size_t)q.V * 4; cap = (size_t)q.V * 4; break;
+    case RT_T_DRAFT_DIST_IDS: off = q.dist_ids_d + seq * bk * RT_MAX_TOP_K * 4; cap = bk * RT_MAX_TOP_K * 4; break;
+    case RT_T_DRAFT_DIST_P: off = q.dist_p_d + seq * bk * RT_MAX_TOP_K * 4; cap = bk * RT_MAX_TOP_K * 4; break;
+    case RT_T_VERIFY_DIST_IDS: off = q.dist_ids_v + seq * bk * RT_MAX_TOP_K * 4; cap = bk * RT_MAX_TOP_K * 4; break;
+    case RT_T_VERIFY_DIST_P: off = q.dist_p_v + seq * bk * RT_MAX_TOP_K * 4; cap = bk * RT_MAX_TOP_K * 4; break;
     case RT_T_G: {
       // packed [group][k tile][lane][8] -> row-major [bk][n_cond * d]
       const size_t ncd = (size_t)q.nc * q.d, ldg = (size_t)16 * q.Kp_nc;

@@ -25,6 +25,7 @@ constexpr size_t kPartialFloats = (size_t)8 << 20;   // split-K partial capacity
 constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections
 constexpr int kArMaxSteps = RT_AR_MAX_STEPS;   // target-only greedy steps per rt_ar_steps call
 constexpr int kAttnRowsAr = 64;   // attention rows per block in target-only steps (the 64-row kernel)
+constexpr int kStateSlots = 16;   // int32 slots of per-sequence round state (fields in misc.h)
 
 struct Plan {
   // dimensions
@@ -50,6 +51,9 @@ struct Plan {
   size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys
   size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplits][rpart_rows][d]
   size_t ar_tok;                 // target-only step tokens [bmax][kArMaxSteps]
+  size_t dist_ids_d, dist_p_d;   // sampling: drafter filtered distributions [R][RT_MAX_TOP_K]
+  size_t dist_ids_v, dist_p_v;   // sampling: target filtered distributions [R][RT_MAX_TOP_K]
+  size_t stok;                   // sampling: first / target-only step tokens [bmax]
   int rpart_rows;                // max(32, rows of a round)
   int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init

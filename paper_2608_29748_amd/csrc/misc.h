@@ -15,6 +15,7 @@ enum StateField : int {
   ST_ROUND_POS,      // P of the round just verified (context-append base)
   ST_APPEND,         // rows of that round to append to the drafter context (A + 1, or 0)
   ST_ACCEPT,         // A of the last round
+  ST_ROUND,          // rounds (or target-only steps) completed: the round of the random draws
   kStateFields
 };
 
@@ -54,10 +55,12 @@ void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t*
             int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
 // Target-only greedy step commit for n_seqs (<= 1024) sequences: tokens go to column
 // *step of out (row stride ld_out), then *step is advanced.
-void ar_commit(int32_t* state, const uint64_t* tkeys, int n_seqs, int32_t* out, int ld_out, int32_t* step,
-               hipStream_t s);
+// sampled (may be null): the step's drawn tokens per sequence instead of the argmax keys.
+void ar_commit(int32_t* state, const uint64_t* tkeys, const int32_t* sampled, int n_seqs, int32_t* out, int ld_out,
+               int32_t* step, hipStream_t s);
 void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s);
-void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
+// sampled (may be null): drawn first tokens per sequence instead of the argmax key.
+void first_token(int32_t* state, int seq, const uint64_t* keys, const int32_t* sampled, int prompt_len, int budget,
                  int32_t* first_out, hipStream_t s);
 void fill_zero(void* p, size_t bytes, hipStream_t s);
 

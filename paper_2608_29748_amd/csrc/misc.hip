@@ -252,6 +252,7 @@ __global__ void accept_kernel(int32_t* st_all, const int32_t* __restrict__ dtok,
       st[ST_SEQ_LEN] = P + A + 1;        // rows P+A+1.. of the target KV are rolled back
       st[ST_ANCHOR] = corr;
       st[ST_BUDGET] = budget - n_new;
+      st[ST_ROUND] += 1;
       if (A < B - 1) { st[ST_R] = A + 1; st[ST_COND_LEN] = B - (A + 1); }
       else { st[ST_R] = 0; st[ST_COND_LEN] = 0; }
     } else {
@@ -270,7 +271,8 @@ void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t*
 // K/V of the anchor row were written at position seq_len by this step's layers).  The
 // token goes to out[s * ld_out + k], k = *step, which the last thread advances.
 __global__ __launch_bounds__(1024) void ar_commit_kernel(int32_t* st_all, const uint64_t* __restrict__ tkeys,
-                                                         int n_seqs, int32_t* out, int ld_out, int32_t* step) {
+                                                         const int32_t* sampled, int n_seqs, int32_t* out, int ld_out,
+                                                         int32_t* step) {
   const int k = *step;
   const int sq = threadIdx.x;
   if (sq < n_seqs) {
@@ -278,7 +280,8 @@ __global__ __launch_bounds__(1024) void ar_commit_kernel(int32_t* st_all, const 
     const int budget = st[ST_BUDGET];
     int v = -1;
     if (budget > 0) {
-      v = key_index(tkeys[sq]);
+      v = sampled ? sampled[sq] : key_index(tkeys[sq]);
+      st[ST_ROUND] += 1;
       const int P = st[ST_SEQ_LEN] + 1;
       st[ST_SEQ_LEN] = P;
       st[ST_ANCHOR] = v;
@@ -294,10 +297,10 @@ __global__ __launch_bounds__(1024) void ar_commit_kernel(int32_t* st_all, const 
   __syncthreads();
   if (threadIdx.x == 0) *step = k + 1;
 }
-void ar_commit(int32_t* state, const uint64_t* tkeys, int n_seqs, int32_t* out, int ld_out, int32_t* step,
-               hipStream_t s) {
+void ar_commit(int32_t* state, const uint64_t* tkeys, const int32_t* sampled, int n_seqs, int32_t* out, int ld_out,
+               int32_t* step, hipStream_t s) {
   const int threads = (n_seqs + 63) / 64 * 64;
-  RT_LAUNCH(ar_commit_kernel, dim3(1), dim3(threads), 0, s, state, tkeys, n_seqs, out, ld_out, step);
+  RT_LAUNCH(ar_commit_kernel, dim3(1), dim3(threads), 0, s, state, tkeys, sampled, n_seqs, out, ld_out, step);
 }
 
 __global__ void set_ints_kernel(int32_t* dst, int n, int v0, int v1, int v2, int v3) {
@@ -308,11 +311,11 @@ void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s
   RT_LAUNCH(set_ints_kernel, dim3(1), dim3(64), 0, s, dst, n, v0, v1, v2, v3);
 }
 
-__global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys, int plen, int budget,
-                                   int32_t* first_out) {
+__global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys, const int32_t* sampled, int plen,
+                                   int budget, int32_t* first_out) {
   if (threadIdx.x != 0) return;
   int32_t* st = st_all + sq * kStateFields;
-  const int tok = key_index(keys[0]);
+  const int tok = sampled ? sampled[sq] : key_index(keys[0]);
   st[ST_SEQ_LEN] = plen;
   st[ST_ANCHOR] = tok;
   st[ST_R] = 0;
@@ -321,11 +324,12 @@ __global__ void first_token_kernel(int32_t* st_all, int sq, const uint64_t* keys
   st[ST_ROUND_POS] = plen;
   st[ST_APPEND] = 0;
   st[ST_ACCEPT] = 0;
+  st[ST_ROUND] = 0;
   first_out[sq] = tok;
 }
-void first_token(int32_t* state, int seq, const uint64_t* keys, int prompt_len, int budget,
+void first_token(int32_t* state, int seq, const uint64_t* keys, const int32_t* sampled, int prompt_len, int budget,
                  int32_t* first_out, hipStream_t s) {
-  RT_LAUNCH(first_token_kernel, dim3(1), dim3(64), 0, s, state, seq, keys, prompt_len, budget,
+  RT_LAUNCH(first_token_kernel, dim3(1), dim3(64), 0, s, state, seq, keys, sampled, prompt_len, budget,
                      first_out);
 }
 

@@ -63,6 +63,12 @@ int validate_config(const rt_config* c) {
   if (c->dtype == RT_F32 && c->max_seq_len > 16384)   // fp32 attention keeps a split's page ids in LDS
     return fail(RT_ERR_INVALID, "fp32 storage supports max_seq_len up to 16384");
   if (c->page_size != 16) return fail(RT_ERR_INVALID, "page_size must be 16");
+  if (!(c->temperature >= 0.f) || !isfinite(c->temperature)) return fail(RT_ERR_INVALID, "temperature must be >= 0");
+  if (c->temperature > 0.f) {
+    if (c->top_k < 1 || c->top_k > RT_MAX_TOP_K || c->top_k > c->vocab)
+      return fail(RT_ERR_INVALID, "top_k must be in [1, %d] and at most vocab", RT_MAX_TOP_K);
+    if (!(c->top_p > 0.f && c->top_p <= 1.f)) return fail(RT_ERR_INVALID, "top_p must be in (0, 1]");
+  }
   return RT_OK;
 }
 
@@ -143,7 +149,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.dvc = take(q.cache_layer_elems * e * q.LD);
   q.page_table = take((size_t)q.n_pages * 4);
   q.rope = take((size_t)q.T * (q.hd / 2) * 2 * 4);
-  q.state = take((size_t)q.bmax * 8 * 4);
+  q.state = take((size_t)q.bmax * kStateSlots * 4);
   q.pf_ints = take(16 * 4);
   q.first_tok = take((size_t)q.bmax * 4);
   q.counters = take((size_t)kMaxTiles * 4);
@@ -193,6 +199,11 @@ int make_plan(const rt_config* c, Plan* p) {
   q.out_a = take((size_t)q.bmax * 4);
   q.tokbuf = take((size_t)q.T * 4);
   q.ar_tok = take((size_t)q.bmax * kArMaxSteps * 4);
+  q.dist_ids_d = take((size_t)q.R * RT_MAX_TOP_K * 4);
+  q.dist_p_d = take((size_t)q.R * RT_MAX_TOP_K * 4);
+  q.dist_ids_v = take((size_t)q.R * RT_MAX_TOP_K * 4);
+  q.dist_p_v = take((size_t)q.R * RT_MAX_TOP_K * 4);
+  q.stok = take((size_t)q.bmax * 4);
   q.total = off;
   return RT_OK;
 }

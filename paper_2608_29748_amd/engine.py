@@ -13,7 +13,8 @@ from . import binding as B
 def config_from(shape, *, dtype: str, draft_layers: int, cond_layers: Sequence[int], block_size: int,
                 mask_token_id: int, max_batch: int, max_seq_len: int, rope_theta: float = 1e6,
                 rms_eps: float = 1e-6, beta: float = 1.0, cond_mode: int = B.RT_COND_RETRACE,
-                page_size: int = 16) -> B.rt_config:
+                page_size: int = 16, temperature: float = 0.0, top_k: int = 20, top_p: float = 0.95,
+                sample_seed: int = 42) -> B.rt_config:
     """rt_config from a model-shape object with vocab / hidden / n_layers / n_q_heads /
     n_kv_heads / head_dim / ffn attributes."""
     return B.make_config(
@@ -22,7 +23,8 @@ def config_from(shape, *, dtype: str, draft_layers: int, cond_layers: Sequence[i
         rms_eps=rms_eps, draft_layers=draft_layers, cond_layer_ids=list(cond_layers),
         block_size=block_size, mask_token_id=mask_token_id, beta=beta, cond_mode=cond_mode,
         dtype=B.RT_BF16 if dtype == "bf16" else B.RT_F32, max_batch=max_batch,
-        max_seq_len=max_seq_len, page_size=page_size)
+        max_seq_len=max_seq_len, page_size=page_size, temperature=temperature, top_k=top_k, top_p=top_p,
+        sample_seed=sample_seed)
 
 
 class RoundEngine:

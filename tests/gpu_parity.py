@@ -33,7 +33,8 @@ def engine_for(wl, W, max_batch=None, cond_mode=None):
                       cond_layers=wl.cond_layers, block_size=wl.block_size,
                       mask_token_id=wl.mask_token_id, max_batch=max_batch or wl.batch,
                       max_seq_len=wl.max_seq_len, rope_theta=wl.rope_theta, rms_eps=wl.rms_eps,
-                      beta=wl.beta, cond_mode=cond_mode)
+                      beta=wl.beta, cond_mode=cond_mode, temperature=wl.temperature, top_k=wl.top_k,
+                      top_p=wl.top_p, sample_seed=wl.sample_seed)
     return RoundEngine(cfg, [W[name] for name, _, _ in weight_specs(wl)])
 
 

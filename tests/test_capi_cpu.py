@@ -67,6 +67,11 @@ def test_workspace_and_weight_count(B):
     (dict(draft_layers=0), "draft_layers"),
     (dict(dtype=7), "dtype"),
     (dict(cond_mode=4), "cond_mode"),
+    (dict(temperature=-1.0), "temperature"),
+    (dict(temperature=1.0, top_k=0, top_p=0.9), "top_k"),
+    (dict(temperature=1.0, top_k=65, top_p=0.9), "top_k"),
+    (dict(temperature=1.0, top_k=20, top_p=0.0), "top_p"),
+    (dict(temperature=1.0, top_k=20, top_p=1.5), "top_p"),
     (dict(cond_mode=-1), "cond_mode"),
     (dict(max_seq_len=4), "max_seq_len"),
     (dict(max_batch=0), "max_batch"),
