@@ -335,7 +335,7 @@ struct Engine : EngineBase {
     d.mode = mode; d.state = at<int32_t>(q.state); d.state_stride = kStateFields; d.bk = q.bk; d.seq0 = seq0;
     d.seed = cfg.sample_seed; d.tok_out = tok_out;
     prof_begin(RT_K_MISC, (double)rows * q.V * 4 * 4, 0);
-    HIPCHK(filtered_dists(d, stream));
+    HIPCHK(filtered_dists(d, at<uint64_t>(q.topk_cand), stream));
     prof_end();
     return RT_OK;
   }
@@ -595,6 +595,7 @@ struct Engine : EngineBase {
     const Plan& q = p;
     static_assert(kStateFields <= kStateSlots, "per-sequence state exceeds its slots");
     static_assert(kMaxTopK == RT_MAX_TOP_K, "distribution width");
+    static_assert(kTopkChunk == kSelectChunk, "top-k stage size");
     static_assert(kAttnRowsAr == kAttnRows, "target-only steps use the 64-row attention blocks");
     const int M = n_seqs;
     int32_t* st = at<int32_t>(q.state);

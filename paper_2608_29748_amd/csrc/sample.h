@@ -6,6 +6,7 @@
 namespace rt {
 
 constexpr int kMaxTopK = 64;   // entries of a filtered distribution (one per lane of a wave)
+constexpr int kSelectChunk = 8192;   // logits per workgroup of the first top-k stage
 
 // purposes of a random draw (the counter is (round, sequence, purpose, position))
 enum DrawPurpose : int { U_DRAFT = 1, U_ACCEPT = 2, U_RESAMPLE = 3, U_FIRST = 4, U_STEP = 5 };
@@ -27,10 +28,13 @@ struct DistArgs {
   int32_t* tok_out;                                // may be null (draft tokens given by the host)
 };
 
-// One workgroup per row: the top_k largest logits (ties to the lowest id) by radix
-// selection, the filtered distribution (temperature, top-k, top-p on the renormalised
-// top-k probabilities) and, per mode, one inverse-CDF draw.
-hipError_t filtered_dists(const DistArgs& a, hipStream_t s);
+// The top_k largest logits of each row (ties to the lowest id) in two stages -- every
+// 8192-logit chunk keeps its top_k keys in `cand` ([rows][topk_chunks(V)][kMaxTopK]
+// 64-bit keys), then one wave per row folds those -- followed by the filtered
+// distribution (temperature, top-k, top-p on the renormalised top-k probabilities)
+// and, per mode, one inverse-CDF draw.
+int topk_chunks(int V);
+hipError_t filtered_dists(const DistArgs& a, uint64_t* cand, hipStream_t s);
 
 struct AcceptSampleArgs {
   int32_t* state; int state_stride;

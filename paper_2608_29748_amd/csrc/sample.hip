@@ -44,127 +44,76 @@ __device__ __forceinline__ float wave_scan_f(float v, int lane) {
 // ------------------------------------------------------------------ filtered distributions
 
 constexpr int kDistThreads = 256;
+constexpr int kChunk = kSelectChunk;
 
-// Finds, from the top, the bin where the suffix count reaches `need` among nb bins of
-// hist (nb / kDistThreads consecutive bins per thread).  Returns the bin in *bin and the
-// count of the bins above it in *above.
-template <int NB>
-__device__ void suffix_find(const uint32_t* hist, uint32_t need, uint32_t* part, int* bin, uint32_t* above) {
-  constexpr int PER = NB / kDistThreads;
-  const int t = threadIdx.x;
-  uint32_t mine = 0;
-#pragma unroll
-  for (int j = 0; j < PER; ++j) mine += hist[t * PER + j];
-  part[t] = mine;
-  __syncthreads();
-  // inclusive suffix sums of the per-thread counts (Hillis-Steele over 256 entries)
-  for (int o = 1; o < kDistThreads; o <<= 1) {
-    const uint32_t v = t + o < kDistThreads ? part[t + o] : 0u;
-    __syncthreads();
-    part[t] += v;
-    __syncthreads();
-  }
-  const uint32_t incl = part[t];            // counts of threads t.. (bins >= t*PER)
-  const uint32_t excl = incl - mine;        // bins above this thread's range
-  if (excl < need && incl >= need) {
-    uint32_t acc = excl;
-    for (int j = PER - 1; j >= 0; --j) {
-      const uint32_t h = hist[t * PER + j];
-      if (acc + h >= need) {
-        *bin = t * PER + j;
-        *above = acc;
-        break;
-      }
-      acc += h;
-    }
-  }
-  __syncthreads();
+// key of logit i: orderable value above, (0xffffffff - i) below, so that the larger
+// key is the larger logit and, among equal logits, the lower id; 0 marks padding
+__device__ __forceinline__ uint64_t logit_key(float v, int i) {
+  return ((uint64_t)orderable(v) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
 }
+__device__ __forceinline__ uint64_t kmax(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint64_t kmin(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
-__global__ __launch_bounds__(kDistThreads) void filtered_dist_kernel(DistArgs a) {
-  __shared__ uint32_t hist[4096];
-  __shared__ uint32_t part[kDistThreads];
-  __shared__ int s_bin;
-  __shared__ uint32_t s_above, s_ngt, s_base;
-  __shared__ uint64_t cand[kMaxTopK];
-  __shared__ uint32_t wcnt[kDistThreads / 64];
-  const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const float* z = a.logits + (size_t)row * a.ldl;
-  const int V = a.V, K = a.top_k;
-
-  if (t == 0) { s_bin = 0; s_above = 0u; }
-  __syncthreads();
-  // radix selection of the K-th largest orderable key: 12, 12 and 8 bits
-  uint32_t prefix = 0u, mask = 0u, need = (uint32_t)K;
-  const int shifts[3] = {20, 8, 0}, widths[3] = {12, 12, 8};
-#pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int sh = shifts[pass], nb = 1 << widths[pass];
-    for (int b = t; b < nb; b += kDistThreads) hist[b] = 0u;
-    __syncthreads();
-    for (int i = t; i < V; i += kDistThreads) {
-      const uint32_t k = orderable(z[i]);
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> sh) & (nb - 1)], 1u);
-    }
-    __syncthreads();
-    if (nb == 4096) suffix_find<4096>(hist, need, part, &s_bin, &s_above);
-    else suffix_find<256>(hist, need, part, &s_bin, &s_above);
-    prefix |= (uint32_t)s_bin << sh;
-    mask |= (uint32_t)(nb - 1) << sh;
-    need -= s_above;
-    __syncthreads();
-  }
-  // prefix is now the K-th largest key: K - need keys lie above it, and the `need`
-  // lowest indices holding it complete the set; n_eq keys hold it in all
-  const uint32_t n_eq = hist[s_bin];
-  if (t == 0) { s_ngt = 0u; s_base = 0u; }
-  __syncthreads();
-  const uint32_t n_gt = (uint32_t)K - need;
-  if (n_eq == need) {
-    // every key at or above the K-th is taken: no ordering by index needed
-    for (int i = t; i < V; i += kDistThreads) {
-      const uint32_t k = orderable(z[i]);
-      if (k >= prefix) {
-        const uint32_t slot = atomicAdd(&s_ngt, 1u);
-        if (slot < (uint32_t)kMaxTopK) cand[slot] = ((uint64_t)k << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-      }
-    }
-  } else {
-    // ties at the K-th key: rank the tied indices in index order
-    for (int i0 = 0; i0 < V; i0 += kDistThreads) {
-      const int i = i0 + t;
-      const uint32_t k = i < V ? orderable(z[i]) : 0u;
-      if (i < V && k > prefix) {
-        const uint32_t slot = atomicAdd(&s_ngt, 1u);
-        if (slot < n_gt) cand[slot] = ((uint64_t)k << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-      }
-      const bool eq = i < V && k == prefix;
-      const uint64_t bal = __ballot(eq);
-      if (lane == 0) wcnt[w] = (uint32_t)__popcll(bal);
-      __syncthreads();
-      uint32_t before = s_base;
-      for (int v = 0; v < w; ++v) before += wcnt[v];
-      const uint32_t rank = before + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
-      if (eq && rank < need) cand[n_gt + rank] = ((uint64_t)k << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-      __syncthreads();
-      if (t == 0) s_base += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
-      __syncthreads();
-    }
-  }
-  __syncthreads();
-
-  if (w != 0) return;
-  // wave 0: sort the K keys (value descending, index ascending), then the distribution
-  uint64_t key = lane < K ? cand[lane] : 0ull;
+// Sorts one key per lane into decreasing order across the wave (bitonic network).
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t v, int lane) {
 #pragma unroll
   for (int k2 = 2; k2 <= 64; k2 <<= 1)
 #pragma unroll
     for (int j = k2 >> 1; j > 0; j >>= 1) {
-      const uint64_t o = __shfl_xor(key, j, 64);
-      const bool keep_max = ((lane & k2) == 0) == ((lane & j) == 0);
-      key = keep_max ? (key > o ? key : o) : (key < o ? key : o);
+      const uint64_t o = __shfl_xor(v, j, 64);
+      v = (((lane & k2) == 0) == ((lane & j) == 0)) ? kmax(v, o) : kmin(v, o);
     }
-  const bool valid = lane < K;
+  return v;
+}
+// The 64 largest of two decreasing wave lists, decreasing: the elementwise maximum of
+// one list and the other reversed is a bitonic sequence holding exactly those keys,
+// which the half-cleaner cascade then sorts.
+__device__ __forceinline__ uint64_t wave_merge_top(uint64_t list, uint64_t batch_sorted, int lane) {
+  uint64_t m = kmax(list, __shfl(batch_sorted, 63 - lane, 64));
+#pragma unroll
+  for (int j = 32; j > 0; j >>= 1) {
+    const uint64_t o = __shfl_xor(m, j, 64);
+    m = ((lane & j) == 0) ? kmax(m, o) : kmin(m, o);
+  }
+  return m;
+}
+
+// Stage 1: workgroup (c, row) keeps the 64 largest keys of logits c*kChunk .. of its row:
+// each wave folds batches of 64 logits into a running top-64, then wave 0 folds the
+// other waves' lists and stores its top_k keys.
+__global__ __launch_bounds__(kDistThreads) void topk_chunk_kernel(DistArgs a, uint64_t* cand, int n_chunks) {
+  __shared__ uint64_t lists[kDistThreads / 64][64];
+  const int c = blockIdx.x, row = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const float* z = a.logits + (size_t)row * a.ldl;
+  const int i0 = c * kChunk, i1 = min(a.V, i0 + kChunk);
+  uint64_t top = 0ull;
+  for (int b = i0 + w * 64; b < i1; b += kDistThreads) {
+    const int i = b + lane;
+    const uint64_t k = i < i1 ? logit_key(z[i], i) : 0ull;
+    top = wave_merge_top(top, wave_sort_desc(k, lane), lane);
+  }
+  lists[w][lane] = top;
+  __syncthreads();
+  if (w != 0) return;
+  for (int v = 1; v < kDistThreads / 64; ++v) top = wave_merge_top(top, lists[v][lane], lane);
+  if (lane < a.top_k) cand[((size_t)row * n_chunks + c) * kMaxTopK + lane] = top;
+}
+
+// Stage 2: one wave per row folds the chunks' candidates into the row's top_k keys,
+// forms the filtered distribution from them and, per mode, draws one token.
+__global__ __launch_bounds__(64) void filtered_dist_kernel(DistArgs a, const uint64_t* cand, int n_chunks) {
+  const int row = blockIdx.x, lane = threadIdx.x;
+  const float* z = a.logits + (size_t)row * a.ldl;
+  const int K = a.top_k;
+  const int n_cand = n_chunks * K;
+  uint64_t key = 0ull;
+  for (int b = 0; b < n_cand; b += 64) {
+    const int j = b + lane;
+    const uint64_t k = j < n_cand ? cand[((size_t)row * n_chunks + j / K) * kMaxTopK + j % K] : 0ull;
+    key = wave_merge_top(key, wave_sort_desc(k, lane), lane);
+  }
+  // the K largest keys in order (value descending, index ascending)
+  const bool valid = lane < K && key != 0ull;
   const int id = valid ? key_index(key) : -1;
   const float lg = valid ? z[id] : 0.f;
   const float l0 = __shfl(lg, 0, 64);
@@ -202,10 +151,14 @@ __global__ __launch_bounds__(kDistThreads) void filtered_dist_kernel(DistArgs a)
   if (lane == 0) a.tok_out[a.mode == SAMPLE_DRAFT ? row : s] = tok;
 }
 
-hipError_t filtered_dists(const DistArgs& a, hipStream_t s) {
+int topk_chunks(int V) { return (V + kChunk - 1) / kChunk; }
+
+hipError_t filtered_dists(const DistArgs& a, uint64_t* cand, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   if (a.top_k < 1 || a.top_k > kMaxTopK || a.top_k > a.V || a.ldd < kMaxTopK) return hipErrorInvalidValue;
-  RT_LAUNCH(filtered_dist_kernel, dim3(a.rows), dim3(kDistThreads), 0, s, a);
+  const int nc = topk_chunks(a.V);
+  RT_LAUNCH(topk_chunk_kernel, dim3(nc, a.rows), dim3(kDistThreads), 0, s, a, cand, nc);
+  RT_LAUNCH(filtered_dist_kernel, dim3(a.rows), dim3(64), 0, s, a, cand, nc);
   return hipGetLastError();
 }
 

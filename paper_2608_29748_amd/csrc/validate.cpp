@@ -204,6 +204,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.dist_ids_v = take((size_t)q.R * RT_MAX_TOP_K * 4);
   q.dist_p_v = take((size_t)q.R * RT_MAX_TOP_K * 4);
   q.stok = take((size_t)q.bmax * 4);
+  q.topk_cand = take((size_t)q.R * ((q.V + kTopkChunk - 1) / kTopkChunk) * RT_MAX_TOP_K * 8);
   q.total = off;
   return RT_OK;
 }
