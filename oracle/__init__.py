@@ -13,6 +13,11 @@ Parity status per part (what pins each one lives in tests/test_oracle_*.py):
   target (Qwen3-style) forward ..................... transformers' Qwen3 on CPU, brute force
   conditioning (Eq.5-9) ............................ special-case closed forms, Fig.3 indices,
                                                      W_v = 0 and beta = 0 reductions
+  ablation and low-rank conditioning forms ......... closed forms; the low-rank form (a
+                                                     reading of one sentence of the paper)
+                                                     is pinned only by its reduction to the
+                                                     full form: parity unpinned against the
+                                                     paper
   acceptance / rollback / losslessness ............. target-only greedy decode, planted drafts
   temperature sampling (sampling.py) ............... Philox4x64-10 against numpy's generator,
                                                      filtered-distribution closed forms, the

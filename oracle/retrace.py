@@ -53,7 +53,7 @@ def align_rejected(hD_prev: np.ndarray, hT_prev: np.ndarray, r: int, B: int):
 
 def condition_inputs(e: np.ndarray, m: np.ndarray, u: np.ndarray, cond_len: int,
                      w_c: np.ndarray, w_v: np.ndarray, w_g: np.ndarray,
-                     beta: float, mode: str = "retrace") -> np.ndarray:
+                     beta: float, mode: str = "retrace", lowrank=None) -> np.ndarray:
     """Eq.7 (correction), Eq.8 (corrected signal), Eq.9 (gated residual) for rows
     j = 1..cond_len.  Weight matrices are [out][in]; W_c's first d input columns
     act on m and W_g's first d on e.
@@ -61,11 +61,26 @@ def condition_inputs(e: np.ndarray, m: np.ndarray, u: np.ndarray, cond_len: int,
     The component ablation (Section 5, Table 3; Appendix "Ablation Settings") uses the
     same aligned signal three ways: "retrace" corrects it (Eq.7-8) and adds it through
     the gate (Eq.9); "raw_gated" adds the raw aligned drafter state r_j = m_j through
-    the same gate; "overwrite" replaces the conditioned mask inputs with m_j."""
+    the same gate; "overwrite" replaces the conditioned mask inputs with m_j.
+
+    "lowrank" is the deployment form of the conditioning path named in the appendix on
+    concurrent serving (rank-64 rejected-suffix latents, input-side latent residual
+    fusion, rank-32 target-aware correction), read as: latent z_j = A m_j, correction
+    in latent space c_j = C_up C_down [m_j; u_j], rho_j = z_j + beta c_j, and
+    e~_j = e_j + (V rho_j) * sigmoid(W_g[:, :d] e_j + G rho_j), with
+    lowrank = (A, C_down, C_up, V, G).  It reduces to the full form when A = I,
+    W_c = C_up C_down, W_v = V and W_g[:, d:] = G."""
     e_t = e.copy()
+    d = e.shape[1]
     for j in range(1, cond_len + 1):
         if mode == "overwrite":
             e_t[j] = m[j]
+            continue
+        if mode == "lowrank":
+            A, c_down, c_up, V, G = lowrank
+            rho = A @ m[j] + beta * (c_up @ (c_down @ np.concatenate([m[j], u[j]])))
+            gate = sigmoid(w_g[:, :d] @ e[j] + G @ rho)
+            e_t[j] = e[j] + (V @ rho) * gate
             continue
         if mode == "raw_gated":
             rj = m[j]
@@ -146,8 +161,10 @@ class OracleRunner:
         e = m.block_inputs(st.anchor)
         if st.cond_len > 0 and self.wl.cond_mode != "off":
             mm, uu = align_rejected(st.hD_prev, st.hT_prev, st.r, self.B)
+            lr = (tuple(W[f"retrace.lr_{n}"] for n in ("a", "c_down", "c_up", "v", "g"))
+                  if self.wl.cond_mode == "lowrank" else None)
             e_t = condition_inputs(e, mm, uu, st.cond_len, W["retrace.w_c"], W["retrace.w_v"],
-                                   W["retrace.w_g"], self.wl.beta, self.wl.cond_mode)
+                                   W["retrace.w_g"], self.wl.beta, self.wl.cond_mode, lr)
         else:
             e_t = e.copy()
         e_t = m.prec.r(e_t)

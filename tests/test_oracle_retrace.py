@@ -175,9 +175,36 @@ def check_overwrite_replaces_rows(cond=condition_inputs):
     np.testing.assert_array_equal(out[6:], e[6:])
 
 
+def check_lowrank_reduces_to_full(cond=condition_inputs):
+    """With d equal to the latent rank (64), A = I, V = W_v, G = W_g[:, d:] and a rank-32
+    W_c = C_up C_down, the low-rank form is the full form of Eq.7-9 (parity of the
+    low-rank reading itself is unpinned against the paper, which describes it in one
+    sentence)."""
+    rng = np.random.default_rng(11)
+    d = 64
+    e, m, u = (rng.standard_normal((6, d)) for _ in range(3))
+    c_down, c_up = rng.standard_normal((32, 2 * d)) * 0.1, rng.standard_normal((d, 32)) * 0.1
+    wv, wg = rng.standard_normal((d, d)) * 0.1, rng.standard_normal((d, 2 * d)) * 0.1
+    for beta in (1.0, 0.5):
+        full = condition_inputs(e, m, u, 4, c_up @ c_down, wv, wg, beta)
+        low = cond(e, m, u, 4, None, None, wg, beta, "lowrank", (np.eye(d), c_down, c_up, wv, wg[:, d:]))
+        np.testing.assert_allclose(low, full, rtol=1e-12, atol=1e-14)
+    # beta = 0: rho = A m (no correction); V = 0: inputs unchanged
+    A, V, G = rng.standard_normal((64, d)), rng.standard_normal((d, 64)), rng.standard_normal((d, 64))
+    s = lambda x: 1 / (1 + np.exp(-x))
+    low = cond(e, m, u, 3, None, None, wg, 0.0, "lowrank", (A, c_down, c_up, V, G))
+    for j in range(1, 4):
+        rho = A @ m[j]
+        np.testing.assert_allclose(low[j], e[j] + (V @ rho) * s(wg[:, :d] @ e[j] + G @ rho), rtol=1e-12)
+    np.testing.assert_array_equal(low[4:], e[4:])
+    low = cond(e, m, u, 3, None, None, wg, 1.0, "lowrank", (A, c_down, c_up, np.zeros_like(V), G))
+    np.testing.assert_array_equal(low, e)
+
+
 def test_ablation_conditioning_closed_forms():
     check_raw_gated_ignores_correction()
     check_overwrite_replaces_rows()
+    check_lowrank_reduces_to_full()
     for mode in ("retrace", "raw_gated", "overwrite"):   # nothing conditioned: inputs unchanged
         rng = np.random.default_rng(7)
         e, m, u = _rows(rng), _rows(rng), _rows(rng)
@@ -222,6 +249,13 @@ def _cond_gate_on_r_only(e, m, u, n, wc, wv, wg, beta):
                                      np.concatenate([e[:1], e[1:n + 1] + m[1:n + 1], e[n + 1:]])}),
     (check_overwrite_replaces_rows, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode:
                                      np.concatenate([e[:1], m[:n], e[n + 1:]])}),
+    # low-rank form with the correction's factors swapped into the wrong order, or the
+    # gate reading the latent through V instead of G
+    (check_lowrank_reduces_to_full, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode, lr:
+                                     condition_inputs(e, m, u, n, wc, wv, wg, b, mode,
+                                                      (lr[0], lr[1], lr[2], lr[3], lr[3]))}),
+    (check_lowrank_reduces_to_full, {"cond": lambda e, m, u, n, wc, wv, wg, b, mode, lr:
+                                     condition_inputs(e, u, m, n, wc, wv, wg, b, mode, lr)}),
 ])
 def test_pins_catch_planted_mistakes(check, kw):
     with pytest.raises(AssertionError):
@@ -245,12 +279,14 @@ def mini():
 
 
 @pytest.mark.parametrize("which,mode", [("tiny", "retrace"), ("mini", "retrace"), ("mini", "raw_gated"),
-                                        ("mini", "overwrite"), ("mini", "off")])
+                                        ("mini", "overwrite"), ("mini", "lowrank"), ("mini", "off")])
 def test_lossless_against_target_greedy(which, mode, tiny, mini):
     """Whatever the drafter's conditioning, greedy verification commits exactly the
     target's own greedy continuation (Section 3, lossless acceptance)."""
     wl, W, prompt = tiny if which == "tiny" else mini
     wl = dataclasses.replace(wl, cond_mode=mode)
+    if mode == "lowrank":
+        W = make_weights(wl)          # adds the low-rank factors; the other tensors are unchanged
     R = OracleRunner(OracleModel(wl, W))
     gen, recs, _ = R.spec_decode(prompt, wl.new_tokens)
     assert len(gen) == wl.new_tokens
@@ -329,13 +365,15 @@ def test_wv_zero_run_is_plain_dflash(mini):
         R.round(st)
 
 
-@pytest.mark.parametrize("mode", ["overwrite", "raw_gated", "off"])
+@pytest.mark.parametrize("mode", ["overwrite", "raw_gated", "lowrank", "off"])
 def test_ablation_rounds_condition_the_drafter_input(mini, mode):
     """Within whole rounds: overwrite puts the previous round's aligned drafter states on
     the conditioned rows (Eq.5 alignment), raw gated and off leave the anchor and the
     unconditioned rows at their embeddings, and off leaves every row there."""
     wl, W, prompt = mini
     wl = dataclasses.replace(wl, cond_mode=mode)
+    if mode == "lowrank":
+        W = make_weights(wl)
     R = OracleRunner(OracleModel(wl, W))
     truth = R.ar_decode(prompt, 60)
     st = R.prefill(prompt, 50)

@@ -50,7 +50,7 @@ class Workload:
     rms_eps: float = 1.0e-6
     page_size: int = 16
     beta: float = 1.0
-    cond_mode: str = "retrace"      # "retrace" (corrected, gated), "raw_gated", "overwrite", "off"
+    cond_mode: str = "retrace"      # "retrace" (corrected, gated), "raw_gated", "overwrite", "lowrank", "off"
     temperature: float = 0.0        # 0: greedy; > 0: speculative sampling with top-k / top-p
     top_k: int = 20
     top_p: float = 0.95

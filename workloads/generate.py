@@ -38,6 +38,10 @@ def _layer_specs(prefix: str, s, d: int) -> List[Tuple[str, Tuple[int, ...], str
     ]
 
 
+LOWRANK_LATENT = 64   # rank of the rejected-suffix latents (appendix, concurrent serving)
+LOWRANK_CORR = 32     # rank of the target-aware correction
+
+
 def weight_specs(wl: Workload) -> List[Tuple[str, Tuple[int, ...], str]]:
     """Canonical tensor order: (name, shape [out, in], kind).  Linear weights are
     stored [out][in] row-major.  The drafter shares the target's embedding and LM
@@ -54,6 +58,12 @@ def weight_specs(wl: Workload) -> List[Tuple[str, Tuple[int, ...], str]]:
     specs += [("draft.final_norm", (d,), "norm")]
     specs += [("retrace.w_c", (d, 2 * d), "linear"), ("retrace.w_v", (d, d), "linear"),
               ("retrace.w_g", (d, 2 * d), "linear")]
+    if wl.cond_mode == "lowrank":   # the low-rank conditioning path's factors
+        specs += [("retrace.lr_a", (LOWRANK_LATENT, d), "linear"),
+                  ("retrace.lr_c_down", (LOWRANK_CORR, 2 * d), "linear"),
+                  ("retrace.lr_c_up", (LOWRANK_LATENT, LOWRANK_CORR), "linear"),
+                  ("retrace.lr_v", (d, LOWRANK_LATENT), "linear"),
+                  ("retrace.lr_g", (d, LOWRANK_LATENT), "linear")]
     return specs
 
 
