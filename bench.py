@@ -180,7 +180,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ar-steps", type=int, default=64, help="timed target-only greedy steps (0: skip)")
-    ap.add_argument("--cond-mode", choices=["retrace", "raw_gated", "overwrite", "off"], default="retrace",
+    ap.add_argument("--cond-mode", choices=["retrace", "raw_gated", "overwrite", "lowrank", "off"], default="retrace",
                     help="drafter conditioning: the method, a component-ablation variant, or none")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="0: greedy; > 0: speculative sampling with the workload's top-k / top-p (20 / 0.95)")

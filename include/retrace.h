@@ -49,9 +49,15 @@ enum { RT_F32 = 0, RT_BF16 = 1 };                   /* weight / activation stora
  *   RT_COND_RETRACE    corrected signal r = m + beta W_c [m; u] (Eq.7-8) fused through the
  *                      gated residual of Eq.9 (the method itself);
  *   RT_COND_RAW_GATED  the same gated residual on the uncorrected signal r = m;
- *   RT_COND_OVERWRITE  the conditioned mask rows are replaced by m_j itself.
+ *   RT_COND_OVERWRITE  the conditioned mask rows are replaced by m_j itself;
+ *   RT_COND_LOWRANK    the deployment form of the conditioning path (appendix on
+ *                      concurrent serving: rank-64 rejected-suffix latents, input-side
+ *                      latent residual fusion, rank-32 target-aware correction), read as
+ *                      rho = A m + beta C_up C_down [m; u] and
+ *                      e~ = e + (V rho) * sigmoid(W_g[:, :d] e + G rho); its five factors
+ *                      follow the other weights (see rt_init_models).
  * Every mode tracks r and cond_len the same way; OFF ignores them. */
-enum { RT_COND_OFF = 0, RT_COND_RETRACE = 1, RT_COND_RAW_GATED = 2, RT_COND_OVERWRITE = 3 };
+enum { RT_COND_OFF = 0, RT_COND_RETRACE = 1, RT_COND_RAW_GATED = 2, RT_COND_OVERWRITE = 3, RT_COND_LOWRANK = 4 };
 
 #define RT_MAX_COND_LAYERS 8
 
@@ -66,7 +72,7 @@ typedef struct rt_config {
   int32_t block_size;      /* rows per draft block, anchor included: B = block_size - 1 proposals */
   int32_t mask_token_id;   /* token whose embedding fills the B proposal rows */
   float beta;              /* correction strength of Eq.8 (1.0 at inference) */
-  int32_t cond_mode;       /* one of RT_COND_OFF / _RETRACE / _RAW_GATED / _OVERWRITE */
+  int32_t cond_mode;       /* one of RT_COND_OFF / _RETRACE / _RAW_GATED / _OVERWRITE / _LOWRANK */
   int32_t dtype;           /* RT_BF16 (fp16 retained states) or RT_F32 (fp32 everywhere) */
   int32_t max_batch;       /* sequences per batch */
   int32_t max_seq_len;     /* per sequence: prompt + generation budget + block_size */
@@ -98,7 +104,7 @@ typedef struct rt_model rt_model;   /* opaque handle */
 size_t rt_workspace_bytes(const rt_config* cfg);
 
 /* Number of weight tensors rt_init_models expects for cfg:
- * 1 + 11*n_layers + 4 + 11*draft_layers + 1 + 3. */
+ * 1 + 11*n_layers + 4 + 11*draft_layers + 1 + 3, plus 5 with RT_COND_LOWRANK. */
 int32_t rt_weight_count(const rt_config* cfg);
 
 /* Builds a model in `d_workspace` (device memory, >= rt_workspace_bytes, 256-byte
@@ -115,7 +121,9 @@ int32_t rt_weight_count(const rt_config* cfg);
  *   per drafter layer: the same eleven tensors as a target layer;
  *   drafter final_norm [d];
  *   W_c [d][2d] (Eq.7: first d inputs act on m, last d on u);
- *   W_v [d][d] (Eq.9); W_g [d][2d] (Eq.9: first d inputs act on e, last d on r).
+ *   W_v [d][d] (Eq.9); W_g [d][2d] (Eq.9: first d inputs act on e, last d on r);
+ *   with RT_COND_LOWRANK also A [64][d], C_down [32][2d], C_up [64][32], V [d][64],
+ *   G [d][64] (W_c and W_v are then unused; W_g's first d columns still act on e).
  * The weights are copied (re-laid out) into the workspace; the caller may free
  * them once the call returns.  The call synchronises the stream. */
 int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_weights,

@@ -20,9 +20,9 @@ LIB_PATH = os.path.join(HERE, "libretrace.so")
 RT_OK, RT_ERR_INVALID, RT_ERR_STATE, RT_ERR_CAPACITY, RT_ERR_WORKSPACE, RT_ERR_HIP, RT_ERR_TOKEN = \
     0, -1, -2, -3, -4, -5, -6
 RT_F32, RT_BF16 = 0, 1
-RT_COND_OFF, RT_COND_RETRACE, RT_COND_RAW_GATED, RT_COND_OVERWRITE = 0, 1, 2, 3
+RT_COND_OFF, RT_COND_RETRACE, RT_COND_RAW_GATED, RT_COND_OVERWRITE, RT_COND_LOWRANK = 0, 1, 2, 3, 4
 COND_MODES = {"off": RT_COND_OFF, "retrace": RT_COND_RETRACE, "raw_gated": RT_COND_RAW_GATED,
-              "overwrite": RT_COND_OVERWRITE}
+              "overwrite": RT_COND_OVERWRITE, "lowrank": RT_COND_LOWRANK}
 RT_MAX_COND_LAYERS = 8
 (RT_T_DRAFT_LOGITS, RT_T_VERIFY_LOGITS, RT_T_HD, RT_T_HT, RT_T_ETILDE, RT_T_DRAFT_TOKENS,
  RT_T_TARGET_TOKENS, RT_T_STATE, RT_T_G, RT_T_AR_LOGITS, RT_T_DRAFT_DIST_IDS, RT_T_DRAFT_DIST_P,

@@ -420,6 +420,16 @@ struct Engine : EngineBase {
     pack_weights<T>(W(b3 + 1), q.d, 2 * q.d, q.Kp_2d, at<T>(q.wc), stream);
     pack_weights<T>(W(b3 + 2), q.d, q.d, q.Kp_d, at<T>(q.wv), stream);
     pack_weights<T>(W(b3 + 3), q.d, 2 * q.d, q.Kp_2d, at<T>(q.wg), stream);
+    if (cfg.cond_mode == RT_COND_LOWRANK) {
+      // [A | 0] (A acts on m only) above C_down, as one packed [96][2d] matrix
+      pack_weights<T>(W(b3 + 4), kLowRankLatent, q.d, q.Kp_2d, at<T>(q.lr_down), stream);
+      pack_weights<T>(W(b3 + 5), kLowRankCorr, 2 * q.d, q.Kp_2d, at<T>(q.lr_down) + (size_t)kLowRankLatent * q.Kp_2d,
+                      stream);
+      HIPCHK(copy(q.lr_cup, b3 + 6, (size_t)kLowRankLatent * kLowRankCorr));
+      HIPCHK(copy(q.lr_v, b3 + 7, (size_t)q.d * kLowRankLatent));
+      HIPCHK(copy(q.lr_g, b3 + 8, (size_t)q.d * kLowRankLatent));
+      lowrank_gate_bias<T>(W(b3 + 3), at<T>(q.embed), q.d, cfg.mask_token_id, at<float>(q.lr_ge), stream);
+    }
     HIPCHK(hipGetLastError());
     // page table: page j of sequence s is pool page j * max_batch + s
     std::vector<int32_t> pt((size_t)q.n_pages);
@@ -524,6 +534,20 @@ struct Engine : EngineBase {
       e.rows_per_seq = q.bk;
       // r occupies packed k tiles d/32 .. 2d/32 of er
       CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.er) + (size_t)(q.d / 32) * 512, ldg2, R, true, at<T>(q.wv), q.d, q.Kp_d, R, e, q.d));
+    } else if (cfg.cond_mode == RT_COND_LOWRANK) {
+      prof_begin(RT_K_MISC, (double)R * q.d * (4 * q.ksz + sizeof(T) + 16), 0);
+      const int ldg2 = 16 * q.Kp_2d;
+      cond_prep<T, K>(at<T>(q.embed), q.d, st, cfg.mask_token_id, at<K>(q.hd_keep), at<K>(q.ht_keep), n_seqs, q.bk,
+                      at<float>(q.mu), at<float>(q.er), ldg2, 0, stream);
+      prof_end();
+      EpiArgs e{};
+      e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.lr_lat); e.ldo = kLowRankRows;
+      CHK(gemm_call(RT_K_GEMM_COND, at<float>(q.mu), ldg2, R, true, at<T>(q.lr_down), kLowRankRows, q.Kp_2d, R, e,
+                    2 * q.d));
+      prof_begin(RT_K_MISC, (double)R * q.d * (sizeof(T) + 8) + (double)q.d * kLowRankLatent * 2 * sizeof(T), 0);
+      lowrank_fuse<T>(at<float>(q.lr_lat), at<T>(q.lr_cup), at<T>(q.lr_v), at<T>(q.lr_g), at<float>(q.lr_ge), cfg.beta,
+                      at<T>(q.embed), q.d, st, cfg.mask_token_id, n_seqs, q.bk, x, at<float>(q.etilde), stream);
+      prof_end();
     } else {
       // plain block drafting, or the overwrite ablation (conditioned rows take m_j)
       const bool ow = cfg.cond_mode == RT_COND_OVERWRITE;

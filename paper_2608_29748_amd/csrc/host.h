@@ -27,6 +27,7 @@ constexpr int kArMaxSteps = RT_AR_MAX_STEPS;   // target-only greedy steps per r
 constexpr int kAttnRowsAr = 64;   // attention rows per block in target-only steps (the 64-row kernel)
 constexpr int kStateSlots = 16;   // int32 slots of per-sequence round state (fields in misc.h)
 constexpr int kTopkChunk = 8192;  // logits per first-stage top-k workgroup (sample.hip)
+constexpr int kLowRankRows = 96;  // low-rank conditioning: 64 latent + 32 correction rows
 
 struct Plan {
   // dimensions
@@ -56,6 +57,7 @@ struct Plan {
   size_t dist_ids_v, dist_p_v;   // sampling: target filtered distributions [R][RT_MAX_TOP_K]
   size_t stok;                   // sampling: first / target-only step tokens [bmax]
   size_t topk_cand;              // sampling: per-chunk top-k keys [R][chunks][RT_MAX_TOP_K]
+  size_t lr_down, lr_cup, lr_v, lr_g, lr_ge, lr_lat;   // low-rank conditioning (0 unless that mode)
   int rpart_rows;                // max(32, rows of a round)
   int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init

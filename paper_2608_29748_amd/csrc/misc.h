@@ -51,6 +51,18 @@ void embed_verify(const T* embed, int d, const int32_t* state, const uint64_t* d
 template <typename T, typename K>
 void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, const K* hD, const K* hT,
                int n_seqs, int bk, float* mu, float* er, int ldg, int raw, hipStream_t s);
+// Low-rank conditioning path: latent rank, correction rank, and the width of the latent
+// GEMM's output rows ([A m ; C_down [m; u]]).
+constexpr int kLowRankLatent = 64;
+constexpr int kLowRankCorr = 32;
+constexpr int kLowRankLat = kLowRankLatent + kLowRankCorr;
+// x / etilde rows from the latent GEMM output lat [rows][kLowRankLat] (see misc.hip).
+template <typename T>
+void lowrank_fuse(const float* lat, const T* cup, const T* V, const T* G, const float* ge, float beta, const T* embed,
+                  int d, const int32_t* state, int mask, int n_seqs, int bk, float* x, float* etilde, hipStream_t s);
+// ge = W_g[:, :d] E[mask] from the unpacked [d][2d] gate weight.
+template <typename T>
+void lowrank_gate_bias(const T* wg, const T* embed, int d, int mask, float* ge, hipStream_t s);
 void accept(int32_t* state, const int32_t* dtok, const uint64_t* tkeys, int32_t* ttok, int n_seqs,
             int bk, int32_t* out_tokens, int32_t* out_n, int32_t* out_a, hipStream_t s);
 // Target-only greedy step commit for n_seqs (<= 1024) sequences: tokens go to column

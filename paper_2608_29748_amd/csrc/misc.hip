@@ -218,6 +218,72 @@ void cond_prep(const T* embed, int d, const int32_t* state, int mask_token, cons
                      mask_token, hD, hT, bk, mu, er, ldg, raw);
 }
 
+// ------------------------------------------------------------------ low-rank conditioning
+// Rows (s, j), four per workgroup, 64 output columns per workgroup:
+//   rho = lat[:64] + beta * C_up lat[64:96]   (lat = [A m ; C_down [m; u]], fp32)
+//   x = e + (V rho) * sigmoid(ge + G rho) on conditioned rows 1..cond_len, else e,
+// with ge = W_g[:, :d] E[mask] precomputed (every conditioned row is a mask row).
+template <typename T>
+__global__ __launch_bounds__(256) void lowrank_fuse_kernel(const float* __restrict__ lat, const T* __restrict__ cup,
+                                                           const T* __restrict__ V, const T* __restrict__ G,
+                                                           const float* __restrict__ ge, float beta,
+                                                           const T* __restrict__ E, int d, const int32_t* st,
+                                                           int mask, int rows, int bk, float* x, float* et) {
+  __shared__ float rho[4][kLowRankLatent];
+  const int t = threadIdx.x, r = t >> 6, o = t & 63;
+  const int row = blockIdx.y * 4 + r;
+  const bool live = row < rows;
+  const int sq = live ? row / bk : 0, j = live ? row % bk : 0;
+  const bool cond = live && j >= 1 && j <= st[sq * kStateFields + ST_COND_LEN];
+  if (live) {
+    const float* lr = lat + (size_t)row * kLowRankLat;
+    float c = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < kLowRankCorr; ++k) c += Elem<T>::to_f32(cup[o * kLowRankCorr + k]) * lr[kLowRankLatent + k];
+    rho[r][o] = lr[o] + beta * c;
+  }
+  __syncthreads();
+  const int i = blockIdx.x * 64 + o;
+  if (!live || i >= d) return;
+  const int tok = j == 0 ? st[sq * kStateFields + ST_ANCHOR] : mask;
+  float v = Elem<T>::to_f32(E[(size_t)tok * d + i]);
+  if (cond) {
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < kLowRankLatent; ++k) {
+      s1 += Elem<T>::to_f32(V[(size_t)i * kLowRankLatent + k]) * rho[r][k];
+      s2 += Elem<T>::to_f32(G[(size_t)i * kLowRankLatent + k]) * rho[r][k];
+    }
+    v += s1 / (1.0f + expf(-(ge[i] + s2)));
+  }
+  x[(size_t)row * d + i] = v;
+  et[(size_t)row * d + i] = v;
+}
+template <typename T>
+void lowrank_fuse(const float* lat, const T* cup, const T* V, const T* G, const float* ge, float beta, const T* embed,
+                  int d, const int32_t* state, int mask, int n_seqs, int bk, float* x, float* etilde, hipStream_t s) {
+  const int rows = n_seqs * bk;
+  RT_LAUNCH((lowrank_fuse_kernel<T>), dim3((d + 63) / 64, (rows + 3) / 4), dim3(256), 0, s, lat, cup, V, G, ge, beta,
+            embed, d, state, mask, rows, bk, x, etilde);
+}
+
+// ge[i] = sum_k W_g[i][k] E[mask][k] over the first d columns of W_g (row-major [d][2d]).
+template <typename T>
+__global__ void lowrank_gate_bias_kernel(const T* __restrict__ wg, const T* __restrict__ E, int d, int mask,
+                                         float* ge) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= d) return;
+  const T* w = wg + (size_t)i * 2 * d;
+  const T* e = E + (size_t)mask * d;
+  float acc = 0.f;
+  for (int k = 0; k < d; ++k) acc += Elem<T>::to_f32(w[k]) * Elem<T>::to_f32(e[k]);
+  ge[i] = acc;
+}
+template <typename T>
+void lowrank_gate_bias(const T* wg, const T* embed, int d, int mask, float* ge, hipStream_t s) {
+  RT_LAUNCH((lowrank_gate_bias_kernel<T>), dim3((d + 255) / 256), dim3(256), 0, s, wg, embed, d, mask, ge);
+}
+
 // ------------------------------------------------------------------ acceptance / rollback
 // One wave per sequence.  Draft tokens y^_i (i = 1..B) sit in dtok[s][i]; the target's
 // token for block position i is the argmax of verify row i-1.
@@ -355,6 +421,12 @@ template void embed_verify<bf16_t>(const bf16_t*, int, const int32_t*, const uin
                                    int, float*, int, hipStream_t);
 template void embed_verify<float>(const float*, int, const int32_t*, const uint64_t*, int, int32_t*, int,
                                   int, float*, int, hipStream_t);
+template void lowrank_fuse<bf16_t>(const float*, const bf16_t*, const bf16_t*, const bf16_t*, const float*, float,
+                                   const bf16_t*, int, const int32_t*, int, int, int, float*, float*, hipStream_t);
+template void lowrank_fuse<float>(const float*, const float*, const float*, const float*, const float*, float,
+                                  const float*, int, const int32_t*, int, int, int, float*, float*, hipStream_t);
+template void lowrank_gate_bias<bf16_t>(const bf16_t*, const bf16_t*, int, int, float*, hipStream_t);
+template void lowrank_gate_bias<float>(const float*, const float*, int, int, float*, hipStream_t);
 template void cond_prep<bf16_t, uint16_t>(const bf16_t*, int, const int32_t*, int, const uint16_t*,
                                           const uint16_t*, int, int, float*, float*, int, int, hipStream_t);
 template void cond_prep<float, float>(const float*, int, const int32_t*, int, const float*, const float*, int,

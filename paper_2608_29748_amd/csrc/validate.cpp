@@ -55,8 +55,8 @@ int validate_config(const rt_config* c) {
   if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab) return fail(RT_ERR_TOKEN, "mask_token_id out of range");
   if (!isfinite(c->beta)) return fail(RT_ERR_INVALID, "beta must be finite");
   if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(RT_ERR_INVALID, "rope_theta / rms_eps invalid");
-  if (c->cond_mode < RT_COND_OFF || c->cond_mode > RT_COND_OVERWRITE)
-    return fail(RT_ERR_INVALID, "cond_mode must be RT_COND_OFF, _RETRACE, _RAW_GATED or _OVERWRITE");
+  if (c->cond_mode < RT_COND_OFF || c->cond_mode > RT_COND_LOWRANK)
+    return fail(RT_ERR_INVALID, "cond_mode must be RT_COND_OFF, _RETRACE, _RAW_GATED, _OVERWRITE or _LOWRANK");
   if (c->max_batch < 1 || c->max_batch > 1024) return fail(RT_ERR_INVALID, "max_batch must be in [1, 1024]");
   if (c->max_seq_len < c->block_size + 1 || c->max_seq_len > (1 << 20))
     return fail(RT_ERR_INVALID, "max_seq_len must be in [block_size + 1, 2^20]");
@@ -72,7 +72,9 @@ int validate_config(const rt_config* c) {
   return RT_OK;
 }
 
-int weight_count(const rt_config* c) { return 1 + 11 * c->n_layers + 4 + 11 * c->draft_layers + 1 + 3; }
+int weight_count(const rt_config* c) {
+  return 1 + 11 * c->n_layers + 4 + 11 * c->draft_layers + 1 + 3 + (c->cond_mode == RT_COND_LOWRANK ? 5 : 0);
+}
 
 int make_plan(const rt_config* c, Plan* p) {
   int st = validate_config(c);
@@ -128,6 +130,13 @@ int make_plan(const rt_config* c, Plan* p) {
   q.wc = take(packed(q.d, q.Kp_2d));
   q.wg = take(packed(q.d, q.Kp_2d));
   q.wv = take(packed(q.d, q.Kp_d));
+  if (c->cond_mode == RT_COND_LOWRANK) {
+    q.lr_down = take(packed(kLowRankRows, q.Kp_2d));        // [A | 0 ; C_down], packed
+    q.lr_cup = take((size_t)64 * 32 * e);
+    q.lr_v = take((size_t)q.d * 64 * e);
+    q.lr_g = take((size_t)q.d * 64 * e);
+    q.lr_ge = take((size_t)q.d * 4);
+  }
   // per-layer block
   size_t lo = 0;
   auto ltake = [&](size_t bytes) { size_t o = lo; lo = rup(lo + bytes, 256); return o; };
@@ -179,6 +188,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.mu = take(Rp * q.Kp_2d * 4);
   q.er = take(Rp * q.Kp_2d * 4);
   q.gate = take(Rp * q.d * 4);
+  q.lr_lat = take(Rp * kLowRankRows * 4);
   q.hd_keep = take((size_t)q.R * q.d * q.ksz);
   q.ht_keep = take((size_t)q.R * q.d * q.ksz);
   q.dlogits = take((size_t)q.R * q.V * 4);

@@ -49,6 +49,8 @@ def test_workspace_and_weight_count(B):
     c = cfg(B)
     assert B.rt_workspace_bytes(c) > 0
     assert B.rt_weight_count(c) == 1 + 11 * 2 + 4 + 11 * 1 + 1 + 3
+    assert B.rt_weight_count(cfg(B, cond_mode=B.RT_COND_LOWRANK)) == 1 + 11 * 2 + 4 + 11 * 1 + 1 + 3 + 5
+    assert B.rt_workspace_bytes(cfg(B, cond_mode=B.RT_COND_LOWRANK)) > B.rt_workspace_bytes(c)
     big = cfg(B, dtype=B.RT_BF16, max_batch=4)
     assert B.rt_workspace_bytes(big) > B.rt_workspace_bytes(cfg(B, dtype=B.RT_BF16))
 
@@ -66,7 +68,7 @@ def test_workspace_and_weight_count(B):
     (dict(cond_layer_ids=[1, 0]), "increase"),
     (dict(draft_layers=0), "draft_layers"),
     (dict(dtype=7), "dtype"),
-    (dict(cond_mode=4), "cond_mode"),
+    (dict(cond_mode=5), "cond_mode"),
     (dict(temperature=-1.0), "temperature"),
     (dict(temperature=1.0, top_k=0, top_p=0.9), "top_k"),
     (dict(temperature=1.0, top_k=65, top_p=0.9), "top_k"),

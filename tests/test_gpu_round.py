@@ -52,10 +52,13 @@ def test_prefill_and_rounds_match_oracle(name):
 
 @pytest.mark.parametrize("name,mode", [("tiny-f32", "raw_gated"), ("tiny-f32", "overwrite"),
                                        ("mini-bf16", "raw_gated"), ("mini-bf16", "overwrite"),
-                                       ("mini-bf16-ragged", "off"), ("mini-bf16-b4", "raw_gated")])
+                                       ("mini-bf16-ragged", "off"), ("mini-bf16-b4", "raw_gated"),
+                                       ("tiny-f32", "lowrank"), ("mini-bf16", "lowrank"),
+                                       ("mini-bf16-ragged", "lowrank"), ("mini-bf16-b4", "lowrank")])
 def test_ablation_conditioning_matches_oracle(name, mode):
-    """The component-ablation drafters of Table 3 (raw gated fusion, overwrite) and
-    plain block drafting, round by round against the oracle run in the same mode."""
+    """The component-ablation drafters of Table 3 (raw gated fusion, overwrite), the
+    low-rank deployment form of the conditioning path, and plain block drafting, round
+    by round against the oracle run in the same mode."""
     wl, W, prompts = _setup(name, norm_init="perturbed", cond_mode=mode)
     log(f"[{name} {mode}] prefill")
     eng = engine_for(wl, W)
