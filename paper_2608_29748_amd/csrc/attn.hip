@@ -424,23 +424,22 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       // rows that have seen no visible key yet (reference -inf) take p = 0
       const float mr = mref[t2];
       const bool all_live = __builtin_amdgcn_ballot_w64(mr == -INFINITY) == 0;
-      Frag<bf16_t> ph, pl;
+      // P in bf16 (its rounding stays below the bf16 rounding of the stored output); the
+      // row sum takes the same rounded weights, so O / sum is their exact weighted mean
+      Frag<bf16_t> ph;
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           float x = __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr));
           if (!all_live) x = mr == -INFINITY ? 0.f : x;
-          lsum[t2] += x;
           const short hb = bf16_bits(x);
           ph.v[tau * 4 + e] = hb;
-          pl.v[tau * 4 + e] = bf16_bits(x - bf16_value(hb));
+          lsum[t2] += bf16_value(hb);
         }
-      // O^T += V^T P^T (P split into bf16 hi + lo parts, ~16 significand bits)
+      // O^T += V^T P^T
 #pragma unroll
       for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], ph);
-#pragma unroll
-      for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], pl);
     }
   }
 #pragma unroll
