@@ -53,8 +53,16 @@ def build_engine(wl, W):
 
 DOMINANT = "gemm_gate_up"
 REPLAY_KINDS = (0, 1, 2, 3, 4, 5, 6, 7, 10)   # GEMM classes, attention, merge, LM head
-DOMINANT_DESC = ("gemm_gate_up: fused gate|up projection GEMM with SwiGLU epilogue "
-                 "(gemm16_kernel, bf16 MFMA, 16 rows x 19456 columns x K 2560 at the Qwen3-4B shape)")
+
+
+def dominant_desc(wl):
+    """The dominant kernel's launch class at this workload's verify shape."""
+    rows = wl.batch * wl.block_size
+    kern = "gemm16_kernel" if rows <= 64 else "gemm_mid_kernel"
+    return (f"gemm_gate_up: fused gate|up projection GEMM with SwiGLU epilogue ({kern}, bf16 MFMA, "
+            f"{rows} rows x {2 * wl.target.ffn} columns x K {wl.target.hidden})")
+
+
 GEMM_SOURCES = ("paper_2608_29748_amd/csrc/gemm.hip", "paper_2608_29748_amd/csrc/gemm.h",
                 "paper_2608_29748_amd/csrc/common.h")
 
@@ -289,7 +297,7 @@ def main():
                    "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
                    "cond_layers": list(wl.cond_layers), "cond_mode": wl.cond_mode, "temperature": wl.temperature,
                    "top_k": wl.top_k, "top_p": wl.top_p, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": DOMINANT_DESC,
+        "roofline": {"bound": "hbm", "kernel": dominant_desc(wl),
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",
                      "algorithmic_bytes_per_launch": per_launch_bytes, "us_per_launch": per_launch_us,
