@@ -306,9 +306,9 @@ struct Engine : EngineBase {
       prof_end();
       return RT_OK;
     }
-    const int parts = lmhead_grid(q.V);
     for (int r0 = 0; r0 < M; r0 += 32) {          // 32-row passes over the vocabulary
       const int m = M - r0 < 32 ? M - r0 : 32;
+      const int parts = lmhead_parts(m, q.V, q.Kp_d, (int)sizeof(T));
       LmHeadArgs h{};
       h.A = at<T>(q.xa) + (size_t)(r0 / 16) * 16 * q.Kp_d; h.lda = 16 * q.Kp_d; h.a_rows = q.Mrows - r0; h.M = m;
       h.B = at<T>(q.lm_head); h.N = q.V; h.Kp = q.Kp_d;
@@ -620,6 +620,7 @@ struct Engine : EngineBase {
     static_assert(kStateFields <= kStateSlots, "per-sequence state exceeds its slots");
     static_assert(kMaxTopK == RT_MAX_TOP_K, "distribution width");
     static_assert(kTopkChunk == kSelectChunk, "top-k stage size");
+    static_assert(kLmGrid <= kLmPartsMin, "LM-head key rows");
     static_assert(kAttnRowsAr == kAttnRows, "target-only steps use the 64-row attention blocks");
     const int M = n_seqs;
     int32_t* st = at<int32_t>(q.state);

@@ -89,6 +89,11 @@ struct LmHeadArgs {
   float* logits; int ldl;          // optional fp32 logits
 };
 int lmhead_grid(int N);
+constexpr int kLmGrid = 512;   // LDS-staged LM head: two workgroups per CU on 256 CUs (K <= 2560)
+// Partial-key rows (workgroups) of one lm_head launch over M rows, and an upper bound
+// over every launch for a vocabulary of N.
+int lmhead_parts(int M, int N, int Kp, int elem_bytes);
+int lmhead_max_parts(int N);
 
 // Host-side launch helpers (implemented in gemm.hip).
 template <typename T>

@@ -586,10 +586,93 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
   }
 }
 
+// LM head for at most 16 rows of bf16 activations with K <= 4096: the workgroup copies
+// the 16 x K activation block into LDS once (direct-to-LDS, 1 KiB per k tile) and its
+// eight waves then stream 16-column weight tiles over the vocabulary (grid stride),
+// taking A fragments from LDS.  The activations are read from L2 once per workgroup
+// instead of once per column tile, which leaves the L1 miss path to the weight stream.
+constexpr int kLmWaves = 8;
+
+static bool lm_lds_ok(int M, int Kp, int elem_bytes) { return elem_bytes == 2 && M <= 16 && Kp <= 4096; }
+
+template <int KTMAX, int U>
+__global__ __launch_bounds__(kLmWaves * 64) void lmhead_lds_kernel(LmHeadArgs a) {
+  static_assert(KTMAX * 1024 >= kLmWaves * 16 * 8, "the keys reuse the activation buffer");
+  __shared__ __attribute__((aligned(1024))) char sa[KTMAX * 1024];
+  const int lane = threadIdx.x & 63, g4 = lane / 16, c16 = lane % 16;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int KT = a.Kp / kTileK;
+  const int n_tiles = a.N / kTileN;
+  for (int t = w; t < KT; t += kLmWaves)
+    __builtin_amdgcn_global_load_lds((const void*)((const char*)a.A + (size_t)t * 1024 + lane * 16),
+                                     (lds_void_t*)(sa + t * 1024), 16, 0, 0);
+  wait_vm<0>();
+  lds_barrier();
+  uint64_t best[4] = {0ull, 0ull, 0ull, 0ull};
+  for (int t = blockIdx.x * kLmWaves + w; t < n_tiles; t += gridDim.x * kLmWaves) {
+    const bf16_t* bptr = (const bf16_t*)a.B + ((size_t)t * KT) * 512 + lane * 8;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < KT; kt += U) {
+      Frag<bf16_t> bf[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) bf[u].load(bptr + (size_t)(kt + u < KT ? kt + u : KT - 1) * 512);
+      __builtin_amdgcn_sched_barrier(0);   // all U weight tiles in flight before the MFMAs
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (kt + u < KT) {
+          Frag<bf16_t> af;
+          af.v = *reinterpret_cast<const bf16x8*>(sa + (kt + u) * 1024 + lane * 16);
+          mma(acc, af, bf[u]);
+        }
+    }
+    // lane (g4, c16) holds rows 4 g4 .. 4 g4 + 3 of column t * 16 + c16
+    const int n = t * kTileN + c16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * g4 + i;
+      if (a.logits && row < a.M) a.logits[(size_t)row * a.ldl + n] = acc[i];
+      const uint64_t kk = argmax_key(acc[i], (uint32_t)n);
+      best[i] = kk > best[i] ? kk : best[i];
+    }
+  }
+  __syncthreads();   // every wave is done with the activations: the keys take their place
+  uint64_t* wkeys = reinterpret_cast<uint64_t*>(sa);   // [kLmWaves][16]
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint64_t k = best[i];
+    for (int o = 8; o > 0; o >>= 1) {
+      const uint64_t other = __shfl_xor(k, o, 64);
+      k = other > k ? other : k;
+    }
+    if (c16 == 0) wkeys[w * 16 + 4 * g4 + i] = k;
+  }
+  __syncthreads();
+  if (threadIdx.x < 16 && (int)threadIdx.x < a.M) {
+    uint64_t k = wkeys[threadIdx.x];
+#pragma unroll
+    for (int v = 1; v < kLmWaves; ++v) k = wkeys[v * 16 + threadIdx.x] > k ? wkeys[v * 16 + threadIdx.x] : k;
+    a.part_keys[(size_t)blockIdx.x * a.M + threadIdx.x] = k;
+  }
+}
+
+int lmhead_parts(int M, int N, int Kp, int elem_bytes) {
+  if (!lm_lds_ok(M, Kp, elem_bytes)) return lmhead_grid(N);
+  const int grid = Kp / kTileK <= 80 ? kLmGrid : kLmGrid / 2;   // 80 KiB: two per CU; 128 KiB: one
+  const int need = (N / kTileN + kLmWaves - 1) / kLmWaves;
+  return grid < need ? grid : need;
+}
+int lmhead_max_parts(int N) { return lmhead_grid(N) > kLmGrid ? lmhead_grid(N) : kLmGrid; }
+
 template <typename T>
 hipError_t lm_head(const LmHeadArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.M > 32) return hipErrorInvalidValue;
+  if (lm_lds_ok(a.M, a.Kp, (int)sizeof(T))) {
+    const dim3 grid(lmhead_parts(a.M, a.N, a.Kp, (int)sizeof(T)));
+    if (a.Kp / kTileK <= 80) RT_LAUNCH((lmhead_lds_kernel<80, 8>), grid, dim3(kLmWaves * 64), 0, s, a);
+    else RT_LAUNCH((lmhead_lds_kernel<128, 8>), grid, dim3(kLmWaves * 64), 0, s, a);
+    return hipGetLastError();
+  }
   dim3 grid(lmhead_grid(a.N));
   if (a.M > 16) RT_LAUNCH((lmhead_kernel<T, 2, 8>), grid, dim3(256), 0, s, a);
   else RT_LAUNCH((lmhead_kernel<T, 1, 8>), grid, dim3(256), 0, s, a);

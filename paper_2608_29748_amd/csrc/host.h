@@ -27,6 +27,7 @@ constexpr int kArMaxSteps = RT_AR_MAX_STEPS;   // target-only greedy steps per r
 constexpr int kAttnRowsAr = 64;   // attention rows per block in target-only steps (the 64-row kernel)
 constexpr int kStateSlots = 16;   // int32 slots of per-sequence round state (fields in misc.h)
 constexpr int kTopkChunk = 8192;  // logits per first-stage top-k workgroup (sample.hip)
+constexpr int kLmPartsMin = 512;  // LM-head key rows always reserved (LDS-staged LM head grid, gemm.hip)
 constexpr int kLowRankRows = 96;  // low-rank conditioning: 64 latent + 32 correction rows
 
 struct Plan {

@@ -200,6 +200,7 @@ int make_plan(const rt_config* c, Plan* p) {
     q.qkvf = take(M * qc * 4);
     q.lm_parts = (q.V + 31) / 32 / 8 + 1;                 // skinny LM head workgroups
     if (2 * ((q.V + 63) / 64) > q.lm_parts) q.lm_parts = 2 * ((q.V + 63) / 64);   // mid-size: 2 per workgroup
+    if (q.lm_parts < kLmPartsMin) q.lm_parts = kLmPartsMin;   // LDS-staged skinny LM head
     q.part_keys = take((size_t)q.lm_parts * M * 8);
   }
   q.dtok = take((size_t)q.R * 4);
