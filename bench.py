@@ -192,12 +192,16 @@ def main():
                     help="drafter conditioning: the method, a component-ablation variant, or none")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="0: greedy; > 0: speculative sampling with the workload's top-k / top-p (20 / 0.95)")
+    ap.add_argument("--prompt-len", type=int, default=None,
+                    help="override every prompt's length (short prefills for counter runs; verify GEMM shapes "
+                         "do not depend on it, attention does)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB copies (reference reading for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
-              "(the round shards by sequence with no exchange; see the design notes)", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (a round's state is "
+              "per sequence, so batches shard by sequence across GPUs with no exchange during a round)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -206,6 +210,8 @@ def main():
     over = {"cond_mode": args.cond_mode, "temperature": args.temperature}
     if args.batch is not None:
         over["batch"] = args.batch
+    if args.prompt_len is not None:
+        over["prompt_len"] = (args.prompt_len, args.prompt_len)
     wl = get(args.workload, **over)
     need = args.warmup + args.steps + args.profile_rounds + 2
     if need > wl.new_tokens - 1:
