@@ -31,7 +31,8 @@ def _exact(wl, W, R):
     return RX
 
 
-@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5", "mini-bf16-b4"])
+@pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5", "mini-bf16-b4",
+                                  "mini-bf16-w4096"])
 def test_prefill_and_rounds_match_oracle(name):
     wl, W, prompts = _setup(name, norm_init="perturbed")
     log(f"[{name}] engine init")

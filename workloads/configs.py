@@ -136,6 +136,14 @@ PRESETS = {
                           head_dim=128, ffn=2048),
         draft_layers=1, cond_layers=(0, 1), block_size=16, batch=4, prompt_len=(30, 90),
         new_tokens=40, seed=10),
+    # Width 4096 at batch 1 (as the Qwen3-8B shape): the LM head stages 128 KiB of
+    # activations per workgroup; q and kv widths below the model width
+    "mini-bf16-w4096": Workload(
+        name="mini-bf16-w4096", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=4096, n_layers=2, n_q_heads=4, n_kv_heads=2,
+                          head_dim=128, ffn=512),
+        draft_layers=1, cond_layers=(0, 1), block_size=16, batch=1, prompt_len=(40, 40),
+        new_tokens=40, seed=11),
     # GQA group of 5 (80 query rows per 16-token block, as at the Qwen3-14B shape), hd 128
     "mini-bf16-gqa5": Workload(
         name="mini-bf16-gqa5", dtype="bf16",
