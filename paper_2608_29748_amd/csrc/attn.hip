@@ -241,25 +241,28 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
 typedef __attribute__((address_space(4))) const int32_t const_i32_t;
 
 __device__ __forceinline__ short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
-__device__ __forceinline__ float bf16_value(short b) { return __uint_as_float(((uint32_t)(uint16_t)b) << 16); }
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // XOR swizzle of the 16-byte pieces of a K row in LDS (row r of chunk page pg), so that
 // the 16 lanes reading one fragment column hit distinct banks.
 template <int NPR>
 __device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)) & (NPR - 1); }
 
-// Work split of a workgroup: wave w owns query rows rh*16*NRT .. +16*NRT-1 of the row
-// block (rh = w/2, NRT 16-row MFMA tiles) and keys kh*32..kh*32+31 of every 64-key chunk
-// (kh = w%2, two pages); the two key halves of the same rows are merged through LDS at
-// the end.  Every K / V byte staged in LDS is read by two waves.
+// Work split of a workgroup of NW waves: wave w owns query rows rh*16*NRT .. +16*NRT-1
+// of the row block (rh = w/2, NRT 16-row MFMA tiles) and keys kh*32..kh*32+31 of every
+// 64-key chunk (kh = w%2, two pages); the two key halves of the same rows are merged
+// through LDS at the end.  Every K / V byte staged in LDS is read by NW/2 waves.  The
+// 96-row blocks use one query tile per wave (12 waves): three waves per SIMD then
+// interleave their dependent chains (LDS reads, score MFMAs, online softmax, PV MFMAs),
+// which four waves holding three tiles each cannot.
 //
 // Key order inside a wave's 32 keys: score tile tau (0, 1), A-operand row m holds key
 // (m/4)*8 + 4*tau + m%4, so that the accumulator lane (g, q) ends up with the eight
 // consecutive keys 8g..8g+7 (tau = 0: 8g..8g+3, tau = 1: 8g+4..8g+7).  Those eight
 // probabilities are exactly the lane's B operand of O^T += V^T P^T, and its V^T operand
 // is one contiguous 16-byte piece of a V page row.
-template <int HD, int NSTAGE, int NRT>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+template <int HD, int NSTAGE, int NRT, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int ROWB = HD * 2;                 // bytes of one K row (one token)
   constexpr int NPR = ROWB / 16;               // 16-byte pieces per K row
   constexpr int PGB = kPage * ROWB;            // bytes of one (page, KV head) slice of K or V
@@ -269,10 +272,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int NHT = HD / 16, NKS = HD / 32;
   constexpr int OPITCH = HD + 4;               // fp32 row pitch of the key-half merge buffer
   constexpr int RH = 16 * NRT;                 // rows per wave
-  constexpr int RBR = 2 * RH;                  // rows per workgroup (row block)
-  constexpr int MERGE = 2 * RH * OPITCH * 4 + 2 * RH * 2 * 4;
+  constexpr int RBR = NW / 2 * RH;             // rows per workgroup (row block)
+  constexpr int MERGE = RBR * OPITCH * 4 + RBR * 2 * 4;
+  // copies per chunk: with four waves each copies one K and one V page; with eight or
+  // more, waves 0-3 copy the K pages and waves 4-7 the V pages (the rest copy nothing)
+  constexpr bool SPREAD = NW >= 8;
+  constexpr int LPC = SPREAD ? NLD : 2 * NLD;  // copies per chunk of a copying wave
+  static_assert(NW % 2 == 0 && (NW == 4 || NW >= 8), "wave pairs; 4 or at least 8 waves");
   constexpr int SMEM = NSTAGE * STG > MERGE ? NSTAGE * STG : MERGE;
-  static_assert(PAGES == 4, "one page per wave");
+  static_assert(PAGES == 4, "four 16-token pages per 64-key chunk");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int lane = threadIdx.x & 63, g4 = lane >> 4, c16 = lane & 15;
@@ -295,7 +303,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const_i32_t* pt = (const_i32_t*)(a.page_table + (size_t)s * a.max_pages);
   // page w of chunk c (pages past kv_end are replaced by the last valid one, so every
   // wave issues the same number of copies per chunk; their keys are masked)
-  auto page_of = [&](int c) { return pt[min(c * PAGES + w, last_page)]; };
+  const int cw = w & (PAGES - 1);               // page of the chunk this wave copies
+  const bool copies_k = SPREAD ? w < PAGES : true, copies_v = SPREAD ? (w >= PAGES && w < 2 * PAGES) : true;
+  auto page_of = [&](int c) { return pt[min(c * PAGES + cw, last_page)]; };
 
   // per-lane source offsets of the copies (LDS slot j*64+lane of this wave's slice)
   int koff[NLD], voff[NLD];
@@ -303,21 +313,25 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   for (int j = 0; j < NLD; ++j) {
     const int sl = j * 64 + lane;
     const int r = sl / NPR, p = sl % NPR;
-    koff[j] = r * ROWB + (p ^ kswz<NPR>(r, w)) * 16;
+    koff[j] = r * ROWB + (p ^ kswz<NPR>(r, cw)) * 16;
     const int h = sl >> 1, vp = sl & 1;
     voff[j] = h * 32 + (vp ^ ((h >> 3) & 1)) * 16;
   }
   auto issue = [&](int pg, int stg) {
     const char* kb = (const char*)a.kcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
     const char* vb = (const char*)a.vcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
-    char* lk = smem + stg * STG + w * PGB;
-    char* lv = smem + stg * STG + PAGES * PGB + w * PGB;
+    char* lk = smem + stg * STG + cw * PGB;
+    char* lv = smem + stg * STG + PAGES * PGB + cw * PGB;
+    if (copies_k) {
 #pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
+      for (int j = 0; j < NLD; ++j)
+        __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
+    }
+    if (copies_v) {
 #pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
+      for (int j = 0; j < NLD; ++j)
+        __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
+    }
   };
 
   // this wave's queries: tile t2 (0..NRT-1) column c16 is row row0 + rh*RH + t2*16 + c16
@@ -335,11 +349,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].load(qp + ks * 32 + g4 * 8);
   }
   const float sl2 = a.scale * 1.4426950408889634f;
-  float mref[NRT], lsum[NRT];   // reference max (log2 units), raised lazily; this lane's share of the sum
+  // reference max (log2 units), raised lazily.  It starts at a finite sentinel: a masked
+  // score (-inf) then still gives exp2(-inf) = 0, and the first visible score of a row
+  // raises the reference before any exponential of it is taken.
+  constexpr float kMrefInit = -1.0e30f;
+  float mref[NRT], lsum[NRT];   // lsum: this lane's share of the row sum
   f32x4 o[NRT][NHT];
 #pragma unroll
   for (int t2 = 0; t2 < NRT; ++t2) {
-    mref[t2] = -INFINITY;
+    mref[t2] = kMrefInit;
     lsum[t2] = 0.f;
   }
 #pragma unroll
@@ -357,7 +375,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     const int i = c - c_beg;
     // this wave's copies of chunk c have landed once at most the later chunks' remain
     if constexpr (NSTAGE >= 3) {
-      if (c + 1 < c_end) wait_vm<2 * NLD>(); else wait_vm<0>();
+      if (c + 1 < c_end) wait_vm<LPC>(); else wait_vm<0>();
     } else {
       wait_vm<0>();
     }
@@ -413,7 +431,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       // stay below 256; the final ratio is unchanged); rescale O and the sum then
       if (__builtin_amdgcn_ballot_w64(mxs > mref[t2] + 8.f)) {
         const float mnew = fmaxf(mref[t2], mxs);
-        const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mref[t2] - mnew);
+        const float alpha = __builtin_amdgcn_exp2f(mref[t2] - mnew);   // 0 when leaving the sentinel
 #pragma unroll
         for (int t = 0; t < NHT; ++t)
 #pragma unroll
@@ -421,22 +439,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         lsum[t2] *= alpha;
         mref[t2] = mnew;
       }
-      // rows that have seen no visible key yet (reference -inf) take p = 0
       const float mr = mref[t2];
-      const bool all_live = __builtin_amdgcn_ballot_w64(mr == -INFINITY) == 0;
       // P in bf16 (its rounding stays below the bf16 rounding of the stored output); the
       // row sum takes the same rounded weights, so O / sum is their exact weighted mean
       Frag<bf16_t> ph;
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float x = __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr));
-          if (!all_live) x = mr == -INFINITY ? 0.f : x;
-          const short hb = bf16_bits(x);
-          ph.v[tau * 4 + e] = hb;
-          lsum[t2] += bf16_value(hb);
-        }
+        for (int e = 0; e < 4; ++e) ph.v[tau * 4 + e] = bf16_bits(__builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr)));
+      // the row sum adds the rounded values in order, read from the packed pairs
+      const u32x4 pw = __builtin_bit_cast(u32x4, ph.v);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        lsum[t2] += __uint_as_float(pw[q] << 16);
+        lsum[t2] += __uint_as_float(pw[q] & 0xffff0000u);
+      }
       // O^T += V^T P^T
 #pragma unroll
       for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], ph);
@@ -449,7 +466,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   // once every wave has passed this barrier)
   lds_barrier();
   float* mo = reinterpret_cast<float*>(smem) + rh * RH * OPITCH;             // [RH][OPITCH] O^T rows
-  float* mml = reinterpret_cast<float*>(smem) + 2 * RH * OPITCH + rh * RH * 2;  // [RH][2] (m, l)
+  float* mml = reinterpret_cast<float*>(smem) + RBR * OPITCH + rh * RH * 2;    // [RH][2] (m, l)
   if (kh == 1) {
 #pragma unroll
     for (int t2 = 0; t2 < NRT; ++t2) {
@@ -571,19 +588,21 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane + 64 * e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
-constexpr int kStages = 2;   // direct-to-LDS pipeline depth (64 KB of LDS per workgroup at hd 128)
-
+// 64-row blocks: 4 waves of two query tiles, two LDS stages (64 KB at hd 128); 96-row
+// blocks: 12 waves of one tile, three stages (96 KB), 15% faster than 4 waves of three
+// tiles at the 14B verify shape (one tile per wave gains ~2% for 64-row blocks, and its
+// different fp32 rounding order changes a few outputs by one bf16 unit)
 template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.splits, a.n_kv_heads, a.n_seqs * a.row_blocks);
   if constexpr (sizeof(T) == 2) {
     if (a.rb_rows == 96) {
-      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages, 3>), grid, dim3(256), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages, 3>), grid, dim3(256), 0, s, a);
+      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 12>), grid, dim3(768), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12>), grid, dim3(768), 0, s, a);
       else return hipErrorInvalidValue;
     } else if (a.rb_rows == 64) {
-      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, kStages, 2>), grid, dim3(256), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, kStages, 2>), grid, dim3(256), 0, s, a);
+      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 2, 4>), grid, dim3(256), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 2, 4>), grid, dim3(256), 0, s, a);
       else return hipErrorInvalidValue;
     } else {
       return hipErrorInvalidValue;
