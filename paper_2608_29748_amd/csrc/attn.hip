@@ -252,9 +252,8 @@ __device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)
 // of the row block (rh = w/2, NRT 16-row MFMA tiles) and keys kh*32..kh*32+31 of every
 // 64-key chunk (kh = w%2, two pages); the two key halves of the same rows are merged
 // through LDS at the end.  Every K / V byte staged in LDS is read by NW/2 waves.  The
-// 96-row blocks use one query tile per wave (12 waves): three waves per SIMD then
-// interleave their dependent chains (LDS reads, score MFMAs, online softmax, PV MFMAs),
-// which four waves holding three tiles each cannot.
+// launches use one query tile per wave (8 or 12 waves): two or three waves per SIMD then
+// interleave their dependent chains (LDS reads, score MFMAs, online softmax, PV MFMAs).
 //
 // Key order inside a wave's 32 keys: score tile tau (0, 1), A-operand row m holds key
 // (m/4)*8 + 4*tau + m%4, so that the accumulator lane (g, q) ends up with the eight
@@ -488,14 +487,15 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     const float M = fmaxf(m0, m1);
     const float f0 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
     const float f1 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-    const float L = f0 * lsum[t2] + f1 * l1;
+    // explicit fused forms: every wave layout rounds the merge identically
+    const float L = fmaf(f0, lsum[t2], f1 * l1);
 #pragma unroll
     for (int t = 0; t < NHT; ++t) {
       const float4 v1 = *reinterpret_cast<const float4*>(mo + rl * OPITCH + t * 16 + 4 * g4);
-      o[t2][t][0] = f0 * o[t2][t][0] + f1 * v1.x;
-      o[t2][t][1] = f0 * o[t2][t][1] + f1 * v1.y;
-      o[t2][t][2] = f0 * o[t2][t][2] + f1 * v1.z;
-      o[t2][t][3] = f0 * o[t2][t][3] + f1 * v1.w;
+      o[t2][t][0] = fmaf(f1, v1.x, f0 * o[t2][t][0]);
+      o[t2][t][1] = fmaf(f1, v1.y, f0 * o[t2][t][1]);
+      o[t2][t][2] = fmaf(f1, v1.z, f0 * o[t2][t][2]);
+      o[t2][t][3] = fmaf(f1, v1.w, f0 * o[t2][t][3]);
     }
     const int qrow = row0 + rh * RH + rl;
     if (a.splits == 1) {
@@ -588,10 +588,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane + 64 * e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
-// 64-row blocks: 4 waves of two query tiles, two LDS stages (64 KB at hd 128); 96-row
-// blocks: 12 waves of one tile, three stages (96 KB), 15% faster than 4 waves of three
-// tiles at the 14B verify shape (one tile per wave gains ~2% for 64-row blocks, and its
-// different fp32 rounding order changes a few outputs by one bf16 unit)
+// One query tile per wave: 64-row blocks 8 waves, two LDS stages (64 KB at hd 128);
+// 96-row blocks 12 waves, three stages (96 KB; 15% faster than 4 waves of three tiles
+// at the 14B verify shape).  Results do not depend on the wave layout (the key-half
+// merge is written in explicit fused form).
 template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.splits, a.n_kv_heads, a.n_seqs * a.row_blocks);
@@ -601,8 +601,8 @@ hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
       else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12>), grid, dim3(768), 0, s, a);
       else return hipErrorInvalidValue;
     } else if (a.rb_rows == 64) {
-      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 2, 4>), grid, dim3(256), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 2, 4>), grid, dim3(256), 0, s, a);
+      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8>), grid, dim3(512), 0, s, a);
       else return hipErrorInvalidValue;
     } else {
       return hipErrorInvalidValue;
