@@ -152,7 +152,7 @@ struct Engine : EngineBase {
   }
 
   int gemm_call(int kind, const void* A, int lda, int a_rows, bool af32, const void* B, int N, int Kp, int M,
-                EpiArgs e, int k_logical = 0) {
+                EpiArgs e, int k_logical = 0, int partial_slabs = kResidSplits) {
     if (M <= 0) return RT_OK;
     if (k_logical <= 0) k_logical = Kp;
     e.M = M;
@@ -179,7 +179,7 @@ struct Engine : EngineBase {
       while (ks > 1 && (size_t)tiles * ks * 128 * 128 > kPartialFloats) --ks;
       if (tiles > kMaxTiles) ks = 1;
     }
-    if (e.kind == EPI_PARTIAL) ks = kResidSplits;
+    if (e.kind == EPI_PARTIAL) ks = partial_slabs;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
     a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.partial_floats = kPartialFloats;
@@ -192,6 +192,16 @@ struct Engine : EngineBase {
     HIPCHK(gemm<T>(a, shape, af32, stream));
     prof_end();
     return RT_OK;
+  }
+
+  // k slabs of the q|k|v projection of M rows when it runs on the mid-size kernel
+  // (bf16, 65..512 rows; the test hook keeps the wide path), else 1
+  int qkv_slabs(int M) const {
+    if (sizeof(T) != 2 || (flags & 4) || M <= 64 || M > 512) return 1;
+    GemmArgs g{};
+    g.Kp = p.Kp_d; g.partial_floats = kPartialFloats;
+    g.e.kind = EPI_STORE_F32; g.e.M = M; g.e.N = p.qkvN;
+    return gemm_mid_store_slabs(g, false);
   }
 
   struct LayerCtx {
@@ -241,11 +251,19 @@ struct Engine : EngineBase {
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
     norm_x((const T*)(lw + q.lo_in), c.M, nullptr, 0);
+    // q|k|v on the mid-size kernel with k slabs: the slabs go to the split buffer and
+    // qkv_post adds them (in slab order, as the slab epilogue would) while reading
+    const int qks = qkv_slabs(c.M);
     EpiArgs e{};
-    e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
-    CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d));
+    if (qks > 1) {
+      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.partial); e.ldo = q.qkvN; e.part_stride = (size_t)c.M * q.qkvN;
+    } else {
+      e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
+    }
+    CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d, qks));
     QkvPostArgs qp{};
-    qp.src = at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
+    qp.src = qks > 1 ? at<float>(q.partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
+    qp.n_part = qks; qp.part_stride = (size_t)c.M * q.qkvN;
     qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
     qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv; qp.q_out = at<T>(q.qbuf); qp.ldq = q.qN;
     qp.q_norm = lw + q.lo_qn; qp.k_norm = lw + q.lo_kn; qp.norm_layer_stride = 0;
@@ -253,7 +271,7 @@ struct Engine : EngineBase {
     qp.page_table = c.pt; qp.max_pages = q.pages_per_seq;
     qp.rope = at<float>(q.rope); qp.rope_max_pos = q.T; qp.eps = cfg.rms_eps;
     qp.rows_per_seq = c.rows_per_seq; qp.seq_stride = c.stride; qp.pos0 = c.pos0; qp.nrows = nullptr;
-    prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 + sizeof(T)), 0);
+    prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 * qks + sizeof(T)), 0);
     HIPCHK(qkv_post<T>(qp, stream));
     prof_end();
     AttnArgs a{};

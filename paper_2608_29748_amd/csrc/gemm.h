@@ -77,6 +77,7 @@ struct QkvPostArgs {
   float eps;
   int rows_per_seq, seq_stride;
   const int32_t* pos0; const int32_t* nrows;
+  int n_part; size_t part_stride;   // n_part > 1: src holds k-slab partials, summed in slab order
 };
 
 // LM head with a fused argmax: logits = X * W^T over the vocabulary; each workgroup
@@ -111,6 +112,10 @@ template <typename T>
 hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s);
 bool gemm_mid_supports(const GemmArgs& a);
 hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s);
+// k slabs the mid-size kernel would use for a GEMM with a stored (non-partial)
+// epilogue of this shape (1: none); a caller that adds the slabs itself requests them
+// with EPI_PARTIAL and this count
+int gemm_mid_store_slabs(const GemmArgs& a, bool a_f32);
 int gemm_mid_cols(int N);
 // Sums ks fp32 slabs part[z][M][N] (row-major, slab stride M*N) in slab order and runs
 // epilogue e on the result.

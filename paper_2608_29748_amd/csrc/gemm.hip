@@ -430,7 +430,18 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(QkvPostArgs a) {
   const int head = region == 0 ? hin : (region == 1 ? hin - qh : hin - qh - kvh);
   if (lane >= half) return;
   const float* src = a.src + (size_t)m * a.lds + (size_t)layer * a.layer_cols + (size_t)hin * hd;
-  float x0 = src[lane], x1 = src[lane + half];
+  float x0, x1;
+  if (a.n_part > 1) {   // k-slab partials, added in slab order
+    x0 = 0.f;
+    x1 = 0.f;
+    for (int z = 0; z < a.n_part; ++z) {
+      x0 += src[(size_t)z * a.part_stride + lane];
+      x1 += src[(size_t)z * a.part_stride + lane + half];
+    }
+  } else {
+    x0 = src[lane];
+    x1 = src[lane + half];
+  }
   if (region < 2) {
     float ss = x0 * x0 + x1 * x1;
     for (int o = half / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);

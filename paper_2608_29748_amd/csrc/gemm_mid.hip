@@ -269,6 +269,13 @@ static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
   return best;
 }
 
+int gemm_mid_store_slabs(const GemmArgs& a, bool a_f32) {
+  GemmArgs g = a;
+  if (g.e.kind == EPI_PARTIAL) g.e.kind = EPI_STORE_F32;
+  if (g.e.M <= 32 || g.e.M > 512) return 1;
+  return mid_plan(g, g.e.M <= 128 ? 128 : 256, a_f32).ks;
+}
+
 hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s) {
   if (!gemm_mid_supports(a)) return hipErrorInvalidValue;
   const int M = a.e.M, N = a.e.N;
