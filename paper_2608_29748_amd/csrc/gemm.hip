@@ -376,7 +376,8 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
     }
     // tile width, waves and loads in flight per shape class (measured on the Qwen3 layer
     // shapes): split reductions 16 columns x 4 waves per slab; N >= 16384 (gate|up) 16
-    // columns; N >= 5120 32 columns; otherwise 16 columns with 8 loads in flight
+    // columns (2 waves x 8 loads at 16 rows); N >= 5120 32 columns; otherwise 16 columns
+    // with 8 loads in flight
     if ((a.e.kind == EPI_PARTIAL) != (a.ksplit > 1) || a.ksplit < 1) return hipErrorInvalidValue;
     dim3 grid((N + 15) / 16, 1, a.ksplit);
     if (a_f32) {
@@ -386,8 +387,10 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
       else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 4, 4>), grid, dim3(256), 0, s, a);
     } else if (N >= 16384) {
+      // 16 rows: two waves of 8 loads in flight, so that all 1216 workgroups of the
+      // Qwen3-4B gate|up are resident at once (5% faster than eight waves of four)
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 4>), grid, dim3(512), 0, s, a);
-      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 8, 4>), grid, dim3(512), 0, s, a);
+      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 2, 8>), grid, dim3(128), 0, s, a);
     } else if (N >= 5120) {
       dim3 g2((N + 31) / 32, 1, 1);
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 2, 8, 4>), g2, dim3(512), 0, s, a);
