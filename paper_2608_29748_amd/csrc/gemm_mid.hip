@@ -225,12 +225,13 @@ static bool mid_direct_kind(int k) {
 
 template <bool AF32>
 static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t s) {
-  // 128-row tiles: 4 waves (2 x 2); 256-row tiles: 8 waves (4 x 2), two per SIMD, 8-13%
-  // faster at the 14B layer shapes than 4 waves (the output tile is split spatially, so
-  // every element is accumulated over k in the same order either way)
+  // 8 waves (4 x 2, two per SIMD) for 256-row tiles and 128 x 128 tiles: 8-13% faster at
+  // the 14B layer shapes and 3-6% at the 8B gate|up and q|k|v than 4 waves (2 x 2); the
+  // narrower and wider 128-row tiles stay at 4 waves.  The output tile is split
+  // spatially, so every element is accumulated over k in the same order either way.
   if (MB == 128) {
     if (NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4, AF32, 4>), grid, dim3(256), 0, s, a);
-    else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32, 4>), grid, dim3(256), 0, s, a);
+    else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32, 8>), grid, dim3(512), 0, s, a);
     else if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<128, 192, 4, false, 4>), grid, dim3(256), 0, s, a);
   } else {
     if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32, 8>), grid, dim3(512), 0, s, a);
