@@ -314,7 +314,7 @@ struct Engine : EngineBase {
       g.A = at<T>(q.xa); g.lda = 16 * q.Kp_d; g.a_rows = q.Mrows; g.B = at<T>(q.lm_head); g.Kp = q.Kp_d; g.ksplit = 1;
       g.e.kind = EPI_ARGMAX; g.e.M = M; g.e.N = q.V; g.e.out_f32 = logits; g.e.ldo = q.V;
       g.e.part_keys = at<uint64_t>(q.part_keys);
-      const int parts = 2 * ((q.V + gemm_mid_cols(q.V) - 1) / gemm_mid_cols(q.V));
+      const int parts = 2 * ((q.V + gemm_mid_cols(q.V, M) - 1) / gemm_mid_cols(q.V, M));
       prof_begin(RT_K_LM_HEAD, (double)q.V * q.d * sizeof(T) + (double)M * q.d * sizeof(T), 2.0 * M * q.V * q.d);
       g.partial = at<float>(q.partial); g.partial_floats = kPartialFloats;
       HIPCHK(gemm_mid(g, false, stream));

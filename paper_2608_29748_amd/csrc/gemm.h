@@ -116,7 +116,9 @@ hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s);
 // epilogue of this shape (1: none); a caller that adds the slabs itself requests them
 // with EPI_PARTIAL and this count
 int gemm_mid_store_slabs(const GemmArgs& a, bool a_f32);
-int gemm_mid_cols(int N);
+// Columns per workgroup of the mid-size kernel's argmax (LM head) launch over N columns
+// and M rows; it writes two partial keys per workgroup and row.
+int gemm_mid_cols(int N, int M);
 // Sums ks fp32 slabs part[z][M][N] (row-major, slab stride M*N) in slab order and runs
 // epilogue e on the result.
 template <typename T>
