@@ -137,7 +137,7 @@ struct Engine : EngineBase {
 
   // Algorithmic bytes an epilogue moves for an M x N result (outputs written, side
   // inputs read).
-  static double epi_bytes(const EpiArgs& e, int M, int N) {
+  static double epi_bytes(const EpiArgs& e, int M, int N, int slabs) {
     const double mn = (double)M * N;
     switch (e.kind) {
       case EPI_STORE_F32: return mn * 4;
@@ -146,7 +146,7 @@ struct Engine : EngineBase {
       case EPI_SWIGLU: return mn / 2 * sizeof(T);
       case EPI_COND_R: return mn * 8;
       case EPI_COND_GATE: return mn * 4;
-      case EPI_PARTIAL: return mn * 4 * kResidSplits;
+      case EPI_PARTIAL: return mn * 4 * slabs;
       default: return mn * (12 + sizeof(T));   // EPI_COND_OUT: gate, e rows, x and etilde
     }
   }
@@ -186,7 +186,7 @@ struct Engine : EngineBase {
     a.e = e;
     if (instrumented()) {
       const double Kl = (double)k_logical;
-      prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + epi_bytes(e, M, N),
+      prof_begin(kind, (double)N * Kl * sizeof(T) + (double)M * Kl * (af32 ? 4 : sizeof(T)) + epi_bytes(e, M, N, e.kind == EPI_PARTIAL ? ks : 1),
                  2.0 * M * N * Kl);
     }
     HIPCHK(gemm<T>(a, shape, af32, stream));
@@ -235,10 +235,18 @@ struct Engine : EngineBase {
     EpiArgs e{};
     if (c.defer && c.M <= q.rpart_rows && (c.M <= 32 || (sizeof(T) == 2 && !(flags & 4)))) {
       const size_t stride = (size_t)q.rpart_rows * q.d;
+      // skinny rows: 4 slabs; 65..512 rows (mid-size kernel): the slab count that fills
+      // the chip (e.g. 40 column tiles x 6 slabs at the 14B shape), at most 8
+      int ks = kResidSplits;
+      if (c.M > 64 && sizeof(T) == 2) {
+        GemmArgs g{};
+        g.Kp = Kp; g.partial_floats = (size_t)kResidSplitsMax * stride;
+        g.e.kind = EPI_PARTIAL; g.e.M = c.M; g.e.N = q.d;
+        ks = gemm_mid_partial_slabs(g, false, kResidSplitsMax);
+      }
       e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.rpart); e.ldo = q.d; e.part_stride = stride;
-      CHK(gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical));
-      pend = NormFold{at<float>(q.rpart), kResidSplits, stride, capture ? (void*)c.cap : nullptr, 16 * q.Kp_nc,
-                      c.cap_k0};
+      CHK(gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical, ks));
+      pend = NormFold{at<float>(q.rpart), ks, stride, capture ? (void*)c.cap : nullptr, 16 * q.Kp_nc, c.cap_k0};
       return RT_OK;
     }
     e.kind = EPI_RESID; e.resid = at<float>(q.x); e.ldr = q.d;

@@ -116,6 +116,9 @@ hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s);
 // epilogue of this shape (1: none); a caller that adds the slabs itself requests them
 // with EPI_PARTIAL and this count
 int gemm_mid_store_slabs(const GemmArgs& a, bool a_f32);
+// k slabs (1..max_slabs) for a GEMM whose fp32 slab partials a later kernel adds: the
+// count that fills the chip in the fewest rounds of the cost model
+int gemm_mid_partial_slabs(const GemmArgs& a, bool a_f32, int max_slabs);
 // Columns per workgroup of the mid-size kernel's argmax (LM head) launch over N columns
 // and M rows; it writes two partial keys per workgroup and row.
 int gemm_mid_cols(int N, int M);

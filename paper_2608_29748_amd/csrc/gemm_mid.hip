@@ -294,6 +294,26 @@ int gemm_mid_store_slabs(const GemmArgs& a, bool a_f32) {
   return mid_plan(g, g.e.M <= 128 ? 128 : 256, a_f32).ks;
 }
 
+int gemm_mid_partial_slabs(const GemmArgs& a, bool a_f32, int max_slabs) {
+  if (a.e.M <= 32 || a.e.M > 512) return 1;
+  const int MB = a.e.M <= 128 ? 128 : 256;
+  GemmArgs g = a;
+  g.e.kind = EPI_PARTIAL;
+  int best = 1;
+  double best_cost = 1e30;
+  for (int ks = 1; ks <= max_slabs; ++ks) {
+    if ((size_t)ks * g.e.M * g.e.N > a.partial_floats) break;
+    g.ksplit = ks;
+    const MidPlan pl = mid_plan(g, MB, a_f32);
+    const int KT = a.Kp / kTileK;
+    const long tiles = (long)((g.e.N + pl.NB - 1) / pl.NB) * ((g.e.M + MB - 1) / MB);
+    const double cost = (double)((tiles * ks + 255) / 256) * ((MB / 16) * (a_f32 ? 2 : 1) + pl.NB / 16) *
+                        ((KT + ks - 1) / ks);
+    if (cost < best_cost) { best_cost = cost; best = ks; }
+  }
+  return best;
+}
+
 hipError_t gemm_mid(const GemmArgs& a, bool a_f32, hipStream_t s) {
   if (!gemm_mid_supports(a)) return hipErrorInvalidValue;
   const int M = a.e.M, N = a.e.N;

@@ -22,7 +22,8 @@ inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 constexpr int kPrefillChunk = 512;     // prompt rows per prefill pass
 constexpr int kMaxTiles = 1 << 16;     // split-K arrival counters
 constexpr size_t kPartialFloats = (size_t)8 << 20;   // split-K partial capacity (32 MiB)
-constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections
+constexpr int kResidSplits = 4;   // k slabs of the round's o / down projections (skinny kernel)
+constexpr int kResidSplitsMax = 8;  // at most, on the mid-size kernel (the norm folds up to 8)
 constexpr int kArMaxSteps = RT_AR_MAX_STEPS;   // target-only greedy steps per rt_ar_steps call
 constexpr int kAttnRowsAr = 64;   // attention rows per block in target-only steps (the 64-row kernel)
 constexpr int kStateSlots = 16;   // int32 slots of per-sequence round state (fields in misc.h)
@@ -52,7 +53,7 @@ struct Plan {
   size_t x, xa, qbuf, attn, mlp, g, fcout, fa, etilde, mu, er, gate;
   size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
   size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys
-  size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplits][rpart_rows][d]
+  size_t rpart;                  // k-slab partials of the deferred residual GEMMs [kResidSplitsMax][rpart_rows][d]
   size_t ar_tok;                 // target-only step tokens [bmax][kArMaxSteps]
   size_t dist_ids_d, dist_p_d;   // sampling: drafter filtered distributions [R][RT_MAX_TOP_K]
   size_t dist_ids_v, dist_p_v;   // sampling: target filtered distributions [R][RT_MAX_TOP_K]

@@ -14,23 +14,25 @@ template <> struct KeepT<float> { __device__ static float of(float v) { return v
 // and added to the row, which is written back (and optionally captured, packed).  Every
 // load of the row (x, partials, weight) is issued before the first use, so the row costs
 // one memory latency; NP is the partial count when known at compile time (-1: runtime,
-// at most 8).
-template <typename T, typename K, int NP>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, int ldx,
+// at most 8), NTH the threads of the workgroup (1024 / NTH chunks per thread).
+template <typename T, typename K, int NP, int NTH>
+__global__ __launch_bounds__(NTH) void rmsnorm_kernel(float* __restrict__ x, int ldx,
                                                       const T* __restrict__ w, int d, float eps,
                                                       T* __restrict__ out, int ldg, K* keep, int ldk,
                                                       NormFold fold) {
   constexpr int MAXP = NP >= 0 ? NP : 8;
-  __shared__ float red[4];
+  constexpr int JM = 1024 / NTH;            // 8-float chunks per thread (d <= 8192)
+  constexpr int NWV = NTH / 64;
+  __shared__ float red[NWV];
   const int row = blockIdx.x;
   float* xr = x + (size_t)row * ldx;
   const int nch = d / 8;
   const int np = NP >= 0 ? NP : fold.n_part;
-  float4 xa[4][2], pa[4][MAXP > 0 ? MAXP : 1][2];
-  Frag<T> wf[4];
+  float4 xa[JM][2], pa[JM][MAXP > 0 ? MAXP : 1][2];
+  Frag<T> wf[JM];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c = threadIdx.x + j * 256;
+  for (int j = 0; j < JM; ++j) {
+    const int c = threadIdx.x + j * NTH;
     if (c < nch) {
       wf[j].load(w + 8 * c);
       xa[j][0] = *reinterpret_cast<const float4*>(xr + 8 * c);
@@ -44,11 +46,11 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, int
         }
     }
   }
-  float v[4][8];
+  float v[JM][8];
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c = threadIdx.x + j * 256;
+  for (int j = 0; j < JM; ++j) {
+    const int c = threadIdx.x + j * NTH;
     if (c < nch) {
       v[j][0] = xa[j][0].x; v[j][1] = xa[j][0].y; v[j][2] = xa[j][0].z; v[j][3] = xa[j][0].w;
       v[j][4] = xa[j][1].x; v[j][5] = xa[j][1].y; v[j][6] = xa[j][1].z; v[j][7] = xa[j][1].w;
@@ -80,11 +82,13 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, int
   ss = warp_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  float tot = red[0];
+#pragma unroll
+  for (int i = 1; i < NWV; ++i) tot += red[i];
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c = threadIdx.x + j * 256;
+  for (int j = 0; j < JM; ++j) {
+    const int c = threadIdx.x + j * NTH;
     if (c < nch) {
       Frag<T> f;
 #pragma unroll
@@ -102,12 +106,15 @@ template <typename T, typename K>
 void rmsnorm(float* x, int ldx, const T* w, int d, float eps, int rows, T* out, int ldg,
              K* keep, int ldk, const NormFold& fold, hipStream_t s) {
   if (rows <= 0) return;
+  // 256 threads with up to four 8-float chunks each; more than four partials (up to 8,
+  // the mid-size kernel's slabs): 1024 threads with one chunk each, so that every load
+  // of a row stays in flight within the register budget
   if (fold.n_part == 0)
-    RT_LAUNCH((rmsnorm_kernel<T, K, 0>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
+    RT_LAUNCH((rmsnorm_kernel<T, K, 0, 256>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
   else if (fold.n_part == 4)
-    RT_LAUNCH((rmsnorm_kernel<T, K, 4>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
+    RT_LAUNCH((rmsnorm_kernel<T, K, 4, 256>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
   else
-    RT_LAUNCH((rmsnorm_kernel<T, K, -1>), dim3(rows), dim3(256), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
+    RT_LAUNCH((rmsnorm_kernel<T, K, -1, 1024>), dim3(rows), dim3(1024), 0, s, x, ldx, w, d, eps, out, ldg, keep, ldk, fold);
 }
 template void rmsnorm<bf16_t, uint16_t>(float*, int, const bf16_t*, int, float, int, bf16_t*, int,
                                         uint16_t*, int, const NormFold&, hipStream_t);

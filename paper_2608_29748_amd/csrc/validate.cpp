@@ -164,7 +164,7 @@ int make_plan(const rt_config* c, Plan* p) {
   q.counters = take((size_t)kMaxTiles * 4);
   q.partial = take(kPartialFloats * 4);
   q.rpart_rows = q.R > 32 ? q.R : 32;
-  q.rpart = take((size_t)kResidSplits * q.rpart_rows * q.d * 4);
+  q.rpart = take((size_t)kResidSplitsMax * q.rpart_rows * q.d * 4);
   {
     size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
     (void)rb;
