@@ -20,6 +20,7 @@ struct AttnArgs {
   int row_blocks;                // row blocks of rb_rows (token, head) rows per sequence
   int rb_rows;                   // rows per block: 64, or 96 (bf16) when a sequence has 65..96 rows
   float* opart; float* mlpart;   // split partials
+  int32_t* plan;                 // [2][64] balanced split plan: first slot, split count per unit
   void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)
 };

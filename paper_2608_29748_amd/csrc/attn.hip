@@ -1,7 +1,7 @@
-// Paged GQA attention with MFMA.  One workgroup (4 waves) owns one sequence, one KV
-// head, one block of 64 (token, head) query rows and one contiguous share of the key
-// range, walked in 64-key chunks (four pages); each wave owns a 16-row MFMA tile of
-// the queries and runs an online softmax.  K pages are stored [token][hd] and V pages
+// Paged GQA attention with MFMA.  One workgroup owns one sequence, one KV head, one
+// block of 64 or 96 (token, head) query rows and one contiguous share of the key range
+// (shares sized by the sequence lengths of the batch), walked in 64-key chunks (four
+// pages); each wave owns a 16-row MFMA tile of the queries and runs an online softmax.  K pages are stored [token][hd] and V pages
 // transposed ([hd][token]), so a K row and a V^T row are contiguous MFMA fragments.
 // Split partials (unnormalised O, running max, running sum) are merged by a second
 // kernel.
@@ -20,6 +20,83 @@ constexpr int kMaxSplitPages = 1024;   // fp32 path: page ids of one split held 
 
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim, int rb_rows) {
   return (size_t)n_seqs * n_kv_heads * row_blocks * splits * rb_rows * head_dim;
+}
+
+extern "C" __device__ int __ockl_wfred_add_i32(int);
+extern "C" __device__ int __ockl_wfred_max_i32(int);
+extern "C" __device__ int __ockl_wfscan_add_i32(int, bool);
+
+// Key splits.  A work unit is one (sequence, row block), u = seq * row_blocks + rb; the
+// workgroups of one KV head are slots 0 .. n_units * splits - 1 (slot = blockIdx.z *
+// splits + blockIdx.x), and the partials of slot x of KV head h sit at block
+// h * n_slots + x.  Uniform plan: unit u owns slots u*splits .. u*splits + splits-1.
+// Balanced plan (2..64 units and splits > 1), for batches of unequal context lengths:
+// unit u owns s_u = ceil(n_u / q) consecutive slots, n_u being its number of 64-key
+// chunks and q the smallest chunk count per split for which the s_u fit in the slots.
+// q never exceeds the uniform plan's ceil(max n_u / splits), so no split is longer than
+// under the uniform plan, and s_u <= 64 (one merge lane per split).  Every wave derives
+// the plan from the sequence lengths; the workgroup of slot 0 of KV head 0 stores it
+// for the merge, which runs after the partial kernel on the same stream.
+__device__ __forceinline__ bool attn_balanced(const AttnArgs& a) {
+  const int nu = a.n_seqs * a.row_blocks;
+  return a.splits > 1 && nu > 1 && nu <= 64;
+}
+__device__ __forceinline__ int attn_unit_chunks(const AttnArgs& a, int u, int rbr) {
+  const int s = u / a.row_blocks, rb = u % a.row_blocks;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
+  const int nrows = nq * G, row0 = rb * rbr;
+  if (row0 >= nrows) return 0;
+  const int P = a.pos0[s * a.seq_stride];
+  const int last_tok = min(nrows, row0 + rbr) - 1;
+  const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;
+  return (kv_end + kChunk - 1) / kChunk;
+}
+struct SplitPlan {
+  int count;   // lane u: s_u (0 past the units)
+  int end;     // lane u: s_0 + .. + s_u
+};
+// Balanced plan; all 64 lanes of the wave must be active.
+__device__ __forceinline__ SplitPlan attn_balanced_plan(const AttnArgs& a, int rbr) {
+  const int lane = threadIdx.x & 63;
+  const int nu = a.n_seqs * a.row_blocks, slots = nu * a.splits;
+  const int n = lane < nu ? attn_unit_chunks(a, lane, rbr) : 0;
+  const int tot = __ockl_wfred_add_i32(n), mx = __ockl_wfred_max_i32(n);
+  int lo = max(1, max((tot + slots - 1) / slots, (mx + 63) / 64));
+  int hi = max(lo, (mx + a.splits - 1) / a.splits);
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (__ockl_wfred_add_i32((n + mid - 1) / mid) <= slots) hi = mid;
+    else lo = mid + 1;
+  }
+  const int cnt = (n + lo - 1) / lo;
+  return SplitPlan{cnt, __ockl_wfscan_add_i32(cnt, true)};
+}
+// Work of the workgroup at (blockIdx.x, blockIdx.z): unit, split index within the unit
+// and the unit's split count; false for a slot the balanced plan leaves idle.
+__device__ __forceinline__ bool attn_slot_work(const AttnArgs& a, int rbr, int& unit, int& split, int& nsplit) {
+  if (!attn_balanced(a)) {
+    unit = blockIdx.z; split = blockIdx.x; nsplit = a.splits;
+    return true;
+  }
+  const SplitPlan p = attn_balanced_plan(a, rbr);
+  const int slot = blockIdx.z * a.splits + blockIdx.x;
+  if (slot == 0 && blockIdx.y == 0 && threadIdx.x < 64) {   // hand the plan to the merge
+    a.plan[threadIdx.x] = p.end - p.count;
+    a.plan[64 + threadIdx.x] = p.count;
+  }
+  const unsigned long long m = __ballot(slot < p.end);   // units whose slots end past this one
+  if (m == 0) return false;
+  unit = __builtin_ctzll(m);                                 // the first of them owns it
+  nsplit = __builtin_amdgcn_readlane(p.count, unit);
+  split = slot - (__builtin_amdgcn_readlane(p.end, unit) - nsplit);
+  return true;
+}
+// First slot (x) and split count (y) of unit u (merge side): the balanced plan as the
+// partial kernel's first workgroup stored it.
+__device__ __forceinline__ int2 attn_unit_slots(const AttnArgs& a, int u) {
+  if (!attn_balanced(a)) return make_int2(u * a.splits, a.splits);
+  return make_int2(a.plan[u], a.plan[64 + u]);
 }
 
 // Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
@@ -44,8 +121,10 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
   constexpr bool kSplitP = sizeof(T) == 2;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g4 = lane / 16, c16 = lane % 16;
-  const int split = blockIdx.x, kvh = blockIdx.y;
-  const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks;
+  const int kvh = blockIdx.y;
+  int unit, split, nsplit;
+  if (!attn_slot_work(a, kAttnRows, unit, split, nsplit)) return;
+  const int s = unit / a.row_blocks, rb = unit % a.row_blocks;
   const int G = a.n_q_heads / a.n_kv_heads;
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int P = a.pos0[s * a.seq_stride];
@@ -56,7 +135,7 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end)
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
   // chunks spread evenly over the splits (counts differ by at most one)
-  const int c_beg = (int)((long)split * nchunks / a.splits), c_end = (int)((long)(split + 1) * nchunks / a.splits);
+  const int c_beg = (int)((long)split * nchunks / nsplit), c_end = (int)((long)(split + 1) * nchunks / nsplit);
   // page ids of this split's keys (pages past kv_end are never dereferenced)
   const int pg_beg = c_beg * PAGES;
   const int npg = max(0, min((kv_end + kPage - 1) / kPage, c_end * PAGES) - pg_beg);
@@ -227,7 +306,7 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
           op[pa_index(orow, h * HD + t * 16 + 4 * g4 + i, a.ldo)] = Elem<T>::from_f32(o[t][i] * inv);
     }
   } else {
-    const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
+    const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
     float* op = a.opart + blk * kAttnRows * HD;
     float* ml = a.mlpart + blk * kAttnRows * 2;
     const int rl = w * 16 + c16;
@@ -285,8 +364,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, g4 = lane >> 4, c16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rh = w >> 1, kh = w & 1;
-  const int split = blockIdx.x, kvh = blockIdx.y;
-  const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks;
+  const int kvh = blockIdx.y;
+  int unit, split, nsplit;
+  if (!attn_slot_work(a, RBR, unit, split, nsplit)) return;
+  const int s = unit / a.row_blocks, rb = unit % a.row_blocks;
   const int G = a.n_q_heads / a.n_kv_heads;
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int P = a.pos0[s * a.seq_stride];
@@ -297,7 +378,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end), kv_end >= 1
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
   // chunks spread evenly over the splits (counts differ by at most one)
-  const int c_beg = (int)((long)split * nchunks / a.splits), c_end = (int)((long)(split + 1) * nchunks / a.splits);
+  const int c_beg = (int)((long)split * nchunks / nsplit), c_end = (int)((long)(split + 1) * nchunks / nsplit);
   const int last_page = (kv_end - 1) / kPage;
   const_i32_t* pt = (const_i32_t*)(a.page_table + (size_t)s * a.max_pages);
   // page w of chunk c (pages past kv_end are replaced by the last valid one, so every
@@ -511,7 +592,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
             op[pa_index(orow, h * HD + t * 16 + 4 * g4 + e, a.ldo)] = f32_to_bf16(o[t2][t][e] * inv);
       }
     } else {
-      const size_t blk = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * a.splits + split;
+      const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
       float* op = a.opart + blk * RBR * HD;
       float* ml = a.mlpart + blk * RBR * 2;
       const int rw = rh * RH + rl;
@@ -535,14 +616,15 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int rl = blockIdx.x * 4 + (threadIdx.x >> 6);        // row within the row block
   const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks, kvh = blockIdx.y;
-  const int G = a.n_q_heads / a.n_kv_heads;
-  const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int RBR = a.rb_rows;
   if (rl >= RBR) return;
+  const int2 us = attn_unit_slots(a, blockIdx.z);
+  const int S = us.y;                         // <= 64
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int r = rb * RBR + rl;
   if (r >= nq * G) return;
-  const int S = a.splits;                     // <= 64
-  const size_t blk0 = (((size_t)s * a.n_kv_heads + kvh) * a.row_blocks + rb) * S;
+  const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
   const float* opp = a.opart + (blk0 * RBR + rl) * HD + lane;   // split j: + j * RBR * HD
   const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;          // split j: + j * RBR * 2
   float ob[NB][PL];

@@ -287,7 +287,7 @@ struct Engine : EngineBase {
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.rb_rows = c.rb_rows;
-    a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart);
+    a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart); a.plan = at<int32_t>(q.attn_plan);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
     if (instrumented()) {
       // keys read: every sequence's context plus the block, K and V, once per KV head

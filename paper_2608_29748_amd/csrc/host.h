@@ -49,7 +49,7 @@ struct Plan {
   size_t t_layers, d_layers, layer_bytes;               // per-layer blocks
   size_t lo_qkv, lo_o, lo_gu, lo_down, lo_in, lo_post, lo_qn, lo_kn;   // offsets within a layer block
   size_t kc, vc, dkc, dvc;
-  size_t page_table, rope, state, pf_ints, first_tok, counters, partial, opart, mlpart;
+  size_t page_table, rope, state, pf_ints, first_tok, counters, partial, opart, mlpart, attn_plan;
   size_t x, xa, qbuf, attn, mlp, g, fcout, fa, etilde, mu, er, gate;
   size_t hd_keep, ht_keep, dlogits, vlogits, dkeys, tkeys, dtok, ttok, out_tok, out_n, out_a, tokbuf;
   size_t qkvf, part_keys;        // fp32 q|k|v projection output; LM-head partial argmax keys

@@ -173,6 +173,7 @@ int make_plan(const rt_config* c, Plan* p) {
     if (ar_rows > rows) rows = ar_rows;
     q.opart = take(rows * q.hd * 4);
     q.mlpart = take(rows * 2 * 4);
+    q.attn_plan = take(2 * 64 * 4);
   }
   const size_t M = q.Mrows;
   q.x = take(M * q.d * 4);
