@@ -91,6 +91,17 @@ __device__ __forceinline__ void mid_argmax(const EpiArgs& e, const f32x4 (&acc)[
     }
 }
 
+// Wait until at most min(N, r) k tiles of LPW copies each are still in flight.
+template <int N, int LPW>
+__device__ __forceinline__ void wait_tiles(int r) {
+  if constexpr (N <= 0) {
+    wait_vm<0>();
+  } else {
+    if (r >= N) wait_vm<N * LPW>();
+    else wait_tiles<N - 1, LPW>(r);
+  }
+}
+
 template <int MB, int NB, int NSTAGE, bool AF32, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_mid_kernel(GemmArgs a) {
   constexpr int WM = NW / 2;            // wave rows (two wave columns)
@@ -150,13 +161,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
   for (int kt = kb; kt < ke; ++kt) {
     const int i = kt - kb;
     // this wave's copies of k tile kt have landed once at most the later tiles' remain
-    if constexpr (NSTAGE == 4) {
-      if (kt + 2 < ke) wait_vm<2 * LPW>(); else if (kt + 1 < ke) wait_vm<LPW>(); else wait_vm<0>();
-    } else if constexpr (NSTAGE == 3) {
-      if (kt + 1 < ke) wait_vm<LPW>(); else wait_vm<0>();
-    } else {
-      wait_vm<0>();
-    }
+    wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kt);
     lds_barrier();   // every wave's copies of tile kt are visible; tile kt-1's stage is free
     if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
     const char* st = smem + (i % NSTAGE) * STG;
@@ -232,8 +237,11 @@ template <bool AF32>
 static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t s) {
   // 8 waves (4 x 2, two per SIMD) for 256-row tiles and 128 x 128 tiles: 8-13% faster at
   // the 14B layer shapes and 3-6% at the 8B gate|up and q|k|v than 4 waves (2 x 2); the
-  // narrower and wider 128-row tiles stay at 4 waves.  The 256 x 192 (gate|up) and
-  // 256 x 256 (LM head) tiles take 16 waves (8 x 2), another 11% / 8% at the 14B shape.
+  // narrower and wider 128-row tiles stay at 4 waves.  The 256 x 160 and 256 x 192
+  // (gate|up) and 256 x 256 (LM head) tiles take 16 waves (8 x 2), another 11% / 8% at
+  // the 14B shape.  256 x 160 makes 218 workgroups of the 14B gate|up where 256 x 192
+  // makes 182 on 256 CUs: 3-5% faster there and 6% at a 512-row 4B-shape gate|up;
+  // deeper LDS rings (5, 6 stages) measured no faster at any of these shapes.
   // The output tile is split spatially, so every element is accumulated over k in the
   // same order either way.
   if (MB == 128) {
@@ -244,7 +252,8 @@ static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t
     if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32, 8>), grid, dim3(512), 0, s, a);
     else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, AF32 ? 3 : 4, AF32, 8>), grid, dim3(512), 0, s, a);
     else if constexpr (!AF32) {
-      if (NB == 192) RT_LAUNCH((gemm_mid_kernel<256, 192, 4, false, 16>), grid, dim3(1024), 0, s, a);
+      if (NB == 160) RT_LAUNCH((gemm_mid_kernel<256, 160, 4, false, 16>), grid, dim3(1024), 0, s, a);
+      else if (NB == 192) RT_LAUNCH((gemm_mid_kernel<256, 192, 4, false, 16>), grid, dim3(1024), 0, s, a);
       else RT_LAUNCH((gemm_mid_kernel<256, 256, 3, false, 16>), grid, dim3(1024), 0, s, a);
     }
   }
@@ -263,8 +272,9 @@ static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
   const size_t slab = (size_t)M * N;
   MidPlan best{64, 1};
   double best_cost = 1e30;
-  for (int NB : {64, 128, 192}) {
-    if (NB == 192 && a_f32) continue;
+  for (int NB : {64, 128, 160, 192}) {
+    if (NB >= 160 && a_f32) continue;
+    if (NB == 160 && (MB != 256 || a.e.kind == EPI_PARTIAL)) continue;
     const long tiles = (long)((N + NB - 1) / NB) * ((M + MB - 1) / MB);
     int ks = 1;
     if (a.e.kind == EPI_PARTIAL) {
@@ -276,7 +286,7 @@ static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
       if ((size_t)ks > a.partial_floats / slab) ks = (int)(a.partial_floats / slab);
       if (ks < 1) ks = 1;
     }
-    if (NB == 192 && ks > 1) continue;   // the wide tile is for large outputs only
+    if (NB >= 160 && ks > 1) continue;   // the wide tiles are for large outputs only
     const double rounds = (double)((tiles * ks + 255) / 256);
     double cost = rounds * (ai + NB / 16) * ((KT + ks - 1) / ks);
     // slabs are written and read back once (mostly from cache): a quarter of their
