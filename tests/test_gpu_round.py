@@ -51,6 +51,26 @@ def test_prefill_and_rounds_match_oracle(name):
     eng.close()
 
 
+@pytest.mark.parametrize("name,lens", [("tiny-f32", (20, 600)), ("mini-bf16-ragged", (20, 900))])
+def test_ragged_batch_key_splits_match_oracle(name, lens):
+    """A batch of very unequal contexts: the attention's key-split workgroups are shared
+    out by context length (one split for the short sequences, several for the long
+    ones, some workgroups idle), in the fp32 and the bf16 kernels."""
+    wl, W, prompts = _setup(name, norm_init="perturbed", batch=4, prompt_len=lens)
+    log(f"[{name} ragged] prompts {[len(p) for p in prompts]}")
+    eng = engine_for(wl, W)
+    R = OracleRunner(OracleModel(wl, W))
+    first = eng.prefill(prompts, wl.new_tokens)
+    states = [R.prefill(p, wl.new_tokens) for p in prompts]
+    assert list(first) == [st.anchor for st in states]
+    tol = TOL[wl.dtype]
+    rep = compare_prefill(eng, R, wl, prompts, states, tol)
+    log(f"[{name} ragged] prefill max err {rep.max_err}")
+    rep = run_teacher_forced(eng, R, wl, states, 4, tol, exact=_exact(wl, W, R))
+    log(f"[{name} ragged] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}")
+    eng.close()
+
+
 @pytest.mark.parametrize("name,mode", [("tiny-f32", "raw_gated"), ("tiny-f32", "overwrite"),
                                        ("mini-bf16", "raw_gated"), ("mini-bf16", "overwrite"),
                                        ("mini-bf16-ragged", "off"), ("mini-bf16-b4", "raw_gated"),
