@@ -22,6 +22,7 @@ size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int split
   return (size_t)n_seqs * n_kv_heads * row_blocks * splits * rb_rows * head_dim;
 }
 
+// wave-wide integer reductions and scan of the ROCm device library (DPP based)
 extern "C" __device__ int __ockl_wfred_add_i32(int);
 extern "C" __device__ int __ockl_wfred_max_i32(int);
 extern "C" __device__ int __ockl_wfscan_add_i32(int, bool);
@@ -93,10 +94,13 @@ __device__ __forceinline__ bool attn_slot_work(const AttnArgs& a, int rbr, int& 
   return true;
 }
 // First slot (x) and split count (y) of unit u (merge side): the balanced plan as the
-// partial kernel's first workgroup stored it.
+// partial kernel's first workgroup stored it, clamped to this launch's slots (a merge
+// replayed on its own, for timing, may find another launch's plan there).
 __device__ __forceinline__ int2 attn_unit_slots(const AttnArgs& a, int u) {
   if (!attn_balanced(a)) return make_int2(u * a.splits, a.splits);
-  return make_int2(a.plan[u], a.plan[64 + u]);
+  const int slots = a.n_seqs * a.row_blocks * a.splits;
+  const int first = min(max(a.plan[u], 0), slots);
+  return make_int2(first, min(max(a.plan[64 + u], 0), min(slots - first, 64)));
 }
 
 // Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
