@@ -241,11 +241,14 @@ static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t
   // (gate|up) and 256 x 256 (LM head) tiles take 16 waves (8 x 2), another 11% / 8% at
   // the 14B shape.  256 x 160 makes 218 workgroups of the 14B gate|up where 256 x 192
   // makes 182 on 256 CUs: 3-5% faster there and 6% at a 512-row 4B-shape gate|up;
-  // deeper LDS rings (5, 6 stages) measured no faster at any of these shapes.
+  // deeper LDS rings (5, 6 stages) measured no faster at any of these shapes.  Likewise
+  // 128 x 96 makes 256 workgroups of the 8B gate|up at 128 rows (192 of 128 x 128):
+  // 50.6 -> 49.0 us.
   // The output tile is split spatially, so every element is accumulated over k in the
   // same order either way.
   if (MB == 128) {
     if (NB == 64) RT_LAUNCH((gemm_mid_kernel<128, 64, 4, AF32, 4>), grid, dim3(256), 0, s, a);
+    else if (NB == 96) { if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<128, 96, 4, false, 8>), grid, dim3(512), 0, s, a); }
     else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32, 8>), grid, dim3(512), 0, s, a);
     else if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<128, 192, 4, false, 4>), grid, dim3(256), 0, s, a);
   } else {
@@ -272,9 +275,10 @@ static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
   const size_t slab = (size_t)M * N;
   MidPlan best{64, 1};
   double best_cost = 1e30;
-  for (int NB : {64, 128, 160, 192}) {
-    if (NB >= 160 && a_f32) continue;
+  for (int NB : {64, 96, 128, 160, 192}) {
+    if ((NB >= 160 || NB == 96) && a_f32) continue;
     if (NB == 160 && (MB != 256 || a.e.kind == EPI_PARTIAL)) continue;
+    if (NB == 96 && (MB != 128 || a.e.kind == EPI_PARTIAL)) continue;
     const long tiles = (long)((N + NB - 1) / NB) * ((M + MB - 1) / MB);
     int ks = 1;
     if (a.e.kind == EPI_PARTIAL) {
@@ -286,7 +290,7 @@ static MidPlan mid_plan(const GemmArgs& a, int MB, bool a_f32) {
       if ((size_t)ks > a.partial_floats / slab) ks = (int)(a.partial_floats / slab);
       if (ks < 1) ks = 1;
     }
-    if (NB >= 160 && ks > 1) continue;   // the wide tiles are for large outputs only
+    if ((NB >= 160 || NB == 96) && ks > 1) continue;   // tiles for large outputs only
     const double rounds = (double)((tiles * ks + 255) / 256);
     double cost = rounds * (ai + NB / 16) * ((KT + ks - 1) / ks);
     // slabs are written and read back once (mostly from cache): a quarter of their
