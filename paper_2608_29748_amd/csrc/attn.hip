@@ -701,9 +701,100 @@ hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   }
   return hipGetLastError();
 }
+// Sixteen lanes per (token, head) row: lane c of the row owns hd elements c*PL ..
+// c*PL + PL-1.  Each lane reads the (max, sum) pairs of splits c, c+16, .. for the row's
+// maximum and denominator (two DPP row reductions), then walks all splits in order,
+// loading a batch of partial O pieces and their maxima before weighting them, so the
+// split weights need no cross-lane exchange.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void attn_merge16_kernel(AttnArgs a) {
+  constexpr int PL = HD / 16;                 // hd elements per lane
+  constexpr int NB = 8;                       // splits per batch of loads
+  const int c = threadIdx.x & 15;
+  const int rl = blockIdx.x * 16 + (threadIdx.x >> 4);       // row within the row block
+  const int s = blockIdx.z / a.row_blocks, rb = blockIdx.z % a.row_blocks, kvh = blockIdx.y;
+  const int RBR = a.rb_rows;
+  if (rl >= RBR) return;                      // whole rows leave together
+  const int2 us = attn_unit_slots(a, blockIdx.z);
+  const int S = us.y;                         // <= 64
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
+  const int r = rb * RBR + rl;
+  if (r >= nq * G) return;
+  const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
+  const float* opp = a.opart + (blk0 * RBR + rl) * HD + c * PL;   // split j: + j * RBR * HD
+  const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;            // split j: + j * RBR * 2
+  float mj[4], lj[4];
+  float M = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = c + 16 * i;
+    mj[i] = -INFINITY;
+    lj[i] = 0.f;
+    if (j < S) {
+      const float2 v = *reinterpret_cast<const float2*>(mlp + (size_t)j * RBR * 2);
+      mj[i] = v.x;
+      lj[i] = v.y;
+    }
+    M = fmaxf(M, mj[i]);
+  }
+  M = row16_max(M);
+  float den = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    den += (M == -INFINITY || mj[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj[i] - M) * lj[i];
+  den = row16_sum(den);
+  float num[PL];
+#pragma unroll
+  for (int e = 0; e < PL; ++e) num[e] = 0.f;
+  for (int j0 = 0; j0 < S; j0 += NB) {
+    float4 ob[NB][PL / 4];
+    float mb[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      mb[j] = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < PL / 4; ++q) ob[j][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (j0 + j < S) {
+        const float* op = opp + (size_t)(j0 + j) * RBR * HD;
+#pragma unroll
+        for (int q = 0; q < PL / 4; ++q) ob[j][q] = *reinterpret_cast<const float4*>(op + 4 * q);
+        mb[j] = mlp[(size_t)(j0 + j) * RBR * 2];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float f = (M == -INFINITY || mb[j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mb[j] - M);
+#pragma unroll
+      for (int q = 0; q < PL / 4; ++q) {
+        num[4 * q] += f * ob[j][q].x;
+        num[4 * q + 1] += f * ob[j][q].y;
+        num[4 * q + 2] += f * ob[j][q].z;
+        num[4 * q + 3] += f * ob[j][q].w;
+      }
+    }
+  }
+  const int tok = r / G, h = kvh * G + r % G;
+  T* out = (T*)a.out;
+  const int orow = s * a.rows_per_seq + tok;
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+  for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + c * PL + e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
+}
+
 template <typename T>
 hipError_t attention_merge(const AttnArgs& a, hipStream_t s) {
   if (a.splits <= 1) return hipSuccess;
+  // few splits (batches): sixteen lanes per row, one batch of loads (8B-shape batch 8:
+  // 7.3 -> 3.5 us, 14B batch 16: 13.6 -> 4.4 us); many splits (batch 1, 32 splits): one
+  // wave per row with all 32 splits' loads in flight at once (3.6 us against 5.8)
+  if (a.splits <= 8) {
+    dim3 grid(kAttnRowsMax / 16, a.n_kv_heads, a.n_seqs * a.row_blocks);
+    if (a.head_dim == 128) RT_LAUNCH((attn_merge16_kernel<T, 128>), grid, dim3(256), 0, s, a);
+    else if (a.head_dim == 64) RT_LAUNCH((attn_merge16_kernel<T, 64>), grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   dim3 grid(kAttnRowsMax / 4, a.n_kv_heads, a.n_seqs * a.row_blocks);
   if (a.head_dim == 128) RT_LAUNCH((attn_merge_kernel<T, 128>), grid, dim3(256), 0, s, a);
   else if (a.head_dim == 64) RT_LAUNCH((attn_merge_kernel<T, 64>), grid, dim3(256), 0, s, a);
