@@ -71,11 +71,11 @@ def apply_rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray
 
 
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray,
-              k_pos: np.ndarray, causal: bool, round_p=None) -> np.ndarray:
+              k_pos: np.ndarray, causal: bool) -> np.ndarray:
     """Grouped-query softmax attention.  q[n, Hq, hd], k/v[T, Hkv, hd]; query head h
     reads kv head h // (Hq/Hkv).  causal: key position must not exceed the query's.
-    round_p: rounding applied to the unnormalised probabilities exp(s - max) before both
-    the weighted sum of values and the normaliser (the storage type for bf16 models)."""
+    The probabilities are the plain softmax of the scaled scores (no storage rounding:
+    only the stored output is rounded)."""
     n, hq, hd = q.shape
     group = hq // k.shape[1]
     out = np.empty_like(q)
@@ -86,8 +86,6 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray,
         s = np.where(visible, s, -np.inf)
         s = s - s.max(axis=1, keepdims=True)
         p = np.exp(s)
-        if round_p is not None:
-            p = round_p(p)
         p /= p.sum(axis=1, keepdims=True)
         out[:, h, :] = p @ v[:, kh, :]
     return out
@@ -192,7 +190,7 @@ class OracleModel:
     def _attn_mlp(self, pre: str, x, q, keys, vals, q_pos, k_pos, causal: bool):
         W, P = self.W, self.prec
         n = x.shape[0]
-        o = P.a(attention(q, keys, vals, q_pos, k_pos, causal, round_p=P.a)).reshape(n, -1)
+        o = P.a(attention(q, keys, vals, q_pos, k_pos, causal)).reshape(n, -1)
         x = P.r(x + o @ W[f"{pre}.o_proj"].T)
         h = P.a(rms_norm(x, W[f"{pre}.post_norm"], self.eps))
         a = P.a(silu(h @ W[f"{pre}.gate_proj"].T) * (h @ W[f"{pre}.up_proj"].T))
