@@ -148,10 +148,15 @@ def cpu_baseline(eng, wl, W, prompts, seconds: float):
         el = time.perf_counter() - t0
         if el >= seconds or st.done:
             break
-    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    return {"value": committed / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    blas = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    host = os.cpu_count() or 1
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else host
+    used = min(blas, usable)
+    return {"value": committed / el, "unit": "tokens/s", "cores": used, "kind": "oracle",
             "sample": f"{rounds} round(s) of sequence 0 at context {P}, started from the GPU's KV caches and "
-                      f"carried state; {el:.1f}s of CPU time; float64 numpy with {threads} BLAS threads",
+                      f"carried state; {el:.1f}s of wall time; float64 numpy, {blas} BLAS threads on "
+                      f"{usable} usable of {host} host CPUs",
+            "host_cpus": host, "usable_cpus": usable, "blas_threads": blas,
             "seconds_per_round": el / rounds}
 
 
@@ -268,8 +273,8 @@ def main():
     for name, v in kinds.items():
         if not v["launches"]:
             continue
-        per_round = v["launches"] / args.profile_rounds
-        rec = {"launches_per_round": per_round, "GB_per_launch": v["bytes"] / v["launches"] / 1e9,
+        launches_per_round = v["launches"] / args.profile_rounds
+        rec = {"launches_per_round": launches_per_round, "GB_per_launch": v["bytes"] / v["launches"] / 1e9,
                "us_per_launch_profiled_round": v["ms"] * 1e3 / v["launches"]}
         if name in replay:
             r = replay[name]
@@ -278,6 +283,10 @@ def main():
             rec["achieved_GBs"] = r["bytes"] / r["launches"] / (us * 1e-6) / 1e9
             rec["achieved_TFLOPs"] = r["flops"] / r["launches"] / (us * 1e-6) / 1e12
         kernels[name] = rec
+    round_ms_p50 = float(np.median(per_round) * 1e3)
+    # the timed loop's per-round wall times and its mean must describe the same rounds
+    assert abs(round_ms_p50 - elapsed * 1e3 / args.steps) <= 0.25 * elapsed * 1e3 / args.steps, \
+        (round_ms_p50, elapsed * 1e3 / args.steps)
     dom = replay[DOMINANT]
     per_launch_bytes = dom["bytes"] / dom["launches"]
     per_launch_us = dom["ms"] * 1e3 / dom["launches"]
@@ -314,7 +323,7 @@ def main():
         "kernels": kernels,
         "acceptance": {"mean_A": float(np.mean(accepted)) if accepted else None,
                        "mean_committed_per_round": committed / args.steps / wl.batch},
-        "round_ms_p50": float(np.median(per_round) * 1e3),
+        "round_ms_p50": round_ms_p50,
         "prefill_s": prefill_s,
     }
     if not args.no_cpu_baseline:

@@ -223,7 +223,12 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
 
 /* Debug flags: 1 = store fp32 logits of both LM heads; 2 = run rounds without
  * HIP-graph replay; 4 = split the reduction of every GEMM four ways (exercises the
- * split-K path on small models). */
+ * split-K path on small models); 8 = layer trace: rounds run without graph replay and
+ * keep every drafter and target layer's residual input and both LM heads' input
+ * operands (RT_T_TRACE_*), so each layer can be checked on its own inputs.  Setting
+ * flag 8 the first time allocates the trace buffer on the device (released by
+ * rt_destroy): (draft_layers + n_layers + 2) x max_batch x block_size x hidden x 4
+ * bytes plus two LM-head operands.  Returns RT_ERR_HIP if that allocation fails. */
 int rt_set_debug(rt_model* m, int32_t flags);
 
 /* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)
@@ -253,10 +258,21 @@ enum {
   RT_T_TARGET_K = 100,     /* + layer: [pos][Hkv][hd] storage type, positions 0.. */
   RT_T_TARGET_V = 200,     /* + layer */
   RT_T_DRAFT_K = 300,      /* + drafter layer: context keys */
-  RT_T_DRAFT_V = 400       /* + drafter layer */
+  RT_T_DRAFT_V = 400,      /* + drafter layer */
+  /* layer trace of the last round (debug flag 8), [block][d] per sequence: */
+  RT_T_TRACE_DRAFT_X = 500,   /* + l, l = 0..draft_layers: f32 residual input of drafter layer l
+                                 (l = draft_layers: the residual entering the final norm) */
+  RT_T_TRACE_TARGET_X = 600,  /* + l, l = 0..n_layers: the same for the verify pass */
+  RT_T_TRACE_DRAFT_HEAD = 700,  /* drafter LM-head input (final-norm output, storage type) */
+  RT_T_TRACE_VERIFY_HEAD = 701  /* verify LM-head input (storage type) */
 };
-/* Copies `bytes` of tensor `tensor_id` for sequence `seq` to host memory. */
+/* Copies `bytes` of tensor `tensor_id` for sequence `seq` to host memory.  Reading a
+ * trace tensor before flag 8 was set returns RT_ERR_STATE. */
 int rt_debug_read(rt_model* m, int32_t tensor_id, int32_t seq, void* host_dst, size_t bytes);
+/* Like rt_debug_read for the KV cache tensors (RT_T_TARGET_K/V, RT_T_DRAFT_K/V + layer),
+ * starting at position pos0: `bytes` covers positions pos0.. in the [pos][Hkv][hd]
+ * layout.  Other tensors return RT_ERR_INVALID. */
+int rt_debug_read_rows(rt_model* m, int32_t tensor_id, int32_t seq, int32_t pos0, void* host_dst, size_t bytes);
 /* Overwrites RT_T_HD, RT_T_HT or RT_T_STATE of sequence `seq` from host memory
  * (state injection for tests). */
 int rt_debug_write(rt_model* m, int32_t tensor_id, int32_t seq, const void* host_src, size_t bytes);

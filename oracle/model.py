@@ -207,24 +207,30 @@ class OracleModel:
                         ctx_k=z(wl.draft_layers), ctx_v=z(wl.draft_layers), budget=budget)
 
     # -- target
+    def target_layer(self, st: SeqState, l: int, x: np.ndarray, pos0: int) -> np.ndarray:
+        """Target decoder layer l on residual rows x at positions pos0..: writes their
+        K/V into st's cache at layer l (rows at and beyond pos0 are overwritten) and
+        attends causally to cache rows 0..pos.  Returns the layer's output residual."""
+        n = x.shape[0]
+        pos = pos0 + np.arange(n)
+        pre = f"target.{l}"
+        q, k, v = self._qkv(pre, x, pos)
+        st.tgt_k[l, pos0:pos0 + n] = k
+        st.tgt_v[l, pos0:pos0 + n] = v
+        end = pos0 + n
+        return self._attn_mlp(pre, x, q, st.tgt_k[l, :end], st.tgt_v[l, :end], pos,
+                              np.arange(end), causal=True)
+
     def target_forward(self, st: SeqState, tokens, pos0: int) -> VerifyOut:
         """Run rows `tokens` at positions pos0.. through the target, writing their K/V
         into st's cache (rows at and beyond pos0 are overwritten), attending causally
         to cache rows 0..pos."""
         s, W, P = self.s, self.W, self.prec
         tokens = np.asarray(tokens)
-        n = len(tokens)
-        pos = pos0 + np.arange(n)
         x = P.r(W.rows("embed", tokens))
         g = []
         for l in range(s.n_layers):
-            pre = f"target.{l}"
-            q, k, v = self._qkv(pre, x, pos)
-            st.tgt_k[l, pos0:pos0 + n] = k
-            st.tgt_v[l, pos0:pos0 + n] = v
-            end = pos0 + n
-            x = self._attn_mlp(pre, x, q, st.tgt_k[l, :end], st.tgt_v[l, :end], pos,
-                               np.arange(end), causal=True)
+            x = self.target_layer(st, l, x, pos0)
             if l in self.wl.cond_layers:
                 g.append(P.a(x))
         h = rms_norm(x, W["target.final_norm"], self.eps)
@@ -246,21 +252,24 @@ class OracleModel:
                                                        pos, self.theta))
             st.ctx_v[l, pos0:pos0 + n] = P.a(v)
 
+    def drafter_layer(self, st: SeqState, l: int, x: np.ndarray) -> np.ndarray:
+        """Drafter layer l on the block's residual rows x at positions P..P+B: queries
+        attend to context rows 0..P-1 of st's drafter cache and to every block row."""
+        n = x.shape[0]
+        pos = st.P + np.arange(n)
+        pre = f"draft.{l}"
+        q, k, v = self._qkv(pre, x, pos)
+        keys = np.concatenate([st.ctx_k[l, :st.P], k], axis=0)
+        vals = np.concatenate([st.ctx_v[l, :st.P], v], axis=0)
+        return self._attn_mlp(pre, x, q, keys, vals, pos, np.concatenate([np.arange(st.P), pos]),
+                              causal=False)
+
     def drafter_forward(self, st: SeqState, e_tilde: np.ndarray):
         """Block of B+1 conditioned rows at positions P..P+B over context rows 0..P-1."""
-        W, P = self.W, self.prec
-        n = e_tilde.shape[0]
-        pos = st.P + np.arange(n)
-        ctx_pos = np.arange(st.P)
-        x = P.r(e_tilde)
+        x = self.prec.r(e_tilde)
         for l in range(self.wl.draft_layers):
-            pre = f"draft.{l}"
-            q, k, v = self._qkv(pre, x, pos)
-            keys = np.concatenate([st.ctx_k[l, :st.P], k], axis=0)
-            vals = np.concatenate([st.ctx_v[l, :st.P], v], axis=0)
-            x = self._attn_mlp(pre, x, q, keys, vals, pos, np.concatenate([ctx_pos, pos]),
-                               causal=False)
-        h = rms_norm(x, W["draft.final_norm"], self.eps)
+            x = self.drafter_layer(st, l, x)
+        h = rms_norm(x, self.W["draft.final_norm"], self.eps)
         return h, self.lm_logits(h)
 
     def block_inputs(self, anchor: int) -> np.ndarray:

@@ -30,6 +30,7 @@ RT_MAX_COND_LAYERS = 8
 RT_MAX_TOP_K = 64
 RT_AR_MAX_STEPS = 256
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
+RT_T_TRACE_DRAFT_X, RT_T_TRACE_TARGET_X, RT_T_TRACE_DRAFT_HEAD, RT_T_TRACE_VERIFY_HEAD = 500, 600, 700, 701
 (RT_K_GEMM_QKV, RT_K_GEMM_O, RT_K_GEMM_GATE_UP, RT_K_GEMM_DOWN, RT_K_GEMM_CONTEXT, RT_K_GEMM_COND,
  RT_K_ATTENTION, RT_K_ATTN_MERGE, RT_K_NORM, RT_K_QKV_POST, RT_K_LM_HEAD, RT_K_MISC) = range(12)
 RT_K_KINDS = 12
@@ -40,7 +41,7 @@ RT_PROF_STAGES = 7
 
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
-           "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps"]
+           "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps", "rt_debug_read_rows"]
 
 
 class RetraceError(RuntimeError):
@@ -87,13 +88,14 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_last_error.restype = C.c_char_p
     lib.rt_set_debug.argtypes = [P, C.c_int32]
     lib.rt_debug_read.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
+    lib.rt_debug_read_rows.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_debug_write.argtypes = [P, C.c_int32, C.c_int32, P, C.c_size_t]
     lib.rt_profile_round.argtypes = [P, C.POINTER(rt_kernel_stat), C.POINTER(C.c_double), i32p, i32p, i32p]
     lib.rt_time_kernel.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(rt_kernel_stat)]
     lib.rt_ar_steps.argtypes = [P, C.c_int32, i32p, i32p]
     for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
-                 "rt_set_debug", "rt_debug_read", "rt_debug_write", "rt_profile_round", "rt_time_kernel",
-                 "rt_ar_steps"):
+                 "rt_set_debug", "rt_debug_read", "rt_debug_read_rows", "rt_debug_write", "rt_profile_round",
+                 "rt_time_kernel", "rt_ar_steps"):
         getattr(lib, name).restype = C.c_int
     return lib
 
@@ -213,6 +215,12 @@ def rt_set_debug(h: int, flags: int) -> None:
 def rt_debug_read(h: int, tensor_id: int, seq: int, nbytes: int) -> bytes:
     buf = C.create_string_buffer(nbytes)
     _check(_lib.rt_debug_read(C.c_void_p(h), tensor_id, seq, buf, nbytes))
+    return buf.raw
+
+
+def rt_debug_read_rows(h: int, tensor_id: int, seq: int, pos0: int, nbytes: int) -> bytes:
+    buf = C.create_string_buffer(nbytes)
+    _check(_lib.rt_debug_read_rows(C.c_void_p(h), tensor_id, seq, pos0, buf, nbytes))
     return buf.raw
 
 

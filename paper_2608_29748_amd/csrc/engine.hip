@@ -46,6 +46,33 @@ struct EngineBase {
   hipGraphExec_t ar_gexec = nullptr;
   bool ar_mode = false;                // target-only steps ran since the last prefill
   int32_t* h_out = nullptr;      // pinned: tokens [R], n [bmax], a [bmax], first [bmax]
+  // Layer trace (test hook, debug flag 8): every layer's residual input and both LM
+  // heads' inputs of the last eager round, copied into a device buffer of its own.
+  // Slots: drafter residuals 0..LD (LD: after the last layer), target residuals
+  // LD+1 .. LD+1+L, each [R][d] f32; then the drafter and verify LM-head operands,
+  // packed as the activation buffer.
+  char* trace = nullptr;
+  size_t trace_slot_bytes = 0, trace_head_bytes = 0;
+  bool tracing() const { return trace && (flags & 8) && !instrumented(); }
+  int trace_copy(size_t off, const void* src, size_t bytes) {
+    if (!tracing()) return RT_OK;
+    HIPCHK(hipMemcpyAsync(trace + off, src, bytes, hipMemcpyDeviceToDevice, stream));
+    return RT_OK;
+  }
+  int trace_x(int slot, const float* x, int rows) {
+    return trace_copy((size_t)slot * trace_slot_bytes, x, (size_t)rows * p.d * 4);
+  }
+  int trace_head(int which, const void* xa) {
+    return trace_copy((size_t)(p.LD + p.L + 2) * trace_slot_bytes + (size_t)which * trace_head_bytes, xa,
+                      trace_head_bytes);
+  }
+  int alloc_trace() {
+    if (trace) return RT_OK;
+    trace_slot_bytes = rup((size_t)p.R * p.d * 4, 256);
+    trace_head_bytes = rup(rup((size_t)p.R, 16) * p.Kp_d * p.esz, 256);
+    HIPCHK(hipMalloc((void**)&trace, (size_t)(p.LD + p.L + 2) * trace_slot_bytes + 2 * trace_head_bytes));
+    return RT_OK;
+  }
   // profiling: an event pair around every launch, aggregated per kernel kind
   bool profiling = false;
   std::vector<hipEvent_t> ev_pool;
@@ -91,6 +118,7 @@ struct EngineBase {
     for (hipEvent_t e : stage_ev) if (e) (void)hipEventDestroy(e);
     drop_graph();
     if (h_out) (void)hipHostFree(h_out);
+    if (trace) (void)hipFree(trace);
     if (own_stream && stream) (void)hipStreamDestroy(stream);
   }
   void drop_graph() {
@@ -126,7 +154,7 @@ struct EngineBase {
   int ar_steps(int n, int32_t* tokens, int32_t* n_gen);
   int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int time_kernel(int kind, int reps, rt_kernel_stat* out);
-  int debug_read(int id, int seq, void* dst, size_t bytes);
+  int debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0 = 0);
   int debug_write(int id, int seq, const void* src, size_t bytes);
 };
 
@@ -215,6 +243,7 @@ struct Engine : EngineBase {
     int cap_k0;                  // column offset of this layer's slot in the capture
     const int32_t* prof_ctx;     // host copy of each sequence's context length (profiling only)
     int defer;                   // o / down (<= 32 rows): k-slab partials, added by the next norm
+    int trace = -1;              // layer-trace slot of this layer's residual input (-1: none)
   };
   // partials of the last deferred residual GEMM, consumed by the next norm of x
   NormFold pend{};
@@ -259,6 +288,7 @@ struct Engine : EngineBase {
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
     norm_x((const T*)(lw + q.lo_in), c.M, nullptr, 0);
+    if (c.trace >= 0) CHK(trace_x(c.trace, x, c.M));   // the norm has folded any deferred partials into x
     // q|k|v on the mid-size kernel with k slabs: the slabs go to the split buffer and
     // qkv_post adds them (in slab order, as the slab epilogue would) while reading
     const int qks = qkv_slabs(c.M);
@@ -588,10 +618,13 @@ struct Engine : EngineBase {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 0, q.attn_splits, q.attn_rb, q.attn_rows, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.dkc) + (size_t)l * q.cache_layer_elems, at<T>(q.dvc) + (size_t)l * q.cache_layer_elems,
                  nullptr, 0, prof_ctx.data(), 1};
+      c.trace = l;
       CHK(layer(dlayer(l), c));
     }
     stage(2);
     norm_x(at<T>(q.d_final_norm), R, at<K>(q.hd_keep), q.d);
+    CHK(trace_x(q.LD, x, R));
+    CHK(trace_head(0, xa));
     const bool smp = sampling();
     CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (smp || (flags & 1)) ? at<float>(q.dlogits) : nullptr));
     // sampling: the drafter's filtered distributions, drafts drawn into dtok (unless forced)
@@ -609,10 +642,13 @@ struct Engine : EngineBase {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, q.attn_rows, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
                  slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data(), 1};
+      c.trace = q.LD + 1 + l;
       CHK(layer(tlayer(l), c));
     }
     stage(4);
     norm_x(at<T>(q.t_final_norm), R, at<K>(q.ht_keep), q.d);
+    CHK(trace_x(q.LD + 1 + q.L, x, R));
+    CHK(trace_head(1, xa));
     CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (smp || (flags & 1)) ? at<float>(q.vlogits) : nullptr));
     if (smp)
       CHK(dists(at<float>(q.vlogits), R, at<int32_t>(q.dist_ids_v), at<float>(q.dist_p_v), SAMPLE_NONE, 0, nullptr));
@@ -725,7 +761,7 @@ int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, i
       }
     HIPCHK(hipMemcpyAsync(ws + q.dtok, h.data(), h.size() * 4, hipMemcpyHostToDevice, stream));
     CHK(run_round(true));
-  } else if (flags & 2) {
+  } else if (flags & 10) {   // eager launches (debug flag 2, or the layer trace)
     CHK(run_round(false));
   } else {
     CHK(capture_once(graph, gexec, [&] { return run_round(false); }));
@@ -852,37 +888,70 @@ int EngineBase::time_kernel(int kind, int reps, rt_kernel_stat* out) {
 }
 
 static int copy_pages(const EngineBase& m, size_t cache_off, int layer, int seq, bool vlayout, void* dst,
-                      size_t bytes) {
+                      size_t bytes, size_t pos0 = 0) {
   const Plan& q = m.p;
   const size_t E = q.esz, hd = q.hd, H = q.Hkv;
   const size_t per_pos = H * hd * E;
   const size_t npos = bytes / per_pos;
-  if (npos > (size_t)q.T) return fail(RT_ERR_INVALID, "read past max_seq_len");
+  if (bytes % per_pos) return fail(RT_ERR_INVALID, "read of %zu bytes is not a whole number of positions", bytes);
+  if (pos0 + npos > (size_t)q.T) return fail(RT_ERR_INVALID, "read past max_seq_len");
   std::vector<int32_t> pt((size_t)q.pages_per_seq);
   HIPCHK(hipMemcpy(pt.data(), m.ws + q.page_table + (size_t)seq * q.pages_per_seq * 4, pt.size() * 4,
                    hipMemcpyDeviceToHost));
   const size_t page_bytes = H * 16 * hd * E;
   std::vector<char> buf(page_bytes);
   char* out = (char*)dst;
-  for (size_t pg = 0; pg * 16 < npos; ++pg) {
+  const size_t end = pos0 + npos;
+  for (size_t pg = pos0 / 16; pg * 16 < end; ++pg) {
     const char* src = m.ws + cache_off + ((size_t)layer * q.cache_layer_elems) * E + (size_t)pt[pg] * page_bytes;
     HIPCHK(hipMemcpy(buf.data(), src, page_bytes, hipMemcpyDeviceToHost));
-    for (size_t t = 0; t < 16 && pg * 16 + t < npos; ++t)
+    for (size_t t = 0; t < 16; ++t) {
+      const size_t pos = pg * 16 + t;
+      if (pos < pos0 || pos >= end) continue;
       for (size_t h = 0; h < H; ++h)
         for (size_t e = 0; e < hd; ++e) {
           const size_t si = vlayout ? ((h * hd + e) * 16 + t) : ((h * 16 + t) * hd + e);
-          memcpy(out + ((pg * 16 + t) * H * hd + h * hd + e) * E, buf.data() + si * E, E);
+          memcpy(out + ((pos - pos0) * H * hd + h * hd + e) * E, buf.data() + si * E, E);
         }
+    }
   }
   return RT_OK;
 }
 
-int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
+int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0) {
   const Plan& q = p;
   if (!dst) return fail(RT_ERR_INVALID, "null destination");
   if (seq < 0 || seq >= q.bmax) return fail(RT_ERR_INVALID, "sequence index out of range");
+  const bool kv = (id >= RT_T_TARGET_K && id < RT_T_TARGET_K + q.L) || (id >= RT_T_TARGET_V && id < RT_T_TARGET_V + q.L) ||
+                  (id >= RT_T_DRAFT_K && id < RT_T_DRAFT_K + q.LD) || (id >= RT_T_DRAFT_V && id < RT_T_DRAFT_V + q.LD);
+  if (pos0 && !kv) return fail(RT_ERR_INVALID, "a first position applies to KV cache tensors only");
   size_t off = 0, cap = 0;
   const size_t bk = q.bk;
+  const bool trace_x_id = (id >= RT_T_TRACE_DRAFT_X && id <= RT_T_TRACE_DRAFT_X + q.LD) ||
+                          (id >= RT_T_TRACE_TARGET_X && id <= RT_T_TRACE_TARGET_X + q.L);
+  if (trace_x_id || id == RT_T_TRACE_DRAFT_HEAD || id == RT_T_TRACE_VERIFY_HEAD) {
+    if (!trace) return fail(RT_ERR_STATE, "the layer trace is off (debug flag 8)");
+    HIPCHK(hipStreamSynchronize(stream));
+    if (trace_x_id) {
+      const int slot = id < RT_T_TRACE_TARGET_X ? id - RT_T_TRACE_DRAFT_X : q.LD + 1 + (id - RT_T_TRACE_TARGET_X);
+      if (bytes > bk * q.d * 4) return fail(RT_ERR_INVALID, "read too large");
+      HIPCHK(hipMemcpy(dst, trace + (size_t)slot * trace_slot_bytes + (size_t)seq * bk * q.d * 4, bytes,
+                       hipMemcpyDeviceToHost));
+      return RT_OK;
+    }
+    // packed LM-head operand -> row-major [bk][d] of the storage type
+    const size_t ldg = (size_t)16 * q.Kp_d;
+    if (bytes > bk * q.d * q.esz) return fail(RT_ERR_INVALID, "read too large");
+    std::vector<char> buf(trace_head_bytes);
+    const size_t base = (size_t)(q.LD + q.L + 2) * trace_slot_bytes + (id == RT_T_TRACE_VERIFY_HEAD ? trace_head_bytes : 0);
+    HIPCHK(hipMemcpy(buf.data(), trace + base, trace_head_bytes, hipMemcpyDeviceToHost));
+    char* out = (char*)dst;
+    const size_t nrow = bytes / ((size_t)q.d * q.esz);
+    for (size_t r = 0; r < nrow; ++r)
+      for (size_t k = 0; k < (size_t)q.d; ++k)
+        memcpy(out + (r * q.d + k) * q.esz, buf.data() + pa_index((int)(seq * bk + r), (int)k, ldg) * q.esz, q.esz);
+    return RT_OK;
+  }
   switch (id) {
     case RT_T_DRAFT_LOGITS: off = q.dlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
     case RT_T_VERIFY_LOGITS: off = q.vlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
@@ -916,10 +985,10 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes) {
     }
     default: {
       HIPCHK(hipStreamSynchronize(stream));
-      if (id >= RT_T_TARGET_K && id < RT_T_TARGET_K + q.L) return copy_pages(*this, q.kc, id - RT_T_TARGET_K, seq, false, dst, bytes);
-      if (id >= RT_T_TARGET_V && id < RT_T_TARGET_V + q.L) return copy_pages(*this, q.vc, id - RT_T_TARGET_V, seq, true, dst, bytes);
-      if (id >= RT_T_DRAFT_K && id < RT_T_DRAFT_K + q.LD) return copy_pages(*this, q.dkc, id - RT_T_DRAFT_K, seq, false, dst, bytes);
-      if (id >= RT_T_DRAFT_V && id < RT_T_DRAFT_V + q.LD) return copy_pages(*this, q.dvc, id - RT_T_DRAFT_V, seq, true, dst, bytes);
+      if (id >= RT_T_TARGET_K && id < RT_T_TARGET_K + q.L) return copy_pages(*this, q.kc, id - RT_T_TARGET_K, seq, false, dst, bytes, pos0);
+      if (id >= RT_T_TARGET_V && id < RT_T_TARGET_V + q.L) return copy_pages(*this, q.vc, id - RT_T_TARGET_V, seq, true, dst, bytes, pos0);
+      if (id >= RT_T_DRAFT_K && id < RT_T_DRAFT_K + q.LD) return copy_pages(*this, q.dkc, id - RT_T_DRAFT_K, seq, false, dst, bytes, pos0);
+      if (id >= RT_T_DRAFT_V && id < RT_T_DRAFT_V + q.LD) return copy_pages(*this, q.dvc, id - RT_T_DRAFT_V, seq, true, dst, bytes, pos0);
       return fail(RT_ERR_INVALID, "unknown tensor id %d", id);
     }
   }
@@ -1088,7 +1157,11 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
 
 int rt_set_debug(rt_model* m, int32_t flags) {
   if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
-  if (flags < 0 || flags > 7) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  if (flags < 0 || flags > 15) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  if (flags & 8) {
+    const int st = m->e->alloc_trace();
+    if (st) return st;
+  }
   m->e->flags = flags;
   m->e->drop_graph();
   return RT_OK;
@@ -1100,6 +1173,16 @@ int rt_debug_read(rt_model* m, int32_t tensor_id, int32_t seq, void* host_dst, s
     return m->e->debug_read(tensor_id, seq, host_dst, bytes);
   } catch (...) {
     return fail(RT_ERR_INVALID, "unexpected exception in rt_debug_read");
+  }
+}
+
+int rt_debug_read_rows(rt_model* m, int32_t tensor_id, int32_t seq, int32_t pos0, void* host_dst, size_t bytes) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    if (pos0 < 0) return fail(RT_ERR_INVALID, "negative first position");
+    return m->e->debug_read(tensor_id, seq, host_dst, bytes, (size_t)pos0);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_debug_read_rows");
   }
 }
 

@@ -36,14 +36,14 @@ int validate_config(const rt_config* c) {
   if (c->vocab < 16 || c->vocab % 16) return fail(RT_ERR_INVALID, "vocab must be a positive multiple of 16");
   if (c->hidden < 32 || c->hidden % 32 || c->hidden > 8192)
     return fail(RT_ERR_INVALID, "hidden must be a multiple of 32 in [32, 8192]");
-  if (c->n_layers < 1) return fail(RT_ERR_INVALID, "n_layers must be >= 1");
+  if (c->n_layers < 1 || c->n_layers > 99) return fail(RT_ERR_INVALID, "n_layers must be in [1, 99]");
   if (c->head_dim != 64 && c->head_dim != 128) return fail(RT_ERR_INVALID, "head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
     return fail(RT_ERR_INVALID, "n_q_heads must be a positive multiple of n_kv_heads");
   if ((c->n_q_heads * c->head_dim) % 128 || (c->n_kv_heads * c->head_dim) % 128)
     return fail(RT_ERR_INVALID, "q and kv projection widths must be multiples of 128");
   if (c->ffn < 16 || c->ffn % 16) return fail(RT_ERR_INVALID, "ffn must be a positive multiple of 16");
-  if (c->draft_layers < 1) return fail(RT_ERR_INVALID, "draft_layers must be >= 1");
+  if (c->draft_layers < 1 || c->draft_layers > 99) return fail(RT_ERR_INVALID, "draft_layers must be in [1, 99]");
   if (c->n_cond_layers < 1 || c->n_cond_layers > RT_MAX_COND_LAYERS)
     return fail(RT_ERR_INVALID, "n_cond_layers must be in [1, %d]", RT_MAX_COND_LAYERS);
   for (int i = 0; i < c->n_cond_layers; ++i) {

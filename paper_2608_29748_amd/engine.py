@@ -90,6 +90,12 @@ class RoundEngine:
         n = int(np.prod(shape)) * dt.itemsize
         return np.frombuffer(B.rt_debug_read(self.h, tensor_id, seq, n), dtype=dt).reshape(shape).copy()
 
+    def read_rows(self, tensor_id: int, seq: int, pos0: int, shape, dtype) -> np.ndarray:
+        """KV cache rows pos0.. of one sequence ([n][Hkv][hd])."""
+        dt = np.dtype(dtype)
+        n = int(np.prod(shape)) * dt.itemsize
+        return np.frombuffer(B.rt_debug_read_rows(self.h, tensor_id, seq, pos0, n), dtype=dt).reshape(shape).copy()
+
     def write(self, tensor_id: int, seq: int, arr: np.ndarray) -> None:
         B.rt_debug_write(self.h, tensor_id, seq, np.ascontiguousarray(arr).tobytes())
 

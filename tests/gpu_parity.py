@@ -16,6 +16,7 @@ from typing import List
 import numpy as np
 
 from oracle import OracleModel, OracleRunner
+from oracle.model import rms_norm
 from paper_2608_29748_amd import binding as B
 from paper_2608_29748_amd.engine import RoundEngine, config_from
 from workloads import weight_specs
@@ -60,6 +61,7 @@ class Report:
     near_ties: int = 0
     decisions: int = 0
     accept: List[int] = field(default_factory=list)
+    conditioned: int = 0         # sequence rounds checked with conditioned rows (cond_len > 0)
 
     p999: dict = field(default_factory=dict)
 
@@ -191,8 +193,105 @@ def inject_state(eng, st, b, wl, carried, kv=False):
             st.ctx_v[l, :st.P] = store_to_f64(eng.read(B.RT_T_DRAFT_V + l, b, shp, et), wl)
 
 
+def sync_kv_rows(eng, st, b, wl, p0, n):
+    """Copies the GPU's target and drafter-context KV rows p0..p0+n-1 of sequence b into
+    the oracle state st."""
+    s = wl.target
+    et = np.uint16 if wl.dtype == "bf16" else np.float32
+    shp = (n, s.n_kv_heads, s.head_dim)
+    for l in range(s.n_layers):
+        st.tgt_k[l, p0:p0 + n] = store_to_f64(eng.read_rows(B.RT_T_TARGET_K + l, b, p0, shp, et), wl)
+        st.tgt_v[l, p0:p0 + n] = store_to_f64(eng.read_rows(B.RT_T_TARGET_V + l, b, p0, shp, et), wl)
+    for l in range(wl.draft_layers):
+        st.ctx_k[l, p0:p0 + n] = store_to_f64(eng.read_rows(B.RT_T_DRAFT_K + l, b, p0, shp, et), wl)
+        st.ctx_v[l, p0:p0 + n] = store_to_f64(eng.read_rows(B.RT_T_DRAFT_V + l, b, p0, shp, et), wl)
+
+
+def check_stages(eng, R: OracleRunner, wl, st, b, y_hat, forced, rep, tol, target_layers, draft_layers, what):
+    """Per-stage teacher-forced check of the last round of GPU sequence b (layer trace on,
+    fp32 logits stored): every checked layer is recomputed by the oracle from the GPU's
+    own residual input (and the GPU's KV cache, which st holds for rows 0..P-1), and each
+    LM head from the GPU's own operand.  Layer outputs, block K/V, final states and
+    logits must agree within `tol` (stored values within tol plus one unit in the last
+    place), and every argmax decision whose top-2 gap exceeds `tol` exactly: no decision
+    is left to a calibrated bound.  Each comparison spans one layer or one head, so the
+    error amplification of a deep random network across layers does not enter."""
+    m, W, P = R.m, R.m.W, R.m.prec
+    s, bk, d = wl.target, wl.block_size, wl.target.hidden
+    et = np.uint16 if wl.dtype == "bf16" else np.float32
+    kd = keep_dtype(wl)
+
+    def tr(base, l):
+        return eng.read(base + l, b, (bk, d), np.float32).astype(np.float64)
+
+    # drafter: B+1 rows at P..P+B over the context cache
+    for l in draft_layers:
+        ref = m.drafter_layer(st, l, tr(B.RT_T_TRACE_DRAFT_X, l))
+        e = rep.err("stage_draft_layer", tr(B.RT_T_TRACE_DRAFT_X, l + 1), ref)
+        assert e <= tol, f"{what} drafter layer {l}: output max abs error {e}"
+    h = rms_norm(tr(B.RT_T_TRACE_DRAFT_X, wl.draft_layers), W["draft.final_norm"], m.eps)
+    g_hd = eng.read(B.RT_T_HD, b, (bk, d), kd)
+    rep.err("stage_h_draft", g_hd, P.k(h))
+    assert kept_excess(g_hd, P.k(h), tol, wl) <= 0, f"{what}: h^D from the GPU's final residual"
+    head = store_to_f64(eng.read(B.RT_T_TRACE_DRAFT_HEAD, b, (bk, d), et), wl)
+    assert rep.stored_err("stage_draft_head_in", head, P.a(h), tol, wl) <= 0, f"{what}: drafter LM-head input"
+    logits = m.lm_logits(head)
+    g_dl = eng.read(B.RT_T_DRAFT_LOGITS, b, (bk, s.vocab), np.float32)
+    e = rep.err("stage_draft_logits", g_dl[1:], logits[1:])
+    assert e <= tol, f"{what}: drafter logits from the GPU's LM-head input, max abs error {e}"
+    if not forced:
+        g_dt = eng.read(B.RT_T_DRAFT_TOKENS, b, (bk,), np.int32)
+        check_decisions(rep, logits[1:], g_dt[1:], tol, f"{what} draft (per stage)")
+    # verify: [anchor, drafts] at P..P+B, causal over the target cache
+    toks = np.array([st.anchor] + [int(t) for t in y_hat])
+    e = rep.err("stage_embed", tr(B.RT_T_TRACE_TARGET_X, 0), P.r(W.rows("embed", toks)))
+    assert e == 0.0, f"{what}: verify embedding rows differ by {e}"
+    shp = (bk, s.n_kv_heads, s.head_dim)
+    for l in target_layers:
+        ref = m.target_layer(st, l, tr(B.RT_T_TRACE_TARGET_X, l), st.P)
+        e = rep.err("stage_target_layer", tr(B.RT_T_TRACE_TARGET_X, l + 1), ref)
+        assert e <= tol, f"{what} target layer {l}: output max abs error {e}"
+        for tid, cache in ((B.RT_T_TARGET_K + l, st.tgt_k), (B.RT_T_TARGET_V + l, st.tgt_v)):
+            gkv = store_to_f64(eng.read_rows(tid, b, st.P, shp, et), wl)
+            assert rep.stored_err("stage_block_kv", gkv, cache[l, st.P:st.P + bk], tol, wl) <= 0, \
+                f"{what} target layer {l}: block K/V written at P..P+B"
+    xT = tr(B.RT_T_TRACE_TARGET_X, s.n_layers)
+    h = rms_norm(xT, W["target.final_norm"], m.eps)
+    g_ht = eng.read(B.RT_T_HT, b, (bk, d), kd)
+    rep.err("stage_h_target", g_ht, P.k(h))
+    assert kept_excess(g_ht, P.k(h), tol, wl) <= 0, f"{what}: h^T from the GPU's final residual"
+    head = store_to_f64(eng.read(B.RT_T_TRACE_VERIFY_HEAD, b, (bk, d), et), wl)
+    assert rep.stored_err("stage_verify_head_in", head, P.a(h), tol, wl) <= 0, f"{what}: verify LM-head input"
+    logits = m.lm_logits(head)
+    g_vl = eng.read(B.RT_T_VERIFY_LOGITS, b, (bk, s.vocab), np.float32)
+    e = rep.err("stage_verify_logits", g_vl, logits)
+    assert e <= tol, f"{what}: verify logits from the GPU's LM-head input, max abs error {e}"
+    g_tt = eng.read(B.RT_T_TARGET_TOKENS, b, (bk,), np.int32)
+    check_decisions(rep, logits, g_tt, tol, f"{what} verify (per stage)")
+    # captured conditioning-layer states: the storage rounding of the traced residuals
+    g = store_to_f64(eng.read(B.RT_T_G, b, (bk, len(wl.cond_layers) * d), et), wl)
+    for i, l in enumerate(wl.cond_layers):
+        e = rep.err("stage_capture", g[:, i * d:(i + 1) * d], P.a(tr(B.RT_T_TRACE_TARGET_X, l + 1)))
+        assert e == 0.0, f"{what}: captured state of layer {l} differs by {e}"
+    return g
+
+
+def check_context_rows(eng, R: OracleRunner, wl, st, b, g, P0, n, rep, tol, what):
+    """The drafter context rows P0..P0+n-1 the GPU appended, against the oracle's context
+    pathway applied to the GPU's own captured states g[:n]; then st takes the GPU's rows."""
+    s = wl.target
+    et = np.uint16 if wl.dtype == "bf16" else np.float32
+    R.m.context_append(st, g[:n], P0)
+    shp = (n, s.n_kv_heads, s.head_dim)
+    for l in range(wl.draft_layers):
+        for tid, cache in ((B.RT_T_DRAFT_K + l, st.ctx_k), (B.RT_T_DRAFT_V + l, st.ctx_v)):
+            gkv = store_to_f64(eng.read_rows(tid, b, P0, shp, et), wl)
+            assert rep.stored_err("stage_context_kv", gkv, cache[l, P0:P0 + n], tol, wl) <= 0, \
+                f"{what} drafter layer {l}: appended context K/V"
+
+
 def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forced=None, rep=None,
-                       inject=True, inject_kv=False, exact: OracleRunner = None):
+                       inject=True, inject_kv=False, exact: OracleRunner = None, stages=None):
     """Runs n_rounds GPU rounds (debug: logits stored, no graph) and checks each
     against the oracle continuing from the same decisions.  With inject, every
     round starts the oracle from the GPU's carried state, so each comparison
@@ -204,10 +303,21 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
     arithmetic on the same inputs (deep random bf16 networks sit near 2e-2 there),
     never below `tol`; the widened bound and the distance are reported.  Argmax
     decisions are then fixed only where the oracle's top-2 gap exceeds twice the
-    logit bound (otherwise where it exceeds `tol`)."""
+    logit bound (otherwise where it exceeds `tol`).
+
+    stages: per-stage checks (check_stages) with the layer trace on, a dict with the
+    target and drafter layers to recompute ("target_layers", "draft_layers"; default
+    all).  The oracle's caches then always hold the GPU's rows: all of them before the
+    first round, and the rows each round commits after it, so every layer is checked
+    on the GPU's own inputs at tolerance `tol`; the end-to-end comparison above stays
+    as an additional check."""
     s, bk, B_ = wl.target, wl.block_size, wl.B
     rep = rep or Report()
-    eng.set_debug(3)
+    eng.set_debug(11 if stages is not None else 3)
+    if stages is not None:
+        inject, inject_kv = True, True
+        t_layers = list(stages.get("target_layers", range(s.n_layers)))
+        d_layers = list(stages.get("draft_layers", range(wl.draft_layers)))
     kd = keep_dtype(wl)
     ns = len(seq_states)
     for t in range(n_rounds):
@@ -224,6 +334,7 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
                 continue
             if inject:
                 inject_state(eng, st, b, wl, carried[b], kv=inject_kv and t == 0)
+            rep.conditioned += st.cond_len > 0 and wl.cond_mode != "off"
             d = R.draft(st)
             dx = exact.draft(st) if exact is not None else None
 
@@ -256,6 +367,10 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
             else:
                 assert list(g_dt[1:]) == list(forced[t][b])
             y_hat = g_dt[1:].astype(np.int64)
+            g_cap = None
+            if stages is not None:
+                g_cap = check_stages(eng, R, wl, st, b, y_hat, forced is not None, rep, tol, t_layers, d_layers,
+                                     f"round {t} seq {b}")
             vx = exact.verify(st, y_hat) if exact is not None else None   # before the mixed verify,
             v = R.verify(st, y_hat)                                        # which rewrites rows P..P+B
             g_ht = eng.read(B.RT_T_HT, b, (bk, s.hidden), kd)
@@ -272,6 +387,9 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
             A, new = R.commit(st, y_hat, g_tt.astype(np.int64), d, v)
             assert A == acc[b], f"round {t} seq {b}: A oracle {A} gpu {acc[b]}"
             assert list(tok[b][: n_c[b]]) == new, f"round {t} seq {b}: committed {tok[b][:n_c[b]]} vs {new}"
+            if stages is not None:
+                check_context_rows(eng, R, wl, st, b, g_cap, P_before, A + 1, rep, tol, f"round {t} seq {b}")
+                sync_kv_rows(eng, st, b, wl, P_before, A + 1)
             gst = eng.read(B.RT_T_STATE, b, (8,), np.int32)
             assert gst[0] == st.P and gst[1] == st.anchor, f"state {gst} vs P {st.P} anchor {st.anchor}"
             assert gst[3] == st.cond_len and (st.cond_len == 0 or gst[2] == st.r), f"carry {gst} vs {st.r},{st.cond_len}"
@@ -279,3 +397,47 @@ def run_teacher_forced(eng, R: OracleRunner, wl, seq_states, n_rounds, tol, forc
             rep.accept.append(A)
         rep.rounds += 1
     return rep
+
+
+def planted_drafts(eng, wl, n_seqs, plan):
+    """Forced drafts with a known acceptance length per sequence.  plan[b] = k plants a
+    mismatch at block position k (A = k - 1); None gives the full greedy continuation
+    (A = B); sequences absent from plan draft token 0.  The target's greedy
+    continuation is found on the GPU: the next round is run with forced drafts and
+    undone (retained states and round state written back; the caches only hold rows
+    beyond the committed length, which the next round rewrites) until every planned
+    prefix matches the target's own verify tokens, one block position or more per
+    repeat.  Returns drafts [n_seqs][B]; the GPU is left in the state it had."""
+    bk, B_, V = wl.block_size, wl.B, wl.target.vocab
+    kd, d = keep_dtype(wl), wl.target.hidden
+    saved = [(eng.read(B.RT_T_STATE, b, (9,), np.int32), eng.read(B.RT_T_HD, b, (bk, d), kd),
+              eng.read(B.RT_T_HT, b, (bk, d), kd)) for b in range(n_seqs)]
+    need = {b: (B_ if k is None else k - 1) for b, k in plan.items()}
+    drafts = np.zeros((n_seqs, B_), np.int32)
+
+    def restore():
+        for b, (stv, hd, ht) in enumerate(saved):
+            eng.write(B.RT_T_STATE, b, stv)
+            eng.write(B.RT_T_HD, b, hd)
+            eng.write(B.RT_T_HT, b, ht)
+
+    for _ in range(B_ + 1):
+        eng.spec_round_forced(drafts)
+        done = True
+        for b, n in need.items():
+            y_t = eng.read(B.RT_T_TARGET_TOKENS, b, (bk,), np.int32)
+            A = 0
+            while A < B_ and drafts[b][A] == y_t[A]:
+                A += 1
+            if A < n:
+                drafts[b][A] = y_t[A]      # verify row A saw the continuation's first A tokens
+                done = False
+        restore()
+        if done:
+            break
+    else:
+        raise AssertionError("greedy continuations not found within B + 1 repeats")
+    for b, k in plan.items():
+        if k is not None:
+            drafts[b][k - 1] = (drafts[b][k - 1] + 1) % V
+    return drafts

@@ -3,7 +3,9 @@
 Qwen3-0.6B shape: full oracle prefill and teacher-forced rounds.  Qwen3-4B shape:
 the oracle cannot prefill 4096 tokens in test time, so the GPU's prefill is checked
 on a causal prefix (KV rows of the first tokens depend on nothing later) and the
-rounds start the oracle from the GPU's KV caches and carried state."""
+rounds start the oracle from the GPU's KV caches and carried state.  Every round is
+also checked stage by stage at 2e-2: all drafter and target layers recomputed from
+the GPU's own residual inputs, both LM heads from the GPU's own operands."""
 import time
 
 import numpy as np
@@ -34,8 +36,9 @@ def test_qwen3_06b_shape_prefill_and_rounds():
     rep = compare_prefill(eng, R, wl, prompts, states, TOL, layers=[0, 1, 13, 27], exact_states=exact)
     log(f"[0.6b] prefill max err {rep.max_err}")
     RX.m.W = R.m.W
-    rep = run_teacher_forced(eng, R, wl, states, 3, TOL, exact=RX)
+    rep = run_teacher_forced(eng, R, wl, states, 3, TOL, exact=RX, stages={})
     log(f"[0.6b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    assert rep.conditioned >= 1
     eng.close()
 
 
@@ -62,6 +65,7 @@ def test_qwen3_4b_shape_prefix_and_injected_rounds():
     st.hD_prev = np.zeros((wl.block_size, wl.target.hidden))
     st.hT_prev = np.zeros((wl.block_size, wl.target.hidden))
     RX.m.W = R.m.W                                   # share the float64 weight cache
-    rep = run_teacher_forced(eng, R, wl, [st], 2, TOL, inject_kv=True, exact=RX)
+    rep = run_teacher_forced(eng, R, wl, [st], 3, TOL, inject_kv=True, exact=RX, stages={})
     log(f"[4b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    assert rep.conditioned >= 1
     eng.close()

@@ -32,8 +32,10 @@ def _exact(wl, W, R):
 
 
 @pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5", "mini-bf16-b4",
-                                  "mini-bf16-w4096"])
+                                  "mini-bf16-w4096", "mini-bf16-b6"])
 def test_prefill_and_rounds_match_oracle(name):
+    """Prefill KV, then six rounds, each checked end to end and stage by stage (every
+    layer from the GPU's own input, both LM heads from the GPU's own operands)."""
     wl, W, prompts = _setup(name, norm_init="perturbed")
     log(f"[{name}] engine init")
     eng = engine_for(wl, W)
@@ -45,9 +47,10 @@ def test_prefill_and_rounds_match_oracle(name):
     tol = TOL[wl.dtype]
     rep = compare_prefill(eng, R, wl, prompts, states, tol)
     log(f"[{name}] prefill max err {rep.max_err}")
-    rep = run_teacher_forced(eng, R, wl, states, 6, tol, exact=_exact(wl, W, R))
+    rep = run_teacher_forced(eng, R, wl, states, 6, tol, exact=_exact(wl, W, R), stages={})
     log(f"[{name}] rounds {rep.rounds} max err {rep.max_err} p99.9 {rep.p999} "
         f"near-ties {rep.near_ties}/{rep.decisions}")
+    assert rep.conditioned > 0, "no round carried a rejected suffix"
     eng.close()
 
 

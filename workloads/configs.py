@@ -136,6 +136,16 @@ PRESETS = {
                           head_dim=128, ffn=2048),
         draft_layers=1, cond_layers=(0, 1), block_size=16, batch=4, prompt_len=(30, 90),
         new_tokens=40, seed=10),
+    # Six ragged sequences (96 round rows): every round GEMM on the mid-size kernel (q|k|v
+    # k-slab partials summed by qkv_post, deferred o / down slabs folded by the norm,
+    # fp32-operand conditioning GEMMs), batched conditioning gathers and one attention
+    # row block per sequence and KV head
+    "mini-bf16-b6": Workload(
+        name="mini-bf16-b6", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=512, n_layers=2, n_q_heads=8, n_kv_heads=2,
+                          head_dim=64, ffn=1024),
+        draft_layers=2, cond_layers=(0, 1), block_size=16, batch=6, prompt_len=(20, 200),
+        new_tokens=40, seed=12),
     # Width 4096 at batch 1 (as the Qwen3-8B shape): the LM head stages 128 KiB of
     # activations per workgroup; q and kv widths below the model width
     "mini-bf16-w4096": Workload(
