@@ -524,23 +524,25 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
         mref[t2] = mnew;
       }
       const float mr = mref[t2];
-      // P in bf16 (its rounding stays below the bf16 rounding of the stored output); the
-      // row sum takes the same rounded weights, so O / sum is their exact weighted mean
-      Frag<bf16_t> ph;
+      // P as a bf16 high part plus the bf16 rounding of its remainder (about 16
+      // significand bits), two MFMAs per tile: the weights entering O are the fp32
+      // exponentials to within 2^-16 relative, and the row sum adds the fp32 values
+      Frag<bf16_t> ph, pl;
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) ph.v[tau * 4 + e] = bf16_bits(__builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr)));
-      // the row sum adds the rounded values in order, read from the packed pairs
-      const u32x4 pw = __builtin_bit_cast(u32x4, ph.v);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        lsum[t2] += __uint_as_float(pw[q] << 16);
-        lsum[t2] += __uint_as_float(pw[q] & 0xffff0000u);
-      }
+        for (int e = 0; e < 4; ++e) {
+          const float x = __builtin_amdgcn_exp2f(fmaf(st[tau][e], sl2, -mr));
+          lsum[t2] += x;
+          const short hb = bf16_bits(x);
+          ph.v[tau * 4 + e] = hb;
+          pl.v[tau * 4 + e] = bf16_bits(x - __uint_as_float((uint32_t)(uint16_t)hb << 16));
+        }
       // O^T += V^T P^T
 #pragma unroll
       for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], ph);
+#pragma unroll
+      for (int t = 0; t < NHT; ++t) mma(o[t2][t], vf[t], pl);
     }
   }
 #pragma unroll

@@ -35,8 +35,8 @@ def test_qwen3_06b_shape_prefill_and_rounds():
     exact = [RX.prefill(p, wl.new_tokens) for p in prompts]
     rep = compare_prefill(eng, R, wl, prompts, states, TOL, layers=[0, 1, 13, 27], exact_states=exact)
     log(f"[0.6b] prefill max err {rep.max_err}")
-    RX.m.W = R.m.W
-    rep = run_teacher_forced(eng, R, wl, states, 3, TOL, exact=RX, stages={})
+    # rounds: end to end at the fixed 2e-2 (no calibrated bound at this depth) and stage by stage
+    rep = run_teacher_forced(eng, R, wl, states, 3, TOL, stages={})
     log(f"[0.6b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
     assert rep.conditioned >= 1
     eng.close()

@@ -20,11 +20,11 @@ def _setup(name, **over):
 
 
 def _exact(wl, W, R):
-    """A float64 runner sharing R's weights, for bf16 models of width >= 1024: their
-    bf16 rounding noise exceeds the fixed tolerance, so the bounds are calibrated by
-    the mixed-precision oracle's own distance from float64 arithmetic (as at the
-    measured shapes)."""
-    if wl.dtype != "bf16" or wl.target.hidden < 1024:
+    """A float64 runner sharing R's weights, for bf16 models of width >= 512: their
+    end-to-end bf16 rounding noise reaches the fixed tolerance, so the end-to-end bounds
+    are calibrated by the mixed-precision oracle's own distance from float64 arithmetic
+    (as at the measured shapes); the per-stage checks keep the fixed tolerance."""
+    if wl.dtype != "bf16" or wl.target.hidden < 512:
         return None
     RX = OracleRunner(OracleModel(wl, W, prec=Precision.for_dtype("f64")))
     RX.m.W = R.m.W
