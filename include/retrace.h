@@ -224,11 +224,13 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
 /* Debug flags: 1 = store fp32 logits of both LM heads; 2 = run rounds without
  * HIP-graph replay; 4 = split the reduction of every GEMM four ways (exercises the
  * split-K path on small models); 8 = layer trace: rounds run without graph replay and
- * keep every drafter and target layer's residual input and both LM heads' input
- * operands (RT_T_TRACE_*), so each layer can be checked on its own inputs.  Setting
- * flag 8 the first time allocates the trace buffer on the device (released by
- * rt_destroy): (draft_layers + n_layers + 2) x max_batch x block_size x hidden x 4
- * bytes plus two LM-head operands.  Returns RT_ERR_HIP if that allocation fails. */
+ * keep, for every drafter and target layer, its residual input, q, attention output,
+ * post-attention residual, post-attention norm output and SwiGLU product, and both LM
+ * heads' input operands (RT_T_TRACE_*), so each step can be checked on its own inputs.
+ * Setting flag 8 the first time allocates the trace buffer on the device (released by
+ * rt_destroy), about (draft_layers + n_layers + 2) x max_batch x block_size x
+ * (10 hidden + 4 Hq*hd + 2 ffn) bytes for bf16.  Returns RT_ERR_HIP if that
+ * allocation fails. */
 int rt_set_debug(rt_model* m, int32_t flags);
 
 /* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)
@@ -264,7 +266,18 @@ enum {
                                  (l = draft_layers: the residual entering the final norm) */
   RT_T_TRACE_TARGET_X = 600,  /* + l, l = 0..n_layers: the same for the verify pass */
   RT_T_TRACE_DRAFT_HEAD = 700,  /* drafter LM-head input (final-norm output, storage type) */
-  RT_T_TRACE_VERIFY_HEAD = 701  /* verify LM-head input (storage type) */
+  RT_T_TRACE_VERIFY_HEAD = 701, /* verify LM-head input (storage type) */
+  /* + l (drafter layer l); the same items of target layer l are at + 1000 + l: */
+  RT_T_TRACE_DRAFT_Q = 1100,    /* [block][Hq*hd] q after q-norm and RoPE (storage type) */
+  RT_T_TRACE_DRAFT_ATTN = 1200, /* [block][Hq*hd] attention output (storage type) */
+  RT_T_TRACE_DRAFT_XMID = 1300, /* [block][d] f32 residual after the attention block */
+  RT_T_TRACE_DRAFT_H2 = 1400,   /* [block][d] post-attention RMSNorm output (storage type) */
+  RT_T_TRACE_DRAFT_MLP = 1500,  /* [block][ffn] SwiGLU product silu(gate) * up (storage type) */
+  RT_T_TRACE_TARGET_Q = 2100,
+  RT_T_TRACE_TARGET_ATTN = 2200,
+  RT_T_TRACE_TARGET_XMID = 2300,
+  RT_T_TRACE_TARGET_H2 = 2400,
+  RT_T_TRACE_TARGET_MLP = 2500
 };
 /* Copies `bytes` of tensor `tensor_id` for sequence `seq` to host memory.  Reading a
  * trace tensor before flag 8 was set returns RT_ERR_STATE. */

@@ -187,14 +187,31 @@ class OracleModel:
         k = P.a(apply_rope(rms_norm(k, W[f"{pre}.k_norm"], self.eps), pos, self.theta))
         return q, k, P.a(v)
 
+    # -- the rest of a decoder layer, one storage point per step
+    def attn_out(self, q, keys, vals, q_pos, k_pos, causal: bool) -> np.ndarray:
+        """Attention output rows [n][Hq*hd], rounded to the storage type."""
+        return self.prec.a(attention(q, keys, vals, q_pos, k_pos, causal)).reshape(q.shape[0], -1)
+
+    def o_residual(self, pre: str, x, o) -> np.ndarray:
+        """Residual after the attention block: x + o W_o^T."""
+        return self.prec.r(x + o @ self.W[f"{pre}.o_proj"].T)
+
+    def mlp_input(self, pre: str, x) -> np.ndarray:
+        """Post-attention RMSNorm, rounded to the storage type."""
+        return self.prec.a(rms_norm(x, self.W[f"{pre}.post_norm"], self.eps))
+
+    def swiglu(self, pre: str, h) -> np.ndarray:
+        """SwiGLU product silu(h W_gate^T) * (h W_up^T), rounded to the storage type."""
+        W = self.W
+        return self.prec.a(silu(h @ W[f"{pre}.gate_proj"].T) * (h @ W[f"{pre}.up_proj"].T))
+
+    def down_residual(self, pre: str, x, a) -> np.ndarray:
+        """Layer output: x + a W_down^T."""
+        return self.prec.r(x + a @ self.W[f"{pre}.down_proj"].T)
+
     def _attn_mlp(self, pre: str, x, q, keys, vals, q_pos, k_pos, causal: bool):
-        W, P = self.W, self.prec
-        n = x.shape[0]
-        o = P.a(attention(q, keys, vals, q_pos, k_pos, causal)).reshape(n, -1)
-        x = P.r(x + o @ W[f"{pre}.o_proj"].T)
-        h = P.a(rms_norm(x, W[f"{pre}.post_norm"], self.eps))
-        a = P.a(silu(h @ W[f"{pre}.gate_proj"].T) * (h @ W[f"{pre}.up_proj"].T))
-        return P.r(x + a @ W[f"{pre}.down_proj"].T)
+        x = self.o_residual(pre, x, self.attn_out(q, keys, vals, q_pos, k_pos, causal))
+        return self.down_residual(pre, x, self.swiglu(pre, self.mlp_input(pre, x)))
 
     def lm_logits(self, h: np.ndarray) -> np.ndarray:
         return self.prec.a(h) @ self.W["lm_head"].T

@@ -31,6 +31,10 @@ RT_MAX_TOP_K = 64
 RT_AR_MAX_STEPS = 256
 RT_T_TARGET_K, RT_T_TARGET_V, RT_T_DRAFT_K, RT_T_DRAFT_V = 100, 200, 300, 400
 RT_T_TRACE_DRAFT_X, RT_T_TRACE_TARGET_X, RT_T_TRACE_DRAFT_HEAD, RT_T_TRACE_VERIFY_HEAD = 500, 600, 700, 701
+RT_T_TRACE_DRAFT_Q, RT_T_TRACE_DRAFT_ATTN, RT_T_TRACE_DRAFT_XMID, RT_T_TRACE_DRAFT_H2, RT_T_TRACE_DRAFT_MLP = \
+    1100, 1200, 1300, 1400, 1500
+RT_T_TRACE_TARGET_Q, RT_T_TRACE_TARGET_ATTN, RT_T_TRACE_TARGET_XMID, RT_T_TRACE_TARGET_H2, RT_T_TRACE_TARGET_MLP = \
+    2100, 2200, 2300, 2400, 2500
 (RT_K_GEMM_QKV, RT_K_GEMM_O, RT_K_GEMM_GATE_UP, RT_K_GEMM_DOWN, RT_K_GEMM_CONTEXT, RT_K_GEMM_COND,
  RT_K_ATTENTION, RT_K_ATTN_MERGE, RT_K_NORM, RT_K_QKV_POST, RT_K_LM_HEAD, RT_K_MISC) = range(12)
 RT_K_KINDS = 12

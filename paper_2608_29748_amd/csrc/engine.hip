@@ -46,31 +46,43 @@ struct EngineBase {
   hipGraphExec_t ar_gexec = nullptr;
   bool ar_mode = false;                // target-only steps ran since the last prefill
   int32_t* h_out = nullptr;      // pinned: tokens [R], n [bmax], a [bmax], first [bmax]
-  // Layer trace (test hook, debug flag 8): every layer's residual input and both LM
-  // heads' inputs of the last eager round, copied into a device buffer of its own.
-  // Slots: drafter residuals 0..LD (LD: after the last layer), target residuals
-  // LD+1 .. LD+1+L, each [R][d] f32; then the drafter and verify LM-head operands,
-  // packed as the activation buffer.
+  // Layer trace (test hook, debug flag 8): the last eager round's intermediates of every
+  // drafter and target layer, copied into a device buffer of its own.  One record per
+  // layer (drafter layers 0..LD-1, then target layers), then one per pass for the
+  // residual entering the final norm and the LM-head operand.  Items of a record: the
+  // residual input (f32 [R][d]), q after its norm and RoPE ([R][qN]), the attention
+  // output (packed operand), the residual after the attention block (f32), the
+  // post-attention norm output (packed) and the SwiGLU product (packed).
+  enum TraceItem { TI_X = 0, TI_Q, TI_ATTN, TI_XMID, TI_H2, TI_MLP, TI_COUNT };
   char* trace = nullptr;
-  size_t trace_slot_bytes = 0, trace_head_bytes = 0;
+  size_t trace_rec_bytes = 0;
+  size_t trace_item_off[TI_COUNT] = {};
+  size_t trace_item_bytes(int it) const {
+    const size_t R = (size_t)p.R, R16 = rup((size_t)p.R, 16), E = (size_t)p.esz;
+    switch (it) {
+      case TI_X: case TI_XMID: return R * p.d * 4;
+      case TI_Q: return R * p.qN * E;
+      case TI_ATTN: return R16 * p.Kp_q * E;
+      case TI_H2: return R16 * p.Kp_d * E;
+      default: return R16 * p.Kp_F * E;
+    }
+  }
   bool tracing() const { return trace && (flags & 8) && !instrumented(); }
-  int trace_copy(size_t off, const void* src, size_t bytes) {
-    if (!tracing()) return RT_OK;
-    HIPCHK(hipMemcpyAsync(trace + off, src, bytes, hipMemcpyDeviceToDevice, stream));
+  int trace_item(int rec, int it, const void* src) {
+    if (rec < 0 || !tracing()) return RT_OK;
+    HIPCHK(hipMemcpyAsync(trace + (size_t)rec * trace_rec_bytes + trace_item_off[it], src, trace_item_bytes(it),
+                          hipMemcpyDeviceToDevice, stream));
     return RT_OK;
-  }
-  int trace_x(int slot, const float* x, int rows) {
-    return trace_copy((size_t)slot * trace_slot_bytes, x, (size_t)rows * p.d * 4);
-  }
-  int trace_head(int which, const void* xa) {
-    return trace_copy((size_t)(p.LD + p.L + 2) * trace_slot_bytes + (size_t)which * trace_head_bytes, xa,
-                      trace_head_bytes);
   }
   int alloc_trace() {
     if (trace) return RT_OK;
-    trace_slot_bytes = rup((size_t)p.R * p.d * 4, 256);
-    trace_head_bytes = rup(rup((size_t)p.R, 16) * p.Kp_d * p.esz, 256);
-    HIPCHK(hipMalloc((void**)&trace, (size_t)(p.LD + p.L + 2) * trace_slot_bytes + 2 * trace_head_bytes));
+    size_t off = 0;
+    for (int it = 0; it < TI_COUNT; ++it) {
+      trace_item_off[it] = off;
+      off += rup(trace_item_bytes(it), 256);
+    }
+    trace_rec_bytes = off;
+    HIPCHK(hipMalloc((void**)&trace, (size_t)(p.LD + p.L + 2) * trace_rec_bytes));
     return RT_OK;
   }
   // profiling: an event pair around every launch, aggregated per kernel kind
@@ -155,6 +167,7 @@ struct EngineBase {
   int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int time_kernel(int kind, int reps, rt_kernel_stat* out);
   int debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0 = 0);
+  int trace_read(int id, int seq, void* dst, size_t bytes);
   int debug_write(int id, int seq, const void* src, size_t bytes);
 };
 
@@ -243,7 +256,7 @@ struct Engine : EngineBase {
     int cap_k0;                  // column offset of this layer's slot in the capture
     const int32_t* prof_ctx;     // host copy of each sequence's context length (profiling only)
     int defer;                   // o / down (<= 32 rows): k-slab partials, added by the next norm
-    int trace = -1;              // layer-trace slot of this layer's residual input (-1: none)
+    int trace = -1;              // layer-trace record of this layer (-1: none)
   };
   // partials of the last deferred residual GEMM, consumed by the next norm of x
   NormFold pend{};
@@ -288,7 +301,7 @@ struct Engine : EngineBase {
     float* x = at<float>(q.x);
     T* xa = at<T>(q.xa);
     norm_x((const T*)(lw + q.lo_in), c.M, nullptr, 0);
-    if (c.trace >= 0) CHK(trace_x(c.trace, x, c.M));   // the norm has folded any deferred partials into x
+    CHK(trace_item(c.trace, TI_X, x));   // the norm has folded any deferred partials into x
     // q|k|v on the mid-size kernel with k slabs: the slabs go to the split buffer and
     // qkv_post adds them (in slab order, as the slab epilogue would) while reading
     const int qks = qkv_slabs(c.M);
@@ -312,6 +325,7 @@ struct Engine : EngineBase {
     prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 * qks + sizeof(T)), 0);
     HIPCHK(qkv_post<T>(qp, stream));
     prof_end();
+    CHK(trace_item(c.trace, TI_Q, at<T>(q.qbuf)));
     AttnArgs a{};
     a.q = at<T>(q.qbuf); a.kcache = c.kc; a.vcache = c.vc; a.page_table = c.pt; a.max_pages = q.pages_per_seq;
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
@@ -335,11 +349,15 @@ struct Engine : EngineBase {
       HIPCHK(attention_merge<T>(a, stream));
       prof_end();
     }
+    CHK(trace_item(c.trace, TI_ATTN, at<T>(q.attn)));
     CHK(resid_gemm(RT_K_GEMM_O, c, at<T>(q.attn), 16 * q.Kp_q, lw + q.lo_o, q.Kp_q, q.qN, false));
     norm_x((const T*)(lw + q.lo_post), c.M, nullptr, 0);
+    CHK(trace_item(c.trace, TI_XMID, x));
+    CHK(trace_item(c.trace, TI_H2, xa));
     e = EpiArgs{};
     e.kind = EPI_SWIGLU; e.out_act = at<T>(q.mlp); e.ldo = 16 * q.Kp_F;
     CHK(gemm_call(RT_K_GEMM_GATE_UP, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_gu, 2 * q.F, q.Kp_d, c.M, e, q.d));
+    CHK(trace_item(c.trace, TI_MLP, at<T>(q.mlp)));
     CHK(resid_gemm(RT_K_GEMM_DOWN, c, at<T>(q.mlp), 16 * q.Kp_F, lw + q.lo_down, q.Kp_F, q.F, c.cap != nullptr));
     return RT_OK;
   }
@@ -623,8 +641,8 @@ struct Engine : EngineBase {
     }
     stage(2);
     norm_x(at<T>(q.d_final_norm), R, at<K>(q.hd_keep), q.d);
-    CHK(trace_x(q.LD, x, R));
-    CHK(trace_head(0, xa));
+    CHK(trace_item(q.LD + q.L, TI_X, x));
+    CHK(trace_item(q.LD + q.L, TI_H2, xa));
     const bool smp = sampling();
     CHK(lm_head_argmax(R, at<uint64_t>(q.dkeys), (smp || (flags & 1)) ? at<float>(q.dlogits) : nullptr));
     // sampling: the drafter's filtered distributions, drafts drawn into dtok (unless forced)
@@ -642,13 +660,13 @@ struct Engine : EngineBase {
       LayerCtx c{R, q.bk, n_seqs, kStateFields, 1, q.attn_splits, q.attn_rb, q.attn_rows, st + ST_SEQ_LEN, nullptr, pt,
                  at<T>(q.kc) + (size_t)l * q.cache_layer_elems, at<T>(q.vc) + (size_t)l * q.cache_layer_elems,
                  slot >= 0 ? at<T>(q.g) : nullptr, slot * q.d, prof_ctx.data(), 1};
-      c.trace = q.LD + 1 + l;
+      c.trace = q.LD + l;
       CHK(layer(tlayer(l), c));
     }
     stage(4);
     norm_x(at<T>(q.t_final_norm), R, at<K>(q.ht_keep), q.d);
-    CHK(trace_x(q.LD + 1 + q.L, x, R));
-    CHK(trace_head(1, xa));
+    CHK(trace_item(q.LD + q.L + 1, TI_X, x));
+    CHK(trace_item(q.LD + q.L + 1, TI_H2, xa));
     CHK(lm_head_argmax(R, at<uint64_t>(q.tkeys), (smp || (flags & 1)) ? at<float>(q.vlogits) : nullptr));
     if (smp)
       CHK(dists(at<float>(q.vlogits), R, at<int32_t>(q.dist_ids_v), at<float>(q.dist_p_v), SAMPLE_NONE, 0, nullptr));
@@ -927,31 +945,8 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0
   if (pos0 && !kv) return fail(RT_ERR_INVALID, "a first position applies to KV cache tensors only");
   size_t off = 0, cap = 0;
   const size_t bk = q.bk;
-  const bool trace_x_id = (id >= RT_T_TRACE_DRAFT_X && id <= RT_T_TRACE_DRAFT_X + q.LD) ||
-                          (id >= RT_T_TRACE_TARGET_X && id <= RT_T_TRACE_TARGET_X + q.L);
-  if (trace_x_id || id == RT_T_TRACE_DRAFT_HEAD || id == RT_T_TRACE_VERIFY_HEAD) {
-    if (!trace) return fail(RT_ERR_STATE, "the layer trace is off (debug flag 8)");
-    HIPCHK(hipStreamSynchronize(stream));
-    if (trace_x_id) {
-      const int slot = id < RT_T_TRACE_TARGET_X ? id - RT_T_TRACE_DRAFT_X : q.LD + 1 + (id - RT_T_TRACE_TARGET_X);
-      if (bytes > bk * q.d * 4) return fail(RT_ERR_INVALID, "read too large");
-      HIPCHK(hipMemcpy(dst, trace + (size_t)slot * trace_slot_bytes + (size_t)seq * bk * q.d * 4, bytes,
-                       hipMemcpyDeviceToHost));
-      return RT_OK;
-    }
-    // packed LM-head operand -> row-major [bk][d] of the storage type
-    const size_t ldg = (size_t)16 * q.Kp_d;
-    if (bytes > bk * q.d * q.esz) return fail(RT_ERR_INVALID, "read too large");
-    std::vector<char> buf(trace_head_bytes);
-    const size_t base = (size_t)(q.LD + q.L + 2) * trace_slot_bytes + (id == RT_T_TRACE_VERIFY_HEAD ? trace_head_bytes : 0);
-    HIPCHK(hipMemcpy(buf.data(), trace + base, trace_head_bytes, hipMemcpyDeviceToHost));
-    char* out = (char*)dst;
-    const size_t nrow = bytes / ((size_t)q.d * q.esz);
-    for (size_t r = 0; r < nrow; ++r)
-      for (size_t k = 0; k < (size_t)q.d; ++k)
-        memcpy(out + (r * q.d + k) * q.esz, buf.data() + pa_index((int)(seq * bk + r), (int)k, ldg) * q.esz, q.esz);
-    return RT_OK;
-  }
+  if ((id >= RT_T_TRACE_DRAFT_X && id <= RT_T_TRACE_VERIFY_HEAD) || (id >= 1100 && id < 2600))
+    return trace_read(id, seq, dst, bytes);
   switch (id) {
     case RT_T_DRAFT_LOGITS: off = q.dlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
     case RT_T_VERIFY_LOGITS: off = q.vlogits + seq * bk * q.V * 4; cap = bk * q.V * 4; break;
@@ -995,6 +990,50 @@ int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0
   if (bytes > cap) return fail(RT_ERR_INVALID, "read of %zu bytes exceeds %zu", bytes, cap);
   HIPCHK(hipStreamSynchronize(stream));
   HIPCHK(hipMemcpy(dst, ws + off, bytes, hipMemcpyDeviceToHost));
+  return RT_OK;
+}
+
+int EngineBase::trace_read(int id, int seq, void* dst, size_t bytes) {
+  const Plan& q = p;
+  if (!trace) return fail(RT_ERR_STATE, "the layer trace is off (debug flag 8)");
+  int rec = -1, it = TI_X;
+  if (id >= RT_T_TRACE_DRAFT_X && id <= RT_T_TRACE_DRAFT_X + q.LD) {
+    const int l = id - RT_T_TRACE_DRAFT_X;
+    rec = l < q.LD ? l : q.LD + q.L;
+  } else if (id >= RT_T_TRACE_TARGET_X && id <= RT_T_TRACE_TARGET_X + q.L) {
+    const int l = id - RT_T_TRACE_TARGET_X;
+    rec = l < q.L ? q.LD + l : q.LD + q.L + 1;
+  } else if (id == RT_T_TRACE_DRAFT_HEAD || id == RT_T_TRACE_VERIFY_HEAD) {
+    rec = q.LD + q.L + (id == RT_T_TRACE_VERIFY_HEAD);
+    it = TI_H2;
+  } else if (id >= 1100 && id < 2600) {
+    const int pass = id / 1000, kind = (id % 1000) / 100, l = id % 100;
+    if (kind >= 1 && kind < TI_COUNT && l < (pass == 1 ? q.LD : q.L)) {
+      rec = pass == 1 ? l : q.LD + l;
+      it = kind;
+    }
+  }
+  if (rec < 0) return fail(RT_ERR_INVALID, "unknown tensor id %d", id);
+  const size_t bk = q.bk, E = q.esz;
+  const size_t width = it == TI_Q || it == TI_ATTN ? (size_t)q.qN : it == TI_MLP ? (size_t)q.F : (size_t)q.d;
+  const size_t esz = it == TI_X || it == TI_XMID ? 4 : E;
+  if (bytes > bk * width * esz) return fail(RT_ERR_INVALID, "read of %zu bytes exceeds %zu", bytes, bk * width * esz);
+  HIPCHK(hipStreamSynchronize(stream));
+  const char* base = trace + (size_t)rec * trace_rec_bytes + trace_item_off[it];
+  if (it == TI_X || it == TI_XMID || it == TI_Q) {   // row-major [R][width]
+    HIPCHK(hipMemcpy(dst, base + (size_t)seq * bk * width * esz, bytes, hipMemcpyDeviceToHost));
+    return RT_OK;
+  }
+  // packed GEMM operand (16-row groups) -> row-major [bk][width]
+  const int Kp = it == TI_ATTN ? q.Kp_q : it == TI_MLP ? q.Kp_F : q.Kp_d;
+  const size_t ldg = (size_t)16 * Kp;
+  std::vector<char> buf(trace_item_bytes(it));
+  HIPCHK(hipMemcpy(buf.data(), base, buf.size(), hipMemcpyDeviceToHost));
+  char* out = (char*)dst;
+  const size_t nrow = bytes / (width * E);
+  for (size_t r = 0; r < nrow; ++r)
+    for (size_t k = 0; k < width; ++k)
+      memcpy(out + (r * width + k) * E, buf.data() + pa_index((int)(seq * bk + r), (int)k, ldg) * E, E);
   return RT_OK;
 }
 
