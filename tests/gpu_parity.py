@@ -62,6 +62,8 @@ class Report:
     decisions: int = 0
     accept: List[int] = field(default_factory=list)
     conditioned: int = 0         # sequence rounds checked with conditioned rows (cond_len > 0)
+    stage_decisions: int = 0     # argmax decisions checked per stage (from the GPU's LM-head operands)
+    stage_near_ties: int = 0     # of those, top-2 gap within the tolerance (GPU's choice adopted)
 
     p999: dict = field(default_factory=dict)
 
@@ -100,14 +102,19 @@ def kept_excess(g, ref, bound, wl):
     return float(np.max(np.abs(g - ref) - bound - ulp))
 
 
-def check_decisions(rep, o_logits, gpu_tok, tol, what):
+def check_decisions(rep, o_logits, gpu_tok, tol, what, stage=False):
     """Oracle argmax must equal the GPU token wherever the oracle's top-2 gap > tol."""
     o_tok = np.argmax(o_logits, axis=-1)
     gap = top2_gap(o_logits)
     for i in range(len(gpu_tok)):
-        rep.decisions += 1
+        if stage:
+            rep.stage_decisions += 1
+        else:
+            rep.decisions += 1
         if gap[i] > tol:
             assert o_tok[i] == gpu_tok[i], f"{what} row {i}: oracle {o_tok[i]} gpu {gpu_tok[i]} gap {gap[i]}"
+        elif stage:
+            rep.stage_near_ties += 1
         else:
             rep.near_ties += 1
 
@@ -313,7 +320,7 @@ def check_stages(eng, R: OracleRunner, wl, st, b, y_hat, forced, rep, tol, targe
     assert e <= tol, f"{what}: drafter logits from the GPU's LM-head input, max abs error {e}"
     if not forced:
         g_dt = eng.read(B.RT_T_DRAFT_TOKENS, b, (bk,), np.int32)
-        check_decisions(rep, logits[1:], g_dt[1:], tol, f"{what} draft (per stage)")
+        check_decisions(rep, logits[1:], g_dt[1:], tol, f"{what} draft (per stage)", stage=True)
     # verify: [anchor, drafts] at P..P+B, causal over the target cache
     toks = np.array([st.anchor] + [int(t) for t in y_hat])
     e = rep.err("stage_embed", tr(B.RT_T_TRACE_TARGET_X, 0), P.r(W.rows("embed", toks)))
@@ -335,7 +342,7 @@ def check_stages(eng, R: OracleRunner, wl, st, b, y_hat, forced, rep, tol, targe
     e = rep.err("stage_verify_logits", g_vl, logits)
     assert e <= tol, f"{what}: verify logits from the GPU's LM-head input, max abs error {e}"
     g_tt = eng.read(B.RT_T_TARGET_TOKENS, b, (bk,), np.int32)
-    check_decisions(rep, logits, g_tt, tol, f"{what} verify (per stage)")
+    check_decisions(rep, logits, g_tt, tol, f"{what} verify (per stage)", stage=True)
     # captured conditioning-layer states: the storage rounding of the traced residuals
     g = store_to_f64(eng.read(B.RT_T_G, b, (bk, len(wl.cond_layers) * d), et), wl)
     for i, l in enumerate(wl.cond_layers):

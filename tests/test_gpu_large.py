@@ -37,7 +37,7 @@ def test_qwen3_06b_shape_prefill_and_rounds():
     log(f"[0.6b] prefill max err {rep.max_err}")
     # rounds: end to end at the fixed 2e-2 (no calibrated bound at this depth) and stage by stage
     rep = run_teacher_forced(eng, R, wl, states, 3, TOL, stages={})
-    log(f"[0.6b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    log(f"[0.6b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions} ({time.time() - t0:.1f}s)")
     assert rep.conditioned >= 1
     eng.close()
 
@@ -66,6 +66,6 @@ def test_qwen3_4b_shape_prefix_and_injected_rounds():
     st.hT_prev = np.zeros((wl.block_size, wl.target.hidden))
     RX.m.W = R.m.W                                   # share the float64 weight cache
     rep = run_teacher_forced(eng, R, wl, [st], 3, TOL, inject_kv=True, exact=RX, stages={})
-    log(f"[4b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+    log(f"[4b] rounds max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions} ({time.time() - t0:.1f}s)")
     assert rep.conditioned >= 1
     eng.close()

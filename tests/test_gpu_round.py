@@ -49,7 +49,7 @@ def test_prefill_and_rounds_match_oracle(name):
     log(f"[{name}] prefill max err {rep.max_err}")
     rep = run_teacher_forced(eng, R, wl, states, 6, tol, exact=_exact(wl, W, R), stages={})
     log(f"[{name}] rounds {rep.rounds} max err {rep.max_err} p99.9 {rep.p999} "
-        f"near-ties {rep.near_ties}/{rep.decisions}")
+        f"near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions}")
     assert rep.conditioned > 0, "no round carried a rejected suffix"
     eng.close()
 
@@ -70,7 +70,7 @@ def test_ragged_batch_key_splits_match_oracle(name, lens):
     rep = compare_prefill(eng, R, wl, prompts, states, tol)
     log(f"[{name} ragged] prefill max err {rep.max_err}")
     rep = run_teacher_forced(eng, R, wl, states, 4, tol, exact=_exact(wl, W, R))
-    log(f"[{name} ragged] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}")
+    log(f"[{name} ragged] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions}")
     eng.close()
 
 
@@ -91,7 +91,7 @@ def test_ablation_conditioning_matches_oracle(name, mode):
     states = [R.prefill(p, wl.new_tokens) for p in prompts]
     assert list(first) == [st.anchor for st in states]
     rep = run_teacher_forced(eng, R, wl, states, 6, TOL[wl.dtype], exact=_exact(wl, W, R))
-    log(f"[{name} {mode}] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}")
+    log(f"[{name} {mode}] rounds {rep.rounds} max err {rep.max_err} near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions}")
     eng.close()
 
 

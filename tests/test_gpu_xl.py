@@ -8,10 +8,10 @@ nothing later).  Then four rounds of two sampled sequences, started from the GPU
 caches and carried state: two unforced rounds (the second conditions its drafts on the
 first round's rejected suffix at batch shape), a round with planted drafts (one
 sequence accepts a prefix and keeps a shorter rejected suffix, the other accepts the
-whole block and resets), and an unforced round after it.  Every round is checked end to
-end (calibrated bound) and stage by stage at 2e-2: every drafter layer and sampled target
-layers recomputed from the GPU's own inputs, both LM heads from the GPU's own operands,
-every argmax decision with a top-2 gap above 2e-2.  The oracle keeps float32 copies of
+whole block and resets), and at the 8B shape an unforced round after it.  Every round
+is checked end to end (calibrated bound) and stage by stage at 2e-2: every drafter
+layer and sampled target layers step by step from the GPU's own operands, both LM heads
+from the GPU's own operands, every argmax decision with a top-2 gap above 2e-2.  The oracle keeps float32 copies of
 the weights (exact for bf16)."""
 import time
 
@@ -35,8 +35,9 @@ def sampled_layers(wl):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("name,seqs", [("qwen3-8b-shape-b8", (0, 5)), ("qwen3-14b-shape-b16", (11, 3))])
-def test_batched_long_context_sampled(name, seqs):
+@pytest.mark.parametrize("name,seqs,after", [("qwen3-8b-shape-b8", (0, 5), True),
+                                              ("qwen3-14b-shape-b16", (11, 3), False)])
+def test_batched_long_context_sampled(name, seqs, after):
     wl = get(name)
     t0 = time.time()
     W = make_weights(wl)
@@ -79,10 +80,12 @@ def test_batched_long_context_sampled(name, seqs):
     assert a3 == [k - 1, wl.B], f"planted acceptance lengths {a3}"
     assert (int(st0[2]), int(st0[3])) == (k, wl.B - k) and int(st1[3]) == 0, (st0, st1)
     log(f"[{name}] round 3 (planted): A {a3} ({time.time() - t0:.1f}s)")
-    # round 4: seqs[0] conditioned on its shorter rejected suffix, seqs[1] on nothing
-    run_teacher_forced(eng, R, wl, states, 1, TOL, rep=rep, exact=RX, stages=stages)
+    # round 4 (8B shape; the 14B shape stops after the planted round to bound the test's
+    # time): seqs[0] conditioned on its shorter rejected suffix, seqs[1] on nothing
+    if after:
+        run_teacher_forced(eng, R, wl, states, 1, TOL, rep=rep, exact=RX, stages=stages)
     assert rep.conditioned >= 3, f"conditioned sequence rounds: {rep.conditioned}"
     assert rep.max_err["e_tilde"] > 0.0, "no conditioned row was compared"
     log(f"[{name}] seqs {seqs} 4 rounds: A {rep.accept}, conditioned {rep.conditioned}, max err {rep.max_err} "
-        f"near-ties {rep.near_ties}/{rep.decisions} ({time.time() - t0:.1f}s)")
+        f"near-ties {rep.near_ties}/{rep.decisions}, per stage {rep.stage_near_ties}/{rep.stage_decisions} ({time.time() - t0:.1f}s)")
     eng.close()
