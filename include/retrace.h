@@ -149,6 +149,24 @@ int rt_prefill(rt_model* m, int32_t n_seqs, const int32_t* prompt_lens, const in
  * round.  Blocks until the outputs are on the host. */
 int rt_spec_round(rt_model* m, int32_t* tokens, int32_t* n_committed, int32_t* accept_len);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): rt_spec_round without any
+ * allocation.  The round's kernels are enqueued on the model's stream directly (no
+ * HIP graph is instantiated); their partial results -- GEMM split partials and split-K
+ * arrival counters, residual k-slab partials, attention key-split partials -- live in a
+ * static device array of the library (128 MiB per GPU, held until the process ends)
+ * instead of the workspace; the outputs (same meaning and layout as rt_spec_round's)
+ * are copied into the caller's DEVICE buffers d_tokens[n_seqs][block_size],
+ * d_n_committed[n_seqs] and d_accept_len[n_seqs] on that stream.  Returns once the
+ * work is enqueued: the caller synchronises the stream before reading the outputs.
+ * Results equal rt_spec_round's bit for bit.  Every allocation-free round on one GPU
+ * shares that GPU's array (the split-K counters are cleared at the start of each call
+ * by a kernel), so calls that overlap on one GPU -- two models on concurrent streams --
+ * race.  Returns RT_ERR_CAPACITY when the configuration's partial results exceed the
+ * array, RT_ERR_STATE before rt_prefill or after rt_ar_steps, RT_ERR_HIP if the array's
+ * device address could not be obtained when the model was built. */
+int rt_spec_round_static(rt_model* m, int32_t* d_tokens, int32_t* d_n_committed, int32_t* d_accept_len);
+
 /* Target-only greedy decoding on the same kernels (the autoregressive baseline that
  * speculative decoding is measured against; Section 5, speedup over target-only
  * decoding).  Each of the n_steps steps (1..RT_AR_MAX_STEPS) runs the target over

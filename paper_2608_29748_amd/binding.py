@@ -45,7 +45,8 @@ RT_PROF_STAGES = 7
 
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
-           "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps", "rt_debug_read_rows"]
+           "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps", "rt_debug_read_rows",
+           "rt_spec_round_static"]
 
 
 class RetraceError(RuntimeError):
@@ -87,6 +88,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_prefill.argtypes = [P, C.c_int32, i32p, i32p, C.c_int32, i32p]
     lib.rt_spec_round.argtypes = [P, i32p, i32p, i32p]
     lib.rt_spec_round_forced.argtypes = [P, i32p, i32p, i32p, i32p]
+    lib.rt_spec_round_static.argtypes = [P, P, P, P]
     lib.rt_destroy.argtypes = [P]
     lib.rt_last_error.argtypes = []
     lib.rt_last_error.restype = C.c_char_p
@@ -97,7 +99,8 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_profile_round.argtypes = [P, C.POINTER(rt_kernel_stat), C.POINTER(C.c_double), i32p, i32p, i32p]
     lib.rt_time_kernel.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(rt_kernel_stat)]
     lib.rt_ar_steps.argtypes = [P, C.c_int32, i32p, i32p]
-    for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_destroy",
+    for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_spec_round_static",
+                 "rt_destroy",
                  "rt_set_debug", "rt_debug_read", "rt_debug_read_rows", "rt_debug_write", "rt_profile_round",
                  "rt_time_kernel", "rt_ar_steps"):
         getattr(lib, name).restype = C.c_int
@@ -165,6 +168,12 @@ def rt_spec_round(h: int, n_seqs: int, block_size: int):
     _check(_lib.rt_spec_round(C.c_void_p(h), tok.ctypes.data_as(C.POINTER(C.c_int32)),
                               n.ctypes.data_as(C.POINTER(C.c_int32)), a.ctypes.data_as(C.POINTER(C.c_int32))))
     return tok, n, a
+
+
+def rt_spec_round_static(h: int, d_tokens: int, d_n_committed: int, d_accept_len: int) -> None:
+    """The allocation-free round: outputs to device buffers (pointers), enqueued only."""
+    _check(_lib.rt_spec_round_static(C.c_void_p(h), C.c_void_p(d_tokens), C.c_void_p(d_n_committed),
+                                     C.c_void_p(d_accept_len)))
 
 
 def rt_spec_round_forced(h: int, drafts: np.ndarray, block_size: int):

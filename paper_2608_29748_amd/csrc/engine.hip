@@ -4,6 +4,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -15,6 +16,31 @@
 
 namespace rt {
 const char* last_error();
+
+// Static scratch of the allocation-free round (rt_spec_round_static): the partial
+// results of its kernels (GEMM split partials and split-K arrival counters, residual
+// k-slab partials, attention key-split partials and plan).  Each GPU the library runs
+// on holds its own copy until the process ends; host code reaches it only through the
+// device address that hipGetSymbolAddress returns for the current device (the array's
+// name is a host-side stand-in).  Every allocation-free round on a GPU shares it.
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's static scratch, looked up once per device.
+static int scratch_setup(int dev, void** out) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (dev < 0 || dev >= kMaxDevices) return fail(RT_ERR_HIP, "device %d outside the static scratch table", dev);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return fail(RT_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return RT_OK;
+}
 LaunchEvents& launch_events() {
   static thread_local LaunchEvents ev;
   return ev;
@@ -35,6 +61,16 @@ struct EngineBase {
   rt_config cfg{};
   Plan p{};
   char* ws = nullptr;
+  int device = 0;                // the GPU the model was built on
+  void* scratch_dev = nullptr;   // that GPU's static scratch (device address), or null
+  int scratch_status = RT_OK;    // why scratch_dev is null
+  // Partial-result buffers: in the workspace (part_base null), or from offset 0 of the
+  // static scratch during rt_spec_round_static.
+  char* part_base = nullptr;
+  size_t part_off(size_t ws_off, size_t static_off) const { return part_base ? static_off : ws_off; }
+  template <class X> X* pat(size_t ws_off, size_t static_off) const {
+    return reinterpret_cast<X*>((part_base ? part_base : ws) + part_off(ws_off, static_off));
+  }
   hipStream_t stream = nullptr;
   bool own_stream = false;
   int n_seqs = 0;
@@ -163,6 +199,7 @@ struct EngineBase {
   virtual int run_round(bool forced) = 0;
   virtual int run_ar_step() = 0;
   int round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, int32_t* acc);
+  int round_static(int32_t* d_tokens, int32_t* d_n_comm, int32_t* d_acc);
   int ar_steps(int n, int32_t* tokens, int32_t* n_gen);
   int profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm, int32_t* acc);
   int time_kernel(int kind, int reps, rt_kernel_stat* out);
@@ -223,7 +260,8 @@ struct Engine : EngineBase {
     if (e.kind == EPI_PARTIAL) ks = partial_slabs;
     GemmArgs a;
     a.A = A; a.lda = lda; a.a_rows = a_rows; a.B = B; a.Kp = Kp; a.ksplit = ks;
-    a.partial = at<float>(p.partial); a.counters = at<uint32_t>(p.counters); a.partial_floats = kPartialFloats;
+    a.partial = pat<float>(p.partial, p.s_partial); a.counters = pat<uint32_t>(p.counters, p.s_counters);
+    a.partial_floats = kPartialFloats;
     a.e = e;
     if (instrumented()) {
       const double Kl = (double)k_logical;
@@ -286,9 +324,10 @@ struct Engine : EngineBase {
         g.e.kind = EPI_PARTIAL; g.e.M = c.M; g.e.N = q.d;
         ks = gemm_mid_partial_slabs(g, false, kResidSplitsMax);
       }
-      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.rpart); e.ldo = q.d; e.part_stride = stride;
+      e.kind = EPI_PARTIAL; e.out_f32 = pat<float>(q.rpart, q.s_rpart); e.ldo = q.d; e.part_stride = stride;
       CHK(gemm_call(kind, A, lda, q.Mrows, false, W, q.d, Kp, c.M, e, k_logical, ks));
-      pend = NormFold{at<float>(q.rpart), ks, stride, capture ? (void*)c.cap : nullptr, 16 * q.Kp_nc, c.cap_k0};
+      pend = NormFold{pat<float>(q.rpart, q.s_rpart), ks, stride, capture ? (void*)c.cap : nullptr, 16 * q.Kp_nc,
+                      c.cap_k0};
       return RT_OK;
     }
     e.kind = EPI_RESID; e.resid = at<float>(q.x); e.ldr = q.d;
@@ -307,13 +346,14 @@ struct Engine : EngineBase {
     const int qks = qkv_slabs(c.M);
     EpiArgs e{};
     if (qks > 1) {
-      e.kind = EPI_PARTIAL; e.out_f32 = at<float>(q.partial); e.ldo = q.qkvN; e.part_stride = (size_t)c.M * q.qkvN;
+      e.kind = EPI_PARTIAL; e.out_f32 = pat<float>(q.partial, q.s_partial); e.ldo = q.qkvN;
+      e.part_stride = (size_t)c.M * q.qkvN;
     } else {
       e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
     }
     CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d, qks));
     QkvPostArgs qp{};
-    qp.src = qks > 1 ? at<float>(q.partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
+    qp.src = qks > 1 ? pat<float>(q.partial, q.s_partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
     qp.n_part = qks; qp.part_stride = (size_t)c.M * q.qkvN;
     qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
     qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv; qp.q_out = at<T>(q.qbuf); qp.ldq = q.qN;
@@ -331,7 +371,8 @@ struct Engine : EngineBase {
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.rb_rows = c.rb_rows;
-    a.opart = at<float>(q.opart); a.mlpart = at<float>(q.mlpart); a.plan = at<int32_t>(q.attn_plan);
+    a.opart = pat<float>(q.opart, q.s_opart); a.mlpart = pat<float>(q.mlpart, q.s_mlpart);
+    a.plan = pat<int32_t>(q.attn_plan, q.s_attn_plan);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
     if (instrumented()) {
       // keys read: every sequence's context plus the block, K and V, once per KV head
@@ -372,7 +413,7 @@ struct Engine : EngineBase {
       g.e.part_keys = at<uint64_t>(q.part_keys);
       const int parts = 2 * ((q.V + gemm_mid_cols(q.V, M) - 1) / gemm_mid_cols(q.V, M));
       prof_begin(RT_K_LM_HEAD, (double)q.V * q.d * sizeof(T) + (double)M * q.d * sizeof(T), 2.0 * M * q.V * q.d);
-      g.partial = at<float>(q.partial); g.partial_floats = kPartialFloats;
+      g.partial = pat<float>(q.partial, q.s_partial); g.partial_floats = kPartialFloats;
       HIPCHK(gemm_mid(g, false, stream));
       prof_end();
       prof_begin(RT_K_MISC, (double)parts * M * 8, 0);
@@ -796,6 +837,32 @@ int EngineBase::round(const int32_t* forced, int32_t* tokens, int32_t* n_comm, i
   return RT_OK;
 }
 
+// The allocation-free round: the kernels of run_round enqueued directly (no graph is
+// instantiated), their partial results in the static scratch, the outputs copied to the
+// caller's device buffers on the model's stream; no host synchronisation.
+int EngineBase::round_static(int32_t* d_tokens, int32_t* d_n_comm, int32_t* d_acc) {
+  const Plan& q = p;
+  if (q.s_total > kStaticScratchBytes)
+    return fail(RT_ERR_CAPACITY, "the configuration's partial results need %zu bytes, beyond the %zu-byte static scratch",
+                q.s_total, kStaticScratchBytes);
+  if (!prefilled) return fail(RT_ERR_STATE, "rt_spec_round_static called before rt_prefill");
+  if (ar_mode) return ar_state_error();
+  if (!d_tokens || !d_n_comm || !d_acc) return fail(RT_ERR_INVALID, "null output pointer");
+  if (!scratch_dev) return scratch_status != RT_OK ? scratch_status : fail(RT_ERR_HIP, "no static scratch on this device");
+  part_base = (char*)scratch_dev;
+  // arrival counters start at zero (a kernel, so the call can be captured into a graph)
+  fill_zero(part_base + q.s_counters, (size_t)kMaxTiles * 4, stream);
+  hipError_t he = hipGetLastError();
+  int st = he == hipSuccess ? run_round(false) : fail(RT_ERR_HIP, "fill_zero: %s", hipGetErrorString(he));
+  part_base = nullptr;
+  if (st != RT_OK) return st;
+  const size_t R = (size_t)n_seqs * q.bk;
+  HIPCHK(hipMemcpyAsync(d_tokens, ws + q.out_tok, R * 4, hipMemcpyDeviceToDevice, stream));
+  HIPCHK(hipMemcpyAsync(d_n_comm, ws + q.out_n, (size_t)n_seqs * 4, hipMemcpyDeviceToDevice, stream));
+  HIPCHK(hipMemcpyAsync(d_acc, ws + q.out_a, (size_t)n_seqs * 4, hipMemcpyDeviceToDevice, stream));
+  return RT_OK;
+}
+
 int EngineBase::profile_round(rt_kernel_stat* stats, double* stage_ms, int32_t* tokens, int32_t* n_comm,
                               int32_t* acc) {
   if (!prefilled) return fail(RT_ERR_STATE, "rt_profile_round called before rt_prefill");
@@ -1099,6 +1166,13 @@ int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_w
     e->cfg = *cfg;
     e->p = p;
     e->ws = (char*)d_workspace;
+    {
+      hipError_t de = hipGetDevice(&e->device);
+      if (de != hipSuccess) { delete e; return fail(RT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(de)); }
+      // the static scratch's device address, looked up once per device with it current
+      e->scratch_status = scratch_setup(e->device, &e->scratch_dev);
+      if (e->scratch_status != RT_OK) e->scratch_dev = nullptr;
+    }
     if (hip_stream) {
       e->stream = (hipStream_t)hip_stream;
     } else {
@@ -1161,6 +1235,15 @@ int rt_spec_round_forced(rt_model* m, const int32_t* drafts, int32_t* tokens, in
     return m->e->round(drafts, tokens, n_committed, accept_len);
   } catch (...) {
     return fail(RT_ERR_INVALID, "unexpected exception in rt_spec_round_forced");
+  }
+}
+
+int rt_spec_round_static(rt_model* m, int32_t* d_tokens, int32_t* d_n_committed, int32_t* d_accept_len) {
+  try {
+    if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
+    return m->e->round_static(d_tokens, d_n_committed, d_accept_len);
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_spec_round_static");
   }
 }
 

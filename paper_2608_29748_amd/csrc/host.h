@@ -64,7 +64,15 @@ struct Plan {
   int lm_parts;                  // upper bound of LM-head workgroups
   size_t zero_from;                      // everything from here on is zero-filled at init
   size_t total;
+  // the partial-result buffers (split partials, split-K arrival counters, residual k-slab
+  // partials, attention key-split partials and plan) laid out from offset 0, for the
+  // allocation-free round whose partial results live in the library's static scratch
+  size_t s_partial, s_counters, s_rpart, s_opart, s_mlpart, s_attn_plan, s_total;
 };
+
+// Bytes of the library's static scratch array (one per GPU), which holds the partial
+// results of rt_spec_round_static; configurations whose s_total exceeds it are refused.
+constexpr size_t kStaticScratchBytes = (size_t)128 << 20;
 
 int make_plan(const rt_config* c, Plan* p);
 

@@ -218,6 +218,18 @@ int make_plan(const rt_config* c, Plan* p) {
   q.stok = take((size_t)q.bmax * 4);
   q.topk_cand = take((size_t)q.R * ((q.V + kTopkChunk - 1) / kTopkChunk) * RT_MAX_TOP_K * 8);
   q.total = off;
+  // the same partial-result buffers, from offset 0 (static scratch)
+  {
+    size_t so = 0;
+    auto stake = [&](size_t bytes) { size_t o = so; so = rup(so + bytes, 256); return o; };
+    q.s_partial = stake(kPartialFloats * 4);
+    q.s_counters = stake((size_t)kMaxTiles * 4);
+    q.s_rpart = stake((size_t)kResidSplitsMax * q.rpart_rows * q.d * 4);
+    q.s_opart = stake(q.mlpart - q.opart);
+    q.s_mlpart = stake(q.attn_plan - q.mlpart);
+    q.s_attn_plan = stake(2 * 64 * 4);
+    q.s_total = so;
+  }
   return RT_OK;
 }
 
