@@ -113,7 +113,10 @@ def cpu_baseline(eng, wl, W, prompts, seconds: float):
     from oracle import OracleModel, OracleRunner
     from paper_2608_29748_amd import binding as B
     s = wl.target
-    model = OracleModel(wl, W)
+    # float64 copies of every weight up to the 4B shape; float32 copies (exact for bf16,
+    # widened on use) beyond, so that the 8B / 14B shapes fit in host memory
+    big = sum(v.nbytes for v in W.values()) > 12e9
+    model = OracleModel(wl, W, cache="f32" if big else True)
     R = OracleRunner(model)
     st_arr = eng.read(B.RT_T_STATE, 0, (9,), np.int32)
     P = int(st_arr[0])
@@ -181,6 +184,15 @@ def target_only(eng, wl, prompts, steps: int, spec_value: float, warmup: int = 4
             "speedup_of_speculative": spec_value / tps}
 
 
+def stream_ceiling(nbytes: int, buf) -> dict:
+    """Best plain-read time of nbytes (one kernel, 1024 or 2048 workgroups, 20 launches
+    each) on this GPU: the streaming ceiling of a single kernel of that size."""
+    from paper_2608_29748_amd import binding as B
+    n = max(16, int(nbytes) // 16 * 16)
+    us = min(B.rt_stream_read(buf.data_ptr(), n, g, 20) for g in (1024, 2048))
+    return {"bytes": n, "us": us, "GBs": n / (us * 1e-6) / 1e9}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +214,9 @@ def main():
                          "do not depend on it, attention does)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB copies (reference reading for the HBM byte counters)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="also time a plain read of each replayed kernel's bytes per launch (the single-kernel "
+                         "streaming ceiling of that size) and of 22 MB .. 1 GiB")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (a round's state is "
@@ -289,8 +304,28 @@ def main():
         (round_ms_p50, elapsed * 1e3 / args.steps)
     dom = replay[DOMINANT]
     per_launch_bytes = dom["bytes"] / dom["launches"]
+    per_launch_flops = dom["flops"] / dom["launches"]
     per_launch_us = dom["ms"] * 1e3 / dom["launches"]
-    achieved = per_launch_bytes / (per_launch_us * 1e-6) / 1e9
+    rows = wl.batch * wl.block_size
+    if rows <= 64:   # weight streaming: 16 flop/byte per 16 rows, far below the ridge
+        bound, unit, peak = "hbm", "GB/s", HBM_PEAK_GBS
+        achieved = per_launch_bytes / (per_launch_us * 1e-6) / 1e9
+    else:            # 128..512 rows: the bf16 matrix cores bound the mid-size GEMM
+        bound, unit, peak = "mfma", "TFLOP/s", BF16_PEAK_TFLOPS
+        achieved = per_launch_flops / (per_launch_us * 1e-6) / 1e12
+    stream = None
+    if args.stream_probe:
+        buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        buf.fill_(1)
+        torch.cuda.synchronize()
+        stream = {"sizes": [stream_ceiling(mb << 20, buf) for mb in (22, 32, 51, 100, 400, 1024)]}
+        for name, rec in kernels.items():
+            if "us_per_launch" in rec and rec["GB_per_launch"] * 1e9 <= (1 << 30):
+                c = stream_ceiling(rec["GB_per_launch"] * 1e9, buf)
+                rec["stream_ceiling_GBs"] = c["GBs"]
+                rec["frac_of_stream_ceiling"] = rec["achieved_GBs"] / c["GBs"]
+        del buf
+        log("stream probe: " + ", ".join(f"{r['bytes'] >> 20} MB {r['GBs']:.0f} GB/s" for r in stream["sizes"]))
     if args.copy_calibration:
         copy_calibration()
 
@@ -312,10 +347,13 @@ def main():
                    "layers": wl.target.n_layers, "draft_layers": wl.draft_layers,
                    "cond_layers": list(wl.cond_layers), "cond_mode": wl.cond_mode, "temperature": wl.temperature,
                    "top_k": wl.top_k, "top_p": wl.top_p, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": dominant_desc(wl),
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+        "roofline": {"bound": bound, "kernel": dominant_desc(wl),
+                     "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                      "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",
-                     "algorithmic_bytes_per_launch": per_launch_bytes, "us_per_launch": per_launch_us,
+                     "algorithmic_bytes_per_launch": per_launch_bytes, "algorithmic_flops_per_launch": per_launch_flops,
+                     "us_per_launch": per_launch_us,
+                     "hbm_frac": per_launch_bytes / (per_launch_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                     "mfma_frac": per_launch_flops / (per_launch_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS,
                      "launches_per_round": dom["launches"],
                      "timing": f"HIP events around {args.replay_reps} graph replays of the round's "
                                f"{dom['launches']} launches of this kernel on the library's stream"},
@@ -326,6 +364,11 @@ def main():
         "round_ms_p50": round_ms_p50,
         "prefill_s": prefill_s,
     }
+    if stream is not None:
+        out["stream_probe"] = stream
+    if wl.dtype == "f32":
+        out["roofline"]["note"] = ("cache-resident fp32 model (about 13 MB per round): rounds are latency-bound, "
+                                   "the HBM fraction is not a meaningful bound")
     if not args.no_cpu_baseline:
         try:
             out["cpu_baseline"] = cpu_baseline(eng, wl, W, prompts, args.cpu_seconds)

@@ -237,6 +237,14 @@ int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32
  * round state are not touched.  Other kinds return RT_ERR_INVALID. */
 int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat);
 
+/* The plain-read ceiling against which the round's weight-streaming kernels are
+ * compared: `reps` (1..1000) back-to-back launches of a kernel that reads the `bytes`
+ * (a positive multiple of 16, 16-byte aligned) of device buffer d_buf once with
+ * `grid` (1..65536) workgroups of 256 threads, between two HIP events on hip_stream
+ * (a hipStream_t; NULL = default stream); *us = the average duration in microseconds
+ * (one warm-up launch first).  Nothing is written.  Needs no model. */
+int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, void* hip_stream, double* us);
+
 /* ---- test hooks -------------------------------------------------------------- */
 
 /* Debug flags: 1 = store fp32 logits of both LM heads; 2 = run rounds without

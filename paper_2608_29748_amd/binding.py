@@ -46,7 +46,7 @@ RT_PROF_STAGES = 7
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
            "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps", "rt_debug_read_rows",
-           "rt_spec_round_static"]
+           "rt_spec_round_static", "rt_stream_read"]
 
 
 class RetraceError(RuntimeError):
@@ -89,6 +89,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_spec_round.argtypes = [P, i32p, i32p, i32p]
     lib.rt_spec_round_forced.argtypes = [P, i32p, i32p, i32p, i32p]
     lib.rt_spec_round_static.argtypes = [P, P, P, P]
+    lib.rt_stream_read.argtypes = [P, C.c_size_t, C.c_int32, C.c_int32, P, C.POINTER(C.c_double)]
     lib.rt_destroy.argtypes = [P]
     lib.rt_last_error.argtypes = []
     lib.rt_last_error.restype = C.c_char_p
@@ -100,7 +101,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_time_kernel.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(rt_kernel_stat)]
     lib.rt_ar_steps.argtypes = [P, C.c_int32, i32p, i32p]
     for name in ("rt_init_models", "rt_prefill", "rt_spec_round", "rt_spec_round_forced", "rt_spec_round_static",
-                 "rt_destroy",
+                 "rt_stream_read", "rt_destroy",
                  "rt_set_debug", "rt_debug_read", "rt_debug_read_rows", "rt_debug_write", "rt_profile_round",
                  "rt_time_kernel", "rt_ar_steps"):
         getattr(lib, name).restype = C.c_int
@@ -219,6 +220,13 @@ def rt_time_kernel(h: int, kind: int, reps: int) -> dict:
     st = rt_kernel_stat()
     _check(_lib.rt_time_kernel(C.c_void_p(h), kind, reps, C.byref(st)))
     return dict(kind=KERNEL_KIND_NAMES[st.kind], launches=st.launches, ms=st.ms, bytes=st.bytes, flops=st.flops)
+
+
+def rt_stream_read(ptr: int, nbytes: int, grid: int, reps: int, stream_ptr: int = 0) -> float:
+    """Average microseconds of a plain read of nbytes at device address ptr."""
+    us = C.c_double()
+    _check(_lib.rt_stream_read(C.c_void_p(ptr), nbytes, grid, reps, C.c_void_p(stream_ptr), C.byref(us)))
+    return us.value
 
 
 def rt_set_debug(h: int, flags: int) -> None:

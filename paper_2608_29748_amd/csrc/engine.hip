@@ -1277,6 +1277,36 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
   }
 }
 
+int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, void* hip_stream, double* us) {
+  try {
+    if (!d_buf || !us) return fail(RT_ERR_INVALID, "null pointer argument");
+    if (bytes < 16 || bytes % 16 || (uintptr_t)d_buf % 16) return fail(RT_ERR_INVALID, "bytes must be a positive multiple of 16 at a 16-byte aligned address");
+    if (grid < 1 || grid > 65536) return fail(RT_ERR_INVALID, "grid must be in [1, 65536]");
+    if (reps < 1 || reps > 1000) return fail(RT_ERR_INVALID, "reps must be in [1, 1000]");
+    hipStream_t s = (hipStream_t)hip_stream;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    uint32_t* sink = nullptr;
+    hipError_t e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    // the sink is never written (the kernel's test never holds); the buffer start serves
+    if (e == hipSuccess) sink = (uint32_t*)d_buf;
+    if (e == hipSuccess) { stream_read(d_buf, bytes, grid, sink, s); e = hipGetLastError(); }   // warm-up
+    if (e == hipSuccess) e = hipEventRecord(e0, s);
+    for (int r = 0; r < reps && e == hipSuccess; ++r) { stream_read(d_buf, bytes, grid, sink, s); e = hipGetLastError(); }
+    if (e == hipSuccess) e = hipEventRecord(e1, s);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (e != hipSuccess) return fail(RT_ERR_HIP, "stream read: %s", hipGetErrorString(e));
+    *us = (double)ms * 1e3 / reps;
+    return RT_OK;
+  } catch (...) {
+    return fail(RT_ERR_INVALID, "unexpected exception in rt_stream_read");
+  }
+}
+
 int rt_set_debug(rt_model* m, int32_t flags) {
   if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
   if (flags < 0 || flags > 15) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);

@@ -75,5 +75,7 @@ void set_ints(int32_t* dst, int n, int v0, int v1, int v2, int v3, hipStream_t s
 void first_token(int32_t* state, int seq, const uint64_t* keys, const int32_t* sampled, int prompt_len, int budget,
                  int32_t* first_out, hipStream_t s);
 void fill_zero(void* p, size_t bytes, hipStream_t s);
+// Plain read of bytes (a multiple of 16) at p by `grid` workgroups of 256 threads.
+void stream_read(const void* p, size_t bytes, int grid, uint32_t* sink, hipStream_t s);
 
 }  // namespace rt
