@@ -1288,7 +1288,7 @@ int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, 
     uint32_t* sink = nullptr;
     hipError_t e = hipEventCreate(&e0);
     if (e == hipSuccess) e = hipEventCreate(&e1);
-    // the sink is never written (the kernel's test never holds); the buffer start serves
+    // the sink is never written (its store is switched off at launch); the buffer serves
     if (e == hipSuccess) sink = (uint32_t*)d_buf;
     if (e == hipSuccess) { stream_read(d_buf, bytes, grid, sink, s); e = hipGetLastError(); }   // warm-up
     if (e == hipSuccess) e = hipEventRecord(e0, s);

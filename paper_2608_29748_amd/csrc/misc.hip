@@ -419,20 +419,25 @@ void fill_zero(void* p, size_t bytes, hipStream_t s) {
 }
 
 // Plain read of a buffer: every byte loaded once with 16-byte loads, four in flight per
-// lane, grid-strided; the values feed a test that never holds, so no load is dropped.
-__global__ __launch_bounds__(256) void stream_read_kernel(const uint4* __restrict__ p, size_t n16, uint32_t* sink) {
+// lane, grid-strided; the values feed a store guarded by a runtime flag (passed as 0), so
+// no load can be dropped and nothing is written.
+__global__ __launch_bounds__(256) void stream_read_kernel(const uint4* __restrict__ p, size_t n16, uint32_t* sink,
+                                                          int store) {
   uint32_t acc = 0;
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
   for (; i + 3 * stride < n16; i += 4 * stride) {
     const uint4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
-    acc ^= a.x ^ b.y ^ c.z ^ d.w;
+    acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^ (d.x ^ d.y ^ d.z ^ d.w);
   }
-  for (; i < n16; i += stride) acc ^= p[i].x;
-  if (acc == 0x9e3779b9u && threadIdx.x == 1024) sink[0] = acc;   // never true (256 threads)
+  for (; i < n16; i += stride) {
+    const uint4 a = p[i];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  if (store) sink[blockIdx.x * blockDim.x + threadIdx.x] = acc;
 }
 void stream_read(const void* p, size_t bytes, int grid, uint32_t* sink, hipStream_t s) {
-  RT_LAUNCH(stream_read_kernel, dim3((unsigned)grid), dim3(256), 0, s, (const uint4*)p, bytes / 16, sink);
+  RT_LAUNCH(stream_read_kernel, dim3((unsigned)grid), dim3(256), 0, s, (const uint4*)p, bytes / 16, sink, 0);
 }
 
 template void embed_rows<bf16_t>(const bf16_t*, int, const int32_t*, int, float*, int, hipStream_t);
