@@ -186,10 +186,11 @@ def target_only(eng, wl, prompts, steps: int, spec_value: float, warmup: int = 4
 
 def stream_ceiling(nbytes: int, buf) -> dict:
     """Best plain-read time of nbytes (one kernel, 1024 or 2048 workgroups, 20 launches
-    each) on this GPU: the streaming ceiling of a single kernel of that size."""
+    each, every launch on data the memory-side cache does not hold) on this GPU: the
+    streaming ceiling of a single kernel of that size."""
     from paper_2608_29748_amd import binding as B
     n = max(16, int(nbytes) // 16 * 16)
-    us = min(B.rt_stream_read(buf.data_ptr(), n, g, 20) for g in (1024, 2048))
+    us = min(B.rt_stream_read(buf.data_ptr(), buf.numel(), n, g, 20) for g in (1024, 2048))
     return {"bytes": n, "us": us, "GBs": n / (us * 1e-6) / 1e9}
 
 
@@ -315,7 +316,7 @@ def main():
         achieved = per_launch_flops / (per_launch_us * 1e-6) / 1e12
     stream = None
     if args.stream_probe:
-        buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
         buf.fill_(1)
         torch.cuda.synchronize()
         stream = {"sizes": [stream_ceiling(mb << 20, buf) for mb in (22, 32, 51, 100, 400, 1024)]}

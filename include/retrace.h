@@ -238,12 +238,17 @@ int rt_profile_round(rt_model* m, rt_kernel_stat* stats, double* stage_ms, int32
 int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat);
 
 /* The plain-read ceiling against which the round's weight-streaming kernels are
- * compared: `reps` (1..1000) back-to-back launches of a kernel that reads the `bytes`
- * (a positive multiple of 16, 16-byte aligned) of device buffer d_buf once with
- * `grid` (1..65536) workgroups of 256 threads, between two HIP events on hip_stream
- * (a hipStream_t; NULL = default stream); *us = the average duration in microseconds
- * (one warm-up launch first).  Nothing is written.  Needs no model. */
-int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, void* hip_stream, double* us);
+ * compared: `reps` (1..1000) back-to-back launches of a kernel that reads `bytes` (a
+ * positive multiple of 16, at most buf_bytes) of the device buffer d_buf (256-byte
+ * aligned, buf_bytes long) once, with `grid` (1..65536) workgroups of 256 threads,
+ * between two HIP events on hip_stream (a hipStream_t; NULL = default stream).
+ * Launch r reads the window starting at ((r + 1) * bytes) mod (buf_bytes - bytes + 1)
+ * rounded down to 256 bytes, so that with buf_bytes well above the 256 MB memory-side
+ * cache every launch reads data that is not cached, as the round's weight streams do.
+ * *us = the average duration in microseconds (one warm-up launch first).  Nothing is
+ * written.  Needs no model. */
+int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t grid, int32_t reps, void* hip_stream,
+                   double* us);
 
 /* ---- test hooks -------------------------------------------------------------- */
 

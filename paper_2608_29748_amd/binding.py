@@ -89,7 +89,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_spec_round.argtypes = [P, i32p, i32p, i32p]
     lib.rt_spec_round_forced.argtypes = [P, i32p, i32p, i32p, i32p]
     lib.rt_spec_round_static.argtypes = [P, P, P, P]
-    lib.rt_stream_read.argtypes = [P, C.c_size_t, C.c_int32, C.c_int32, P, C.POINTER(C.c_double)]
+    lib.rt_stream_read.argtypes = [P, C.c_size_t, C.c_size_t, C.c_int32, C.c_int32, P, C.POINTER(C.c_double)]
     lib.rt_destroy.argtypes = [P]
     lib.rt_last_error.argtypes = []
     lib.rt_last_error.restype = C.c_char_p
@@ -222,10 +222,10 @@ def rt_time_kernel(h: int, kind: int, reps: int) -> dict:
     return dict(kind=KERNEL_KIND_NAMES[st.kind], launches=st.launches, ms=st.ms, bytes=st.bytes, flops=st.flops)
 
 
-def rt_stream_read(ptr: int, nbytes: int, grid: int, reps: int, stream_ptr: int = 0) -> float:
-    """Average microseconds of a plain read of nbytes at device address ptr."""
+def rt_stream_read(ptr: int, buf_bytes: int, nbytes: int, grid: int, reps: int, stream_ptr: int = 0) -> float:
+    """Average microseconds of a plain read of nbytes, rotating over the buf_bytes at ptr."""
     us = C.c_double()
-    _check(_lib.rt_stream_read(C.c_void_p(ptr), nbytes, grid, reps, C.c_void_p(stream_ptr), C.byref(us)))
+    _check(_lib.rt_stream_read(C.c_void_p(ptr), buf_bytes, nbytes, grid, reps, C.c_void_p(stream_ptr), C.byref(us)))
     return us.value
 
 

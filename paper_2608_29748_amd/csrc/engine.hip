@@ -1277,10 +1277,13 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
   }
 }
 
-int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, void* hip_stream, double* us) {
+int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t grid, int32_t reps, void* hip_stream,
+                   double* us) {
   try {
     if (!d_buf || !us) return fail(RT_ERR_INVALID, "null pointer argument");
-    if (bytes < 16 || bytes % 16 || (uintptr_t)d_buf % 16) return fail(RT_ERR_INVALID, "bytes must be a positive multiple of 16 at a 16-byte aligned address");
+    if (bytes < 16 || bytes % 16 || (uintptr_t)d_buf % 256)
+      return fail(RT_ERR_INVALID, "bytes must be a positive multiple of 16 and the buffer 256-byte aligned");
+    if (bytes > buf_bytes) return fail(RT_ERR_INVALID, "bytes exceed the buffer");
     if (grid < 1 || grid > 65536) return fail(RT_ERR_INVALID, "grid must be in [1, 65536]");
     if (reps < 1 || reps > 1000) return fail(RT_ERR_INVALID, "reps must be in [1, 1000]");
     hipStream_t s = (hipStream_t)hip_stream;
@@ -1290,9 +1293,14 @@ int rt_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps, 
     if (e == hipSuccess) e = hipEventCreate(&e1);
     // the sink is never written (its store is switched off at launch); the buffer serves
     if (e == hipSuccess) sink = (uint32_t*)d_buf;
+    // launch r reads the window at ((r + 1) * bytes) mod (buf_bytes - bytes + 1), 256-byte
+    // aligned, so consecutive launches read different data (a window read again comes
+    // buf_bytes / bytes launches later, after the 256 MB memory-side cache has turned over)
+    const size_t span = buf_bytes - bytes + 1;
+    auto window = [&](int r) { return (const char*)d_buf + ((((size_t)r + 1) * bytes) % span & ~(size_t)255); };
     if (e == hipSuccess) { stream_read(d_buf, bytes, grid, sink, s); e = hipGetLastError(); }   // warm-up
     if (e == hipSuccess) e = hipEventRecord(e0, s);
-    for (int r = 0; r < reps && e == hipSuccess; ++r) { stream_read(d_buf, bytes, grid, sink, s); e = hipGetLastError(); }
+    for (int r = 0; r < reps && e == hipSuccess; ++r) { stream_read(window(r), bytes, grid, sink, s); e = hipGetLastError(); }
     if (e == hipSuccess) e = hipEventRecord(e1, s);
     if (e == hipSuccess) e = hipEventSynchronize(e1);
     float ms = 0.f;
