@@ -76,6 +76,14 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python paper_2608_29748_amd/build.py` "
                            "(there is no fallback path)")
+    # refuse a library built from other sources than the ones in the tree
+    from .build import STAMP, source_hash
+    stamp = path + ".sha256" if path != LIB_PATH else STAMP
+    built = open(stamp).read().strip() if os.path.exists(stamp) else None
+    if built != source_hash():
+        raise RuntimeError(f"{path} was not built from the current sources (stamp {stamp}: "
+                           f"{'missing' if built is None else 'different hash'}); rebuild it with "
+                           "`python paper_2608_29748_amd/build.py`")
     lib = C.CDLL(path)
     P = C.c_void_p
     i32p = C.POINTER(C.c_int32)

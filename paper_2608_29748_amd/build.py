@@ -35,8 +35,24 @@ def _compile(src: str) -> str:
     return obj
 
 
+STAMP = OUT + ".sha256"
+
+
+def source_hash() -> str:
+    """SHA-256 over the library's sources (kernels, host code, the C ABI header)."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".h", ".cpp")))
+    for f in files + [os.path.join("..", "..", "include", "retrace.h")]:
+        h.update(f.encode())
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
+    digest = source_hash()
     with cf.ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = OUT + ".tmp"
@@ -45,6 +61,8 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, OUT)
+    with open(STAMP, "w") as fh:     # the sources this library was built from
+        fh.write(digest + "\n")
     if verbose:
         print("built", OUT)
     return OUT

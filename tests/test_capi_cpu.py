@@ -141,3 +141,19 @@ def test_error_message_is_thread_local(B):
     t.join()
     assert "block_size" in seen["msg"]
     assert "page_size" in B.rt_last_error()
+
+
+def test_library_from_other_sources_is_refused(B, tmp_path):
+    """The binding loads only a library whose build stamp matches the tree's sources."""
+    import shutil
+    from paper_2608_29748_amd.build import source_hash
+    lib = tmp_path / "libretrace.so"
+    shutil.copy(LIB, lib)
+    (tmp_path / "libretrace.so.sha256").write_text("0" * 64 + "\n")
+    with pytest.raises(RuntimeError, match="not built from the current sources"):
+        B.load_library(str(lib))
+    (tmp_path / "libretrace.so.sha256").unlink()
+    with pytest.raises(RuntimeError, match="missing"):
+        B.load_library(str(lib))
+    (tmp_path / "libretrace.so.sha256").write_text(source_hash() + "\n")
+    assert B.load_library(str(lib)) is not None
