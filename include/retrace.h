@@ -107,11 +107,17 @@ size_t rt_workspace_bytes(const rt_config* cfg);
  * 1 + 11*n_layers + 4 + 11*draft_layers + 1 + 3, plus 5 with RT_COND_LOWRANK. */
 int32_t rt_weight_count(const rt_config* cfg);
 
+/* Elements of weight tensor `index` (0 .. rt_weight_count() - 1) in the order listed at
+ * rt_init_models, for the configuration; 0 for an invalid configuration or index. */
+int64_t rt_weight_elements(const rt_config* cfg, int32_t index);
+
 /* Builds a model in `d_workspace` (device memory, >= rt_workspace_bytes, 256-byte
  * aligned) on `hip_stream` (a hipStream_t; NULL = default stream).
  *
- * `weights` holds rt_weight_count() DEVICE pointers, each a row-major [out][in]
- * tensor of the storage type (bf16 bit patterns or float), in this order:
+ * `weights` holds rt_weight_count() pointers, each a row-major [out][in] tensor of the
+ * storage type (bf16 bit patterns or float) in device memory or in host memory
+ * (pageable or pinned; such tensors are uploaded through temporary device copies,
+ * released before the call returns), in this order:
  *   embed [V][d];
  *   per target layer: input_norm [d], q_proj [Hq*hd][d], k_proj [Hkv*hd][d],
  *     v_proj [Hkv*hd][d], q_norm [hd], k_norm [hd], o_proj [d][Hq*hd],
@@ -317,8 +323,10 @@ int rt_debug_read(rt_model* m, int32_t tensor_id, int32_t seq, void* host_dst, s
  * starting at position pos0: `bytes` covers positions pos0.. in the [pos][Hkv][hd]
  * layout.  Other tensors return RT_ERR_INVALID. */
 int rt_debug_read_rows(rt_model* m, int32_t tensor_id, int32_t seq, int32_t pos0, void* host_dst, size_t bytes);
-/* Overwrites RT_T_HD, RT_T_HT or RT_T_STATE of sequence `seq` from host memory
- * (state injection for tests). */
+/* Overwrites RT_T_HD, RT_T_HT, RT_T_STATE, or KV cache rows from position 0
+ * (RT_T_TARGET_K/V, RT_T_DRAFT_K/V + layer, [pos][Hkv][hd] storage type) of sequence
+ * `seq` from host memory (state injection for tests: a round can then start from a state
+ * computed elsewhere). */
 int rt_debug_write(rt_model* m, int32_t tensor_id, int32_t seq, const void* host_src, size_t bytes);
 
 #ifdef __cplusplus

@@ -46,7 +46,7 @@ RT_PROF_STAGES = 7
 EXPORTS = ["rt_workspace_bytes", "rt_weight_count", "rt_init_models", "rt_prefill", "rt_spec_round",
            "rt_destroy", "rt_last_error", "rt_set_debug", "rt_spec_round_forced", "rt_debug_read",
            "rt_debug_write", "rt_profile_round", "rt_time_kernel", "rt_ar_steps", "rt_debug_read_rows",
-           "rt_spec_round_static", "rt_stream_read"]
+           "rt_spec_round_static", "rt_stream_read", "rt_weight_elements"]
 
 
 class RetraceError(RuntimeError):
@@ -91,6 +91,8 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.rt_workspace_bytes.restype = C.c_size_t
     lib.rt_weight_count.argtypes = [C.POINTER(rt_config)]
     lib.rt_weight_count.restype = C.c_int32
+    lib.rt_weight_elements.argtypes = [C.POINTER(rt_config), C.c_int32]
+    lib.rt_weight_elements.restype = C.c_int64
     lib.rt_init_models.argtypes = [C.POINTER(rt_config), C.POINTER(P), C.c_int32, P, C.c_size_t, P,
                                    C.POINTER(P)]
     lib.rt_prefill.argtypes = [P, C.c_int32, i32p, i32p, C.c_int32, i32p]
@@ -150,6 +152,10 @@ def rt_workspace_bytes(cfg: rt_config) -> int:
 
 def rt_weight_count(cfg: rt_config) -> int:
     return int(_lib.rt_weight_count(C.byref(cfg)))
+
+
+def rt_weight_elements(cfg: rt_config, index: int) -> int:
+    return int(_lib.rt_weight_elements(C.byref(cfg), index))
 
 
 def rt_init_models(cfg: rt_config, weight_ptrs: Sequence[int], ws_ptr: int, ws_bytes: int,

@@ -1003,6 +1003,36 @@ static int copy_pages(const EngineBase& m, size_t cache_off, int layer, int seq,
   return RT_OK;
 }
 
+// The inverse of copy_pages: positions 0.. of one sequence's cache at `layer`, from
+// host rows [pos][Hkv][hd] (each touched page read, patched and written back).
+static int write_pages(EngineBase& m, size_t cache_off, int layer, int seq, bool vlayout, const void* src,
+                       size_t bytes) {
+  const Plan& q = m.p;
+  const size_t E = q.esz, hd = q.hd, H = q.Hkv;
+  const size_t per_pos = H * hd * E;
+  const size_t npos = bytes / per_pos;
+  if (bytes % per_pos) return fail(RT_ERR_INVALID, "write of %zu bytes is not a whole number of positions", bytes);
+  if (npos > (size_t)q.T) return fail(RT_ERR_INVALID, "write past max_seq_len");
+  std::vector<int32_t> pt((size_t)q.pages_per_seq);
+  HIPCHK(hipMemcpy(pt.data(), m.ws + q.page_table + (size_t)seq * q.pages_per_seq * 4, pt.size() * 4,
+                   hipMemcpyDeviceToHost));
+  const size_t page_bytes = H * 16 * hd * E;
+  std::vector<char> buf(page_bytes);
+  const char* in = (const char*)src;
+  for (size_t pg = 0; pg * 16 < npos; ++pg) {
+    char* dst = m.ws + cache_off + ((size_t)layer * q.cache_layer_elems) * E + (size_t)pt[pg] * page_bytes;
+    HIPCHK(hipMemcpy(buf.data(), dst, page_bytes, hipMemcpyDeviceToHost));
+    for (size_t t = 0; t < 16 && pg * 16 + t < npos; ++t)
+      for (size_t h = 0; h < H; ++h)
+        for (size_t e = 0; e < hd; ++e) {
+          const size_t di = vlayout ? ((h * hd + e) * 16 + t) : ((h * 16 + t) * hd + e);
+          memcpy(buf.data() + di * E, in + ((pg * 16 + t) * H * hd + h * hd + e) * E, E);
+        }
+    HIPCHK(hipMemcpy(dst, buf.data(), page_bytes, hipMemcpyHostToDevice));
+  }
+  return RT_OK;
+}
+
 int EngineBase::debug_read(int id, int seq, void* dst, size_t bytes, size_t pos0) {
   const Plan& q = p;
   if (!dst) return fail(RT_ERR_INVALID, "null destination");
@@ -1114,7 +1144,14 @@ int EngineBase::debug_write(int id, int seq, const void* src, size_t bytes) {
     case RT_T_HD: off = q.hd_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
     case RT_T_HT: off = q.ht_keep + seq * bk * q.d * q.ksz; cap = bk * q.d * q.ksz; break;
     case RT_T_STATE: off = q.state + (size_t)seq * kStateFields * 4; cap = kStateFields * 4; break;
-    default: return fail(RT_ERR_INVALID, "tensor id %d is not writable", id);
+    default: {
+      HIPCHK(hipStreamSynchronize(stream));
+      if (id >= RT_T_TARGET_K && id < RT_T_TARGET_K + q.L) return write_pages(*this, q.kc, id - RT_T_TARGET_K, seq, false, src, bytes);
+      if (id >= RT_T_TARGET_V && id < RT_T_TARGET_V + q.L) return write_pages(*this, q.vc, id - RT_T_TARGET_V, seq, true, src, bytes);
+      if (id >= RT_T_DRAFT_K && id < RT_T_DRAFT_K + q.LD) return write_pages(*this, q.dkc, id - RT_T_DRAFT_K, seq, false, src, bytes);
+      if (id >= RT_T_DRAFT_V && id < RT_T_DRAFT_V + q.LD) return write_pages(*this, q.dvc, id - RT_T_DRAFT_V, seq, true, src, bytes);
+      return fail(RT_ERR_INVALID, "tensor id %d is not writable", id);
+    }
   }
   if (bytes > cap) return fail(RT_ERR_INVALID, "write of %zu bytes exceeds %zu", bytes, cap);
   HIPCHK(hipStreamSynchronize(stream));
@@ -1141,6 +1178,11 @@ size_t rt_workspace_bytes(const rt_config* cfg) {
 int32_t rt_weight_count(const rt_config* cfg) {
   if (validate_config(cfg) != RT_OK) return 0;
   return weight_count(cfg);
+}
+
+int64_t rt_weight_elements(const rt_config* cfg, int32_t index) {
+  if (validate_config(cfg) != RT_OK) return 0;
+  return (int64_t)weight_elems(cfg, index);
 }
 
 int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_weights, void* d_workspace,
@@ -1182,8 +1224,44 @@ int rt_init_models(const rt_config* cfg, const void* const* weights, int32_t n_w
     }
     hipError_t he = hipHostMalloc((void**)&e->h_out, ((size_t)p.R + 3 * (size_t)p.bmax) * 4, hipHostMallocDefault);
     if (he != hipSuccess) { delete e; return fail(RT_ERR_HIP, "hipHostMalloc: %s", hipGetErrorString(he)); }
-    st = e->init(weights);
-    if (st) { delete e; return st; }
+    // weights in host memory (pageable or pinned) go through temporary device copies,
+    // released once the packing on the stream has finished
+    struct Staged {
+      std::vector<void*> b;
+      hipStream_t s = nullptr;
+      ~Staged() {
+        if (s) (void)hipStreamSynchronize(s);
+        for (void* x : b) (void)hipFree(x);
+      }
+    } staged;
+    staged.s = e->stream;
+    std::vector<const void*> wdev(weights, weights + n_weights);
+    for (int i = 0; i < n_weights; ++i) {
+      hipPointerAttribute_t at{};
+      const hipError_t pe = hipPointerGetAttributes(&at, weights[i]);
+      if (pe != hipSuccess) (void)hipGetLastError();   // unregistered host memory
+      if (pe == hipSuccess && (at.type == hipMemoryTypeDevice || at.type == hipMemoryTypeManaged)) continue;
+      const size_t bytes = weight_elems(cfg, i) * (cfg->dtype == RT_BF16 ? 2 : 4);
+      void* b = nullptr;
+      hipError_t ae = hipMalloc(&b, bytes);
+      if (ae == hipSuccess) {
+        staged.b.push_back(b);
+        ae = hipMemcpy(b, weights[i], bytes, hipMemcpyHostToDevice);
+      }
+      if (ae != hipSuccess) {
+        staged.s = nullptr;   // nothing was enqueued yet
+        delete e;
+        return fail(RT_ERR_HIP, "uploading host weight %d: %s", i, hipGetErrorString(ae));
+      }
+      wdev[i] = b;
+    }
+    st = e->init(wdev.data());
+    if (st) {
+      (void)hipStreamSynchronize(e->stream);   // packing kernels done before the copies go
+      staged.s = nullptr;
+      delete e;
+      return st;
+    }
     rt_model* m = new (std::nothrow) rt_model{e};
     if (!m) { delete e; return fail(RT_ERR_INVALID, "out of host memory"); }
     *out = m;

@@ -16,6 +16,7 @@ int fail(int code, const char* fmt, ...);   // sets the message, returns code
 
 int validate_config(const rt_config* c);
 int weight_count(const rt_config* c);
+size_t weight_elems(const rt_config* c, int i);
 
 inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

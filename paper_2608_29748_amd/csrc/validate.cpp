@@ -76,6 +76,29 @@ int weight_count(const rt_config* c) {
   return 1 + 11 * c->n_layers + 4 + 11 * c->draft_layers + 1 + 3 + (c->cond_mode == RT_COND_LOWRANK ? 5 : 0);
 }
 
+// Elements of weight tensor i in the canonical order of rt_init_models (0 if out of range).
+size_t weight_elems(const rt_config* c, int i) {
+  const size_t d = c->hidden, q = (size_t)c->n_q_heads * c->head_dim, kv = (size_t)c->n_kv_heads * c->head_dim;
+  const size_t hd = c->head_dim, F = c->ffn, V = c->vocab, nc = c->n_cond_layers;
+  // the eleven tensors of a decoder layer: input_norm, q, k, v, q_norm, k_norm, o, post_norm, gate, up, down
+  const size_t layer[11] = {d, q * d, kv * d, kv * d, hd, hd, d * q, d, F * d, F * d, d * F};
+  if (i < 0 || i >= weight_count(c)) return 0;
+  if (i == 0) return V * d;                                  // embed
+  i -= 1;
+  if (i < 11 * c->n_layers) return layer[i % 11];
+  i -= 11 * c->n_layers;
+  if (i < 4) {
+    const size_t head[4] = {d, V * d, d * nc * d, d};        // final_norm, lm_head, fc, hidden_norm
+    return head[i];
+  }
+  i -= 4;
+  if (i < 11 * c->draft_layers) return layer[i % 11];
+  i -= 11 * c->draft_layers;
+  const size_t tail[9] = {d, d * 2 * d, d * d, d * 2 * d,      // draft final_norm, W_c, W_v, W_g
+                          64 * d, 32 * 2 * d, 64 * 32, d * 64, d * 64};   // low-rank A, C_down, C_up, V, G
+  return tail[i];
+}
+
 int make_plan(const rt_config* c, Plan* p) {
   int st = validate_config(c);
   if (st) return st;

@@ -157,3 +157,24 @@ def test_library_from_other_sources_is_refused(B, tmp_path):
         B.load_library(str(lib))
     (tmp_path / "libretrace.so.sha256").write_text(source_hash() + "\n")
     assert B.load_library(str(lib)) is not None
+
+
+@pytest.mark.parametrize("name,mode", [("tiny-f32", "retrace"), ("mini-bf16-gqa5", "retrace"),
+                                       ("mini-bf16", "lowrank"), ("qwen3-14b-shape-b16", "retrace")])
+def test_weight_elements_follow_the_canonical_order(B, name, mode):
+    """rt_weight_elements gives every tensor's size in the order rt_init_models reads them."""
+    from workloads import get, weight_specs
+    import numpy as np
+    wl = get(name, cond_mode=mode)
+    c = B.make_config(vocab=wl.target.vocab, hidden=wl.target.hidden, n_layers=wl.target.n_layers,
+                      n_q_heads=wl.target.n_q_heads, n_kv_heads=wl.target.n_kv_heads, head_dim=wl.target.head_dim,
+                      ffn=wl.target.ffn, rope_theta=1e6, rms_eps=1e-6, draft_layers=wl.draft_layers,
+                      cond_layer_ids=list(wl.cond_layers), block_size=wl.block_size, mask_token_id=wl.mask_token_id,
+                      beta=1.0, cond_mode=B.COND_MODES[mode], dtype=B.RT_BF16 if wl.dtype == "bf16" else B.RT_F32,
+                      max_batch=wl.batch, max_seq_len=wl.max_seq_len, page_size=16, temperature=0.0, top_k=20,
+                      top_p=0.95, sample_seed=1)
+    specs = weight_specs(wl)
+    assert B.rt_weight_count(c) == len(specs)
+    for i, (_, shape, _) in enumerate(specs):
+        assert B.rt_weight_elements(c, i) == int(np.prod(shape)), (i, specs[i])
+    assert B.rt_weight_elements(c, len(specs)) == 0 and B.rt_weight_elements(c, -1) == 0
