@@ -267,7 +267,9 @@ int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t gr
  * Setting flag 8 the first time allocates the trace buffer on the device (released by
  * rt_destroy), about (draft_layers + n_layers + 2) x max_batch x block_size x
  * (10 hidden + 4 Hq*hd + 2 ffn) bytes for bf16.  Returns RT_ERR_HIP if that
- * allocation fails. */
+ * allocation fails.  16 = apply the q / k-norm and RoPE and write the block's K / V
+ * rows with the separate post-processing kernel in rounds and target-only steps too
+ * (by default the bf16 attention kernel does it there; both round identically). */
 int rt_set_debug(rt_model* m, int32_t flags);
 
 /* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)

@@ -23,6 +23,18 @@ struct AttnArgs {
   int32_t* plan;                 // [2][64] balanced split plan: first slot, split count per unit
   void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)
+  // Rounds (at most 16 rows per sequence, one q|k|v slab): the q / k per-head RMSNorm,
+  // RoPE and the block's K / V cache write done here instead of by qkv_post.  qkv: the
+  // fp32 q|k|v projection [row][ldqkv] (q at column 0, k at q_cols, v at q_cols + kv_cols);
+  // null: q comes from `q` and the block's K / V are already cached.  Every workgroup
+  // normalises and rotates its own q rows; the workgroups whose chunks hold the block's
+  // positions normalise and rotate the block's k rows, write k and v to the caches and
+  // into their LDS stages.  Key split 0 of each unit also stores its normalised q rows to
+  // q_out ([row][ldq], as qkv_post would).
+  const float* qkv; int ldqkv; int q_cols, kv_cols;
+  const void* q_norm; const void* k_norm;
+  const float* rope; int rope_max_pos; float eps;
+  void* q_out; int ldq;
 };
 
 // Query (token, head) rows handled by one workgroup: 64, or 96 for bf16 blocks of 65..96

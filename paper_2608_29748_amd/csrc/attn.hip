@@ -11,6 +11,11 @@
 // copies of the next chunks are in flight while the current one is used; one barrier
 // per chunk.  fp32 storage (small configurations): chunks are staged through
 // registers.
+//
+// In rounds and target-only steps (bf16, at most 16 rows per sequence) the same kernel
+// also applies the per-head q / k RMSNorm and RoPE to the fp32 q|k|v projection and
+// writes the block's K / V rows to the caches (a launch fewer per layer); it rounds
+// exactly as the separate post-processing kernel does.
 #include "attn.h"
 
 namespace rt {
@@ -326,6 +331,98 @@ typedef __attribute__((address_space(4))) const int32_t const_i32_t;
 __device__ __forceinline__ short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// v[l] + v[l ^ 32] and v[l] + v[l ^ 16] in every lane l (both lanes of a pair add the
+// same two values, so they agree bit for bit)
+__device__ __forceinline__ float xor32_sum(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float xor16_sum(float v) {
+  auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+// LDS accesses hidden from the compiler's wait insertion, which would otherwise wait
+// for every direct-to-LDS copy in flight before them (the next chunk's copies
+// included).  lds_wait() waits for them; a value read is used only after lds_wait() and
+// lds_hold() on it, and a write is followed by lds_wait() before the barrier that
+// publishes it.
+__device__ __forceinline__ u32x4 lds_ld16(const void* p) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"((const lds_void_t*)p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void lds_st16(void* p, u32x4 v) {
+  asm volatile("ds_write_b128 %0, %1" ::"v"((lds_void_t*)p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_st2(void* p, uint32_t v) {
+  asm volatile("ds_write_b16 %0, %1" ::"v"((lds_void_t*)p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// A 16-byte direct-to-LDS copy per lane (lane l writes ldst + 16 l; ldst wave-uniform)
+// the compiler does not see, so that it adds no waits for it (it waits for every such
+// copy in flight before any LDS access it cannot tell apart from the copy).  M0 (the
+// LDS address) is saved and restored around it; the caller waits with vmcnt.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, const void* ldst) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gsrc), "s"((uint32_t)(size_t)(const lds_void_t*)ldst)
+      : "memory");
+}
+__device__ __forceinline__ void lds_hold(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+// Elements ks*32 + g4*8 + e (e = 0..7, ks < NKS) of an fp32 row: the lane's share of a
+// 16-row tile in the MFMA fragment layout (g4 = lane / 16), as raw bits: x[ks][e / 4][e % 4].
+template <int NKS>
+__device__ __forceinline__ void load_frag_u(const float* row, int g4, u32x4 (&x)[NKS][2]) {
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) x[ks][hf] = *reinterpret_cast<const u32x4*>(row + ks * 32 + g4 * 8 + hf * 4);
+}
+
+// Per-head RMSNorm and rotate-half RoPE of a 16-row tile in the fragment layout (lane
+// (g4, c16) holds elements ks*32 + g4*8 + e of row c16: x as raw fp32 bits, w the bf16
+// norm weights of those elements, cs / sn the rotation factors of the pairs kp < NKS/2),
+// rounded to bf16 fragments.  The row's sum of squares is added in the order of the
+// q|k|v post-processing kernel: the pairs (l, l + hd/2), then over the bits of l from
+// the highest down, which here are the pair index kp (bit 5 at hd 128), the lane bits 5
+// and 4, and the element bits of e; so the results agree with that kernel bit for bit.
+template <int NKS>
+__device__ __forceinline__ void qk_tile(const u32x4 (&x)[NKS][2], const u32x4 (&w)[NKS], const u32x4 (&cs)[NKS / 2][2],
+                                        const u32x4 (&sn)[NKS / 2][2], float eps, Frag<bf16_t> (&out)[NKS]) {
+  constexpr int NKP = NKS / 2;
+  auto X = [&](int ks, int e) { return __uint_as_float(x[ks][e >> 2][e & 3]); };
+  auto W = [&](int ks, int e) { return __uint_as_float(((w[ks][e >> 1] >> (16 * (e & 1))) & 0xffffu) << 16); };
+  float t[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    t[e] = qk_sq(X(0, e), X(NKP, e));
+    if constexpr (NKP == 2) t[e] = t[e] + qk_sq(X(1, e), X(3, e));
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = xor32_sum(t[e]);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = xor16_sum(t[e]);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) t[e] = t[e] + t[e + 4];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) t[e] = t[e] + t[e + 2];
+  const float inv = qk_inv(t[0] + t[1], NKS * 32, eps);
+#pragma unroll
+  for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x0 = X(kp, e), x1 = X(kp + NKP, e);
+      qk_norm_rope(x0, x1, inv, W(kp, e), W(kp + NKP, e), __uint_as_float(cs[kp][e >> 2][e & 3]),
+                   __uint_as_float(sn[kp][e >> 2][e & 3]));
+      out[kp].v[e] = bf16_bits(x0);
+      out[kp + NKP].v[e] = bf16_bits(x1);
+    }
+}
+
 // XOR swizzle of the 16-byte pieces of a K row in LDS (row r of chunk page pg), so that
 // the 16 lanes reading one fragment column hit distinct banks.
 template <int NPR>
@@ -343,7 +440,7 @@ __device__ __forceinline__ int kswz(int r, int pg) { return (r ^ ((pg & 1) << 2)
 // consecutive keys 8g..8g+7 (tau = 0: 8g..8g+3, tau = 1: 8g+4..8g+7).  Those eight
 // probabilities are exactly the lane's B operand of O^T += V^T P^T, and its V^T operand
 // is one contiguous 16-byte piece of a V page row.
-template <int HD, int NSTAGE, int NRT, int NW>
+template <int HD, int NSTAGE, int NRT, int NW, bool FUSED>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int ROWB = HD * 2;                 // bytes of one K row (one token)
   constexpr int NPR = ROWB / 16;               // 16-byte pieces per K row
@@ -362,8 +459,25 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int LPC = SPREAD ? NLD : 2 * NLD;  // copies per chunk of a copying wave
   static_assert(NW % 2 == 0 && (NW == 4 || NW >= 8), "wave pairs; 4 or at least 8 waves");
   constexpr int SMEM = NSTAGE * STG > MERGE ? NSTAGE * STG : MERGE;
+  // Fused q / k post-processing: an LDS area fsm behind the stages / merge buffer holds
+  // the block's bf16 K and V rows [2][16][HD].  With eight waves (two stages) the fp32
+  // inputs are staged there too by direct-to-LDS copies: the workgroup's 64 q rows, the
+  // rotation factors of the 16 block positions, the two norm weights and the block's
+  // fp32 k and v rows; so they take one L1 pass per workgroup and the waits for them are
+  // explicit.  (One LDS array: with a second one the compiler tracks the chunk copies by
+  // object and waits for the next chunk's copies before every read of the current one.)
+  constexpr bool STAGED = FUSED && NSTAGE == 2 && NW == 8;
+  constexpr int QST = 2 * 16 * ROWB;                // q rows [64][HD] fp32 (pieces swizzled)
+  constexpr int RP = QST + 256 * HD;                // rotation factors [cos, sin][16][HD/2] fp32
+  constexpr int NWT = RP + 64 * HD;                 // norm weights [q, k][HD] bf16
+  constexpr int KVF = NWT + 4 * HD;                 // block rows [k, v][16][HD] fp32 (pieces swizzled)
+  constexpr int QFX = KVF + 128 * HD;               // normalised q fragments of key half 0 [NW/2][64][HD/2 B]
+  constexpr int FSM = STAGED ? QFX + NW / 2 * 32 * HD : 2 * 16 * ROWB;
+  static_assert(!STAGED || NRT == 1, "one query tile per wave");
   static_assert(PAGES == 4, "four 16-token pages per 64-key chunk");
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  static_assert(NW * 64 >= 32 * NPR, "one thread per 16-byte piece of the block's K and V rows");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM + (FUSED ? FSM : 0)];
+  char* const fsm = smem + SMEM;
 
   const int lane = threadIdx.x & 63, g4 = lane >> 4, c16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -422,15 +536,89 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const int nrt = min(NRT, max(0, (nrows - row0 - rh * RH + 15) / 16));   // tiles with valid rows
   Frag<bf16_t> qf[NRT][NKS];
   int qpos[NRT];
+  // Fused q / k post-processing (a.qkv set): every wave takes its q rows from the fp32
+  // projection (with the norm weights and rotation factors) and normalises them once the
+  // first chunk's copies are issued.  The workgroups whose chunks hold block positions
+  // [kb_lo, kb_hi) also take the block's k (wave 0) and v (wave 1) rows, as a 16-row
+  // tile (row c16 = block row c16); their bf16 values go to the LDS area fsm, into the
+  // stage of the chunk that holds them once its copies have landed, and to the caches at
+  // the end.  Eight waves stage these inputs in LDS (below); twelve load them directly.
+  constexpr bool fused = FUSED;   // a.qkv set (the launch selects this instance)
+  constexpr int NKP = NKS / 2;
+  u32x4 qx[NRT][NKS][2], qcs[NRT][NKP][2], qsn[NRT][NKP][2], qw[NKS];   // raw fp32 / bf16 bits
 #pragma unroll
   for (int t2 = 0; t2 < NRT; ++t2) {
     const int qrow = row0 + rh * RH + t2 * 16 + c16;
     const int r = min(qrow, nrows - 1);
     qpos[t2] = P + r / G;
     const int tok = r / G, h = kvh * G + r % G;
-    const bf16_t* qp = (const bf16_t*)a.q + (size_t)(s * a.rows_per_seq + tok) * a.n_q_heads * HD + (size_t)h * HD;
+    if constexpr (STAGED) {
+    } else if constexpr (fused) {
+      load_frag_u<NKS>(a.qkv + (size_t)(s * a.rows_per_seq + tok) * a.ldqkv + (size_t)h * HD, g4, qx[t2]);
+      const float* cs = a.rope + (size_t)qpos[t2] * (HD / 2);
+      load_frag_u<NKP>(cs, g4, qcs[t2]);
+      load_frag_u<NKP>(cs + (size_t)a.rope_max_pos * (HD / 2), g4, qsn[t2]);
+    } else {
+      const bf16_t* qp = (const bf16_t*)a.q + (size_t)(s * a.rows_per_seq + tok) * a.n_q_heads * HD + (size_t)h * HD;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].load(qp + ks * 32 + g4 * 8);
+      for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].load(qp + ks * 32 + g4 * 8);
+    }
+  }
+  const int kb_lo = max(P, c_beg * kChunk), kb_hi = fused ? min(P + a.rows_per_seq, c_end * kChunk) : kb_lo;
+  // the waves that take the block's k and v rows: staged, the key-half-1 waves 1 and 3
+  // (key half 0 of their row pair normalises the pair's q); else waves 0 and 1
+  constexpr int KW = STAGED ? 1 : 0, VW = STAGED ? 3 : 1;
+  const bool kv_wave = kb_lo < kb_hi && (w == KW || w == VW);
+  const bool q_wave = !STAGED || kh == 0;        // normalises q (staged: shares it through LDS)
+  u32x4 kx[NKS][2], kcs[NKP][2], ksn[NKP][2], kw[NKS];
+  auto load_kv = [&]() {
+    const int i = min(c16, a.rows_per_seq - 1);
+    load_frag_u<NKS>(a.qkv + (size_t)(s * a.rows_per_seq + i) * a.ldqkv + a.q_cols + (w == VW ? a.kv_cols : 0) +
+                         (size_t)kvh * HD, g4, kx);
+    if (w == KW) {
+      const float* cs = a.rope + (size_t)(P + i) * (HD / 2);
+      load_frag_u<NKP>(cs, g4, kcs);
+      load_frag_u<NKP>(cs + (size_t)a.rope_max_pos * (HD / 2), g4, ksn);
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) kw[ks] = *reinterpret_cast<const u32x4*>((const bf16_t*)a.k_norm + ks * 32 + g4 * 8);
+    }
+  };
+  if constexpr (STAGED) {
+    // q rows: piece slot ps of row rr holds the row's 16-byte piece ps ^ (rr % 16)
+    constexpr int PR = HD / 4;                      // 16-byte pieces of an fp32 row
+    constexpr int QI = 64 * PR / 64 / NW;           // copies per wave
+#pragma unroll
+    for (int j = 0; j < QI; ++j) {
+      const int slot = (w * QI + j) * 64 + lane, rr = slot / PR, ps = slot % PR;
+      const int r = min(row0 + rr, nrows - 1), tok = r / G, h = kvh * G + r % G;
+      const float* src = a.qkv + (size_t)(s * a.rows_per_seq + tok) * a.ldqkv + (size_t)h * HD + (ps ^ (rr & 15)) * 4;
+      lds_dma16(src, fsm + QST + (w * QI + j) * 1024);
+    }
+    if (w == 0 && lane < HD / 4) {                  // q-norm then k-norm weights
+      const bf16_t* src = lane < HD / 8 ? (const bf16_t*)a.q_norm + lane * 8 : (const bf16_t*)a.k_norm + (lane - HD / 8) * 8;
+      lds_dma16(src, fsm + NWT);
+    }
+    if (kb_lo < kb_hi) {                            // the block's k and v rows, same piece swizzle
+      constexpr int KI = 2 * 16 * PR / 64 / NW;
+#pragma unroll
+      for (int j = 0; j < KI; ++j) {
+        const int slot = (w * KI + j) * 64 + lane, kv = slot / (16 * PR), rr = slot / PR % 16, ps = slot % PR;
+        const float* src = a.qkv + (size_t)(s * a.rows_per_seq + min(rr, a.rows_per_seq - 1)) * a.ldqkv + a.q_cols +
+                           (kv ? a.kv_cols : 0) + (size_t)kvh * HD + (ps ^ (rr & 15)) * 4;
+        lds_dma16(src, fsm + KVF + (w * KI + j) * 1024);
+      }
+    }
+    // rotation factors of positions P .. P+15 (clamped to the table), cos rows then sin rows
+    constexpr int RI = 2 * 16 * (HD / 2) * 4 / 1024;   // copies (one per wave)
+    if (w < RI) {
+      const int slot = w * 64 + lane, tbl = slot / (16 * HD / 8), t = slot / (HD / 8) % 16, ps = slot % (HD / 8);
+      const int pos = min(P + t, a.rope_max_pos - 1);
+      const float* src = a.rope + (size_t)tbl * a.rope_max_pos * (HD / 2) + (size_t)pos * (HD / 2) + ps * 4;
+      lds_dma16(src, fsm + RP + w * 1024);
+    }
+  } else if constexpr (fused) {
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qw[ks] = *reinterpret_cast<const u32x4*>((const bf16_t*)a.q_norm + ks * 32 + g4 * 8);
   }
   const float sl2 = a.scale * 1.4426950408889634f;
   // reference max (log2 units), raised lazily.  It starts at a finite sentinel: a masked
@@ -455,6 +643,130 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     if (c_beg + i < c_end) issue(page_of(c_beg + i), i);
   int pg_next = page_of(c_beg + NSTAGE - 1);
 
+  if constexpr (STAGED) {
+    // the staged rows have landed once at most this wave's chunk copies remain; the
+    // barrier makes every wave's copies visible
+    if (c_beg < c_end) wait_vm<LPC>(); else wait_vm<0>();
+    lds_barrier();
+    auto read_rows = [&](const char* base, int rr, u32x4 (&x)[NKS][2]) {
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) x[ks][hf] = lds_ld16(base + rr * HD * 4 + (((ks * 8 + g4 * 2 + hf) ^ (rr & 15)) * 16));
+    };
+    auto read_rot = [&](int t, u32x4 (&cs)[NKP][2], u32x4 (&sn)[NKP][2]) {
+      const char* rc = fsm + RP + (t * (HD / 2) + g4 * 8) * 4;
+#pragma unroll
+      for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          cs[kp][hf] = lds_ld16(rc + (kp * 32 + hf * 4) * 4);
+          sn[kp][hf] = lds_ld16(rc + (16 * (HD / 2) + kp * 32 + hf * 4) * 4);
+        }
+    };
+    auto hold = [&](auto& arr) {
+      for (auto& v : arr) lds_hold(v);
+    };
+    if (q_wave) {
+      const char* wts = fsm + NWT;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) qw[ks] = lds_ld16(wts + (ks * 32 + g4 * 8) * 2);
+      const int rr = rh * RH + c16;
+      read_rows(fsm + QST, rr, qx[0]);
+      read_rot(min(row0 + rr, nrows - 1) / G, qcs[0], qsn[0]);
+      lds_wait();
+      hold(qw);
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) hold(qx[0][ks]);
+#pragma unroll
+      for (int kp = 0; kp < NKP; ++kp) {
+        hold(qcs[0][kp]);
+        hold(qsn[0][kp]);
+      }
+    }
+  }
+  if constexpr (fused) {
+    // (unstaged: the compiler waits here for every outstanding load, the copies just
+    // issued included: it does not order direct-to-LDS copies with other loads)
+#pragma unroll
+    for (int t2 = 0; t2 < NRT; ++t2) {
+      if (!q_wave) break;
+      qk_tile<NKS>(qx[t2], qw, qcs[t2], qsn[t2], a.eps, qf[t2]);
+      if constexpr (STAGED) {   // for the key-half-1 wave of the pair (read in the first chunk step)
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) lds_st16(fsm + QFX + (rh * 64 + lane) * (HD / 2) + ks * 16, __builtin_bit_cast(u32x4, qf[t2][ks].v));
+        lds_wait();
+      }
+      // key split 0 of the unit keeps the normalised q (one copy per row: key half 0)
+      const int qrow = row0 + rh * RH + t2 * 16 + c16;
+      if (a.q_out && split == 0 && kh == 0 && qrow < nrows) {
+        const int tok = qrow / G, h = kvh * G + qrow % G;
+        bf16_t* qo = (bf16_t*)a.q_out + (size_t)(s * a.rows_per_seq + tok) * a.ldq + (size_t)h * HD + g4 * 8;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) qf[t2][ks].store(qo + ks * 32);
+      }
+    }
+    if (kv_wave) {
+      if constexpr (STAGED) {
+        const char* wts = fsm + NWT;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            kx[ks][hf] = lds_ld16(fsm + KVF + (w == VW ? 16 * HD * 4 : 0) + c16 * HD * 4 + (((ks * 8 + g4 * 2 + hf) ^ c16) * 16));
+          }
+        if (w == KW) {
+          const char* rc = fsm + RP + (c16 * (HD / 2) + g4 * 8) * 4;
+#pragma unroll
+          for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+              kcs[kp][hf] = lds_ld16(rc + (kp * 32 + hf * 4) * 4);
+              ksn[kp][hf] = lds_ld16(rc + (16 * (HD / 2) + kp * 32 + hf * 4) * 4);
+            }
+#pragma unroll
+          for (int ks = 0; ks < NKS; ++ks) kw[ks] = lds_ld16(wts + (HD + ks * 32 + g4 * 8) * 2);
+        }
+        lds_wait();
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          lds_hold(kx[ks][0]);
+          lds_hold(kx[ks][1]);
+          lds_hold(kw[ks]);
+        }
+#pragma unroll
+        for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            lds_hold(kcs[kp][hf]);
+            lds_hold(ksn[kp][hf]);
+          }
+      } else {   // unstaged (twelve waves, 168 registers per lane): loaded once q is done
+        load_kv();
+      }
+      Frag<bf16_t> kv[NKS];
+      if (w == KW) {
+        qk_tile<NKS>(kx, kw, kcs, ksn, a.eps, kv);
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kv[ks].v[e] = bf16_bits(__uint_as_float(kx[ks][e >> 2][e & 3]));
+      }
+      char* side = fsm + (w == VW ? 16 * ROWB : 0) + c16 * ROWB + g4 * 16;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) lds_st16(side + ks * 64, __builtin_bit_cast(u32x4, kv[ks].v));
+      lds_wait();   // published by the first chunk step's barrier
+    }
+  }
+  // the block's rows in the side area: thread piece (row i, 16-byte piece p) of K (first
+  // 16 * NPR threads) or V (next 16 * NPR threads)
+  const int bt = threadIdx.x % (16 * NPR), bi = bt / NPR, bp = bt % NPR;
+  const bool b_v = threadIdx.x >= 16 * NPR, b_any = threadIdx.x < 32 * NPR;
+  const char* bside = fsm + (b_v ? 16 * ROWB : 0) + bi * ROWB + bp * 16;
+  const bool b_mine = fused && b_any && P + bi >= kb_lo && P + bi < kb_hi;   // a row this workgroup caches
+  const int b_page = b_mine ? pt[(P + bi) / kPage] : 0;
+
   for (int c = c_beg; c < c_end; ++c) {
     const int i = c - c_beg;
     // this wave's copies of chunk c have landed once at most the later chunks' remain
@@ -464,6 +776,39 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
       wait_vm<0>();
     }
     lds_barrier();   // every wave's copies of chunk c are visible; chunk c-1's stage is free
+    if (STAGED && !q_wave && c == c_beg) {   // the pair's normalised q from key half 0
+      u32x4 qr[NKS];
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) qr[ks] = lds_ld16(fsm + QFX + (rh * 64 + lane) * (HD / 2) + ks * 16);
+      lds_wait();
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        lds_hold(qr[ks]);
+        qf[0][ks].v = __builtin_bit_cast(bf16x8, qr[ks]);
+      }
+    }
+    if (fused && kb_lo < kb_hi && c * kChunk < kb_hi && (c + 1) * kChunk > kb_lo) {
+      // the block's rows in this chunk replace what the copies brought from the caches
+      // (before the next chunk's copies are issued: the wait for these LDS accesses also
+      // waits for the scalar page lookup issued with them)
+      const int pos = P + bi;
+      if (b_any && pos >= max(kb_lo, c * kChunk) && pos < min(kb_hi, (c + 1) * kChunk)) {
+        const int pg = pos / kPage - c * PAGES, r = pos % kPage;
+        char* st = smem + (i % NSTAGE) * STG + (b_v ? PAGES * PGB : 0) + pg * PGB;
+        u32x4 v = lds_ld16(bside);
+        lds_wait();
+        lds_hold(v);
+        if (!b_v) {
+          lds_st16(st + r * ROWB + (bp ^ kswz<NPR>(r, pg)) * 16, v);
+        } else {   // V^T: hd row h = bp*8 + e, token r at piece (r / 8) ^ ((h / 8) & 1)
+          char* vt = st + ((r >> 3) ^ (bp & 1)) * 16 + (r & 7) * 2;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) lds_st2(vt + (bp * 8 + e) * 32, (v[e / 2] >> (16 * (e & 1))) & 0xffff);
+        }
+        lds_wait();
+      }
+      lds_barrier();
+    }
     if (c + NSTAGE - 1 < c_end) {
       issue(pg_next, (i + NSTAGE - 1) % NSTAGE);
       pg_next = page_of(c + NSTAGE);
@@ -547,6 +892,20 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   }
 #pragma unroll
   for (int t2 = 0; t2 < NRT; ++t2) lsum[t2] = group4_sum(lsum[t2]);
+  // fused: the block's K / V rows into the caches (last, so that no wait for a chunk's
+  // copies also waits for these stores; the loop's barriers made the side area visible)
+  if (b_mine) {
+    const int tok = (P + bi) % kPage;
+    const size_t pb = ((size_t)b_page * a.n_kv_heads + kvh) * (size_t)(kPage * HD);
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(bside);
+    if (!b_v) {
+      *reinterpret_cast<bf16x8*>((bf16_t*)a.kcache + pb + (size_t)tok * HD + bp * 8) = v;
+    } else {
+      short* vc = (short*)a.vcache + pb + tok;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vc[(size_t)(bp * 8 + e) * kPage] = v[e];
+    }
+  }
 
   // merge the two key halves of each row pair of waves through LDS (stages are free
   // once every wave has passed this barrier)
@@ -683,14 +1042,21 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.splits, a.n_kv_heads, a.n_seqs * a.row_blocks);
+  // the fused q / k post-processing: bf16 kernels, blocks of at most 16 rows per sequence
+  if (a.qkv && (sizeof(T) != 2 || a.rows_per_seq > 16 || a.nq)) return hipErrorInvalidValue;
   if constexpr (sizeof(T) == 2) {
+    const bool f = a.qkv != nullptr;
     if (a.rb_rows == 96) {
-      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 12>), grid, dim3(768), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12>), grid, dim3(768), 0, s, a);
+      if (a.head_dim == 128 && f) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 12, true>), grid, dim3(768), 0, s, a);
+      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 12, false>), grid, dim3(768), 0, s, a);
+      else if (a.head_dim == 64 && f) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12, true>), grid, dim3(768), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12, false>), grid, dim3(768), 0, s, a);
       else return hipErrorInvalidValue;
     } else if (a.rb_rows == 64) {
-      if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8>), grid, dim3(512), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8>), grid, dim3(512), 0, s, a);
+      if (a.head_dim == 128 && f) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64 && f) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
       else return hipErrorInvalidValue;
     } else {
       return hipErrorInvalidValue;

@@ -144,6 +144,27 @@ __device__ __forceinline__ float group4_sum(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// q / k per-head RMSNorm and rotate-half RoPE of one element pair (x_i, x_{i + hd/2}),
+// written out operation by operation with contraction into fused multiply-adds off, so
+// that every kernel that applies them -- the q|k|v post-processing and the attention
+// kernel that takes it over in the rounds -- rounds identically.  qk_sq is a pair's
+// share of the head's sum of squares; the shares are summed over i in the butterfly
+// order of xor offsets hd/4, hd/8, .., 1.
+__device__ __forceinline__ float qk_sq(float x0, float x1) {
+#pragma clang fp contract(off)
+  return x0 * x0 + x1 * x1;
+}
+__device__ __forceinline__ float qk_inv(float ss, int hd, float eps) {
+#pragma clang fp contract(off)
+  return 1.0f / sqrtf(ss / (float)hd + eps);
+}
+__device__ __forceinline__ void qk_norm_rope(float& x0, float& x1, float inv, float w0, float w1, float cs, float sn) {
+#pragma clang fp contract(off)
+  const float a = x0 * inv * w0, b = x1 * inv * w1;
+  x0 = a * cs - b * sn;
+  x1 = b * cs + a * sn;
+}
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Workgroup barrier that orders LDS accesses for the compiler but does not wait for

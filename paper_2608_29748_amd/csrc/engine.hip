@@ -352,20 +352,27 @@ struct Engine : EngineBase {
       e.kind = EPI_STORE_F32; e.out_f32 = at<float>(q.qkvf); e.ldo = q.qkvN;
     }
     CHK(gemm_call(RT_K_GEMM_QKV, xa, 16 * q.Kp_d, q.Mrows, false, lw + q.lo_qkv, q.qkvN, q.Kp_d, c.M, e, q.d, qks));
-    QkvPostArgs qp{};
-    qp.src = qks > 1 ? pat<float>(q.partial, q.s_partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
-    qp.n_part = qks; qp.part_stride = (size_t)c.M * q.qkvN;
-    qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
-    qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv; qp.q_out = at<T>(q.qbuf); qp.ldq = q.qN;
-    qp.q_norm = lw + q.lo_qn; qp.k_norm = lw + q.lo_kn; qp.norm_layer_stride = 0;
-    qp.kcache = c.kc; qp.vcache = c.vc; qp.cache_layer_stride = 0;
-    qp.page_table = c.pt; qp.max_pages = q.pages_per_seq;
-    qp.rope = at<float>(q.rope); qp.rope_max_pos = q.T; qp.eps = cfg.rms_eps;
-    qp.rows_per_seq = c.rows_per_seq; qp.seq_stride = c.stride; qp.pos0 = c.pos0; qp.nrows = nullptr;
-    prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 * qks + sizeof(T)), 0);
-    HIPCHK(qkv_post<T>(qp, stream));
-    prof_end();
-    CHK(trace_item(c.trace, TI_Q, at<T>(q.qbuf)));
+    // Rounds and target-only steps (at most 16 rows per sequence, bf16, one q|k|v slab):
+    // the attention kernel does the q / k-norm, the rotation and the block's K / V cache
+    // write itself (debug flag 16 keeps the separate kernel)
+    const bool fuse = sizeof(T) == 2 && qks == 1 && c.nq == nullptr && c.rows_per_seq <= 16 && !(flags & 16) &&
+                      (q.hd == 64 || q.hd == 128);
+    if (!fuse) {
+      QkvPostArgs qp{};
+      qp.src = qks > 1 ? pat<float>(q.partial, q.s_partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
+      qp.n_part = qks; qp.part_stride = (size_t)c.M * q.qkvN;
+      qp.q_cols = q.qN; qp.kv_cols = q.kvN; qp.layer_cols = q.qkvN; qp.n_layers = 1;
+      qp.head_dim = q.hd; qp.n_kv_heads = q.Hkv; qp.q_out = at<T>(q.qbuf); qp.ldq = q.qN;
+      qp.q_norm = lw + q.lo_qn; qp.k_norm = lw + q.lo_kn; qp.norm_layer_stride = 0;
+      qp.kcache = c.kc; qp.vcache = c.vc; qp.cache_layer_stride = 0;
+      qp.page_table = c.pt; qp.max_pages = q.pages_per_seq;
+      qp.rope = at<float>(q.rope); qp.rope_max_pos = q.T; qp.eps = cfg.rms_eps;
+      qp.rows_per_seq = c.rows_per_seq; qp.seq_stride = c.stride; qp.pos0 = c.pos0; qp.nrows = nullptr;
+      prof_begin(RT_K_QKV_POST, (double)c.M * q.qkvN * (4 * qks + sizeof(T)), 0);
+      HIPCHK(qkv_post<T>(qp, stream));
+      prof_end();
+      CHK(trace_item(c.trace, TI_Q, at<T>(q.qbuf)));
+    }
     AttnArgs a{};
     a.q = at<T>(q.qbuf); a.kcache = c.kc; a.vcache = c.vc; a.page_table = c.pt; a.max_pages = q.pages_per_seq;
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
@@ -374,13 +381,21 @@ struct Engine : EngineBase {
     a.opart = pat<float>(q.opart, q.s_opart); a.mlpart = pat<float>(q.mlpart, q.s_mlpart);
     a.plan = pat<int32_t>(q.attn_plan, q.s_attn_plan);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
+    if (fuse) {
+      a.qkv = at<float>(q.qkvf); a.ldqkv = q.qkvN; a.q_cols = q.qN; a.kv_cols = q.kvN;
+      a.q_norm = lw + q.lo_qn; a.k_norm = lw + q.lo_kn;
+      a.rope = at<float>(q.rope); a.rope_max_pos = q.T; a.eps = cfg.rms_eps;
+      a.q_out = c.trace >= 0 ? at<T>(q.qbuf) : nullptr; a.ldq = q.qN;
+    }
     if (instrumented()) {
-      // keys read: every sequence's context plus the block, K and V, once per KV head
+      // keys read: every sequence's context plus the block, K and V, once per KV head;
+      // fused: the fp32 q|k|v rows read and the block's K / V written instead of bf16 q
       double keys = 0;
       for (int s = 0; s < c.n_seqs; ++s) keys += (double)(c.prof_ctx[s] + c.rows_per_seq);
       const double kvb = keys * 2.0 * q.Hkv * q.hd * sizeof(T);
       const double rows = (double)c.n_seqs * c.rows_per_seq;
-      prof_begin(RT_K_ATTENTION, kvb + rows * q.qN * sizeof(T) * 2, 4.0 * keys * c.rows_per_seq * q.Hq * q.hd);
+      const double qio = fuse ? rows * (q.qkvN * 4.0 + 2.0 * q.kvN * sizeof(T)) : rows * q.qN * sizeof(T);
+      prof_begin(RT_K_ATTENTION, kvb + qio + rows * q.qN * sizeof(T), 4.0 * keys * c.rows_per_seq * q.Hq * q.hd);
     }
     HIPCHK(attention_partials<T>(a, stream));
     prof_end();
@@ -390,6 +405,7 @@ struct Engine : EngineBase {
       HIPCHK(attention_merge<T>(a, stream));
       prof_end();
     }
+    if (fuse) CHK(trace_item(c.trace, TI_Q, at<T>(q.qbuf)));
     CHK(trace_item(c.trace, TI_ATTN, at<T>(q.attn)));
     CHK(resid_gemm(RT_K_GEMM_O, c, at<T>(q.attn), 16 * q.Kp_q, lw + q.lo_o, q.Kp_q, q.qN, false));
     norm_x((const T*)(lw + q.lo_post), c.M, nullptr, 0);
@@ -1395,7 +1411,7 @@ int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t gr
 
 int rt_set_debug(rt_model* m, int32_t flags) {
   if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
-  if (flags < 0 || flags > 15) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  if (flags < 0 || flags > 31) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
   if (flags & 8) {
     const int st = m->e->alloc_trace();
     if (st) return st;

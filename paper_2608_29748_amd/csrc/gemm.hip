@@ -447,17 +447,13 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(QkvPostArgs a) {
     x1 = src[lane + half];
   }
   if (region < 2) {
-    float ss = x0 * x0 + x1 * x1;
-    for (int o = half / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
-    const float inv = 1.0f / sqrtf(ss / (float)hd + a.eps);
+    float ss = qk_sq(x0, x1);
+    for (int o = half / 2; o > 0; o >>= 1) ss = ss + __shfl_xor(ss, o, 64);
+    const float inv = qk_inv(ss, hd, a.eps);
     const T* nw = (const T*)(region == 0 ? a.q_norm : a.k_norm) + (size_t)layer * a.norm_layer_stride;
-    x0 = x0 * inv * Elem<T>::to_f32(nw[lane]);
-    x1 = x1 * inv * Elem<T>::to_f32(nw[lane + half]);
     const float cs = a.rope[(size_t)pos * half + lane];
     const float sn = a.rope[(size_t)a.rope_max_pos * half + (size_t)pos * half + lane];
-    const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
-    x0 = y0;
-    x1 = y1;
+    qk_norm_rope(x0, x1, inv, Elem<T>::to_f32(nw[lane]), Elem<T>::to_f32(nw[lane + half]), cs, sn);
   }
   if (region == 0) {
     T* q = (T*)a.q_out + (size_t)m * a.ldq + (size_t)head * hd;
