@@ -143,8 +143,11 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
   const int last_tok = min(nrows, row0 + kAttnRows) - 1;
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end)
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
-  // chunks spread evenly over the splits (counts differ by at most one)
-  const int c_beg = (int)((long)split * nchunks / nsplit), c_end = (int)((long)(split + 1) * nchunks / nsplit);
+  // chunks spread evenly over the splits (counts differ by at most one); the first splits
+  // take the extra chunks, so the last one, which holds the newest keys (in rounds the
+  // block's, whose K / V it may also write), is never the longest
+  const int cq = nchunks / nsplit, cr = nchunks % nsplit;
+  const int c_beg = split * cq + min(split, cr), c_end = c_beg + cq + (split < cr ? 1 : 0);
   // page ids of this split's keys (pages past kv_end are never dereferenced)
   const int pg_beg = c_beg * PAGES;
   const int npg = max(0, min((kv_end + kPage - 1) / kPage, c_end * PAGES) - pg_beg);
@@ -495,8 +498,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const int last_tok = min(nrows, row0 + RBR) - 1;
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end), kv_end >= 1
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
-  // chunks spread evenly over the splits (counts differ by at most one)
-  const int c_beg = (int)((long)split * nchunks / nsplit), c_end = (int)((long)(split + 1) * nchunks / nsplit);
+  // chunks spread evenly over the splits (counts differ by at most one); the first splits
+  // take the extra chunks, so the last one, which holds the newest keys (in rounds the
+  // block's, whose K / V it may also write), is never the longest
+  const int cq = nchunks / nsplit, cr = nchunks % nsplit;
+  const int c_beg = split * cq + min(split, cr), c_end = c_beg + cq + (split < cr ? 1 : 0);
   const int last_page = (kv_end - 1) / kPage;
   const_i32_t* pt = (const_i32_t*)(a.page_table + (size_t)s * a.max_pages);
   // page w of chunk c (pages past kv_end are replaced by the last valid one, so every

@@ -249,6 +249,109 @@ __global__ __launch_bounds__(NW * 64) void gemm16_kernel(GemmArgs a) {
   run_epilogue<T, ROWS, COLS, LDT, NW * 64>(a.e, tile, m0, n0);
 }
 
+// ------------------------------------------------------------------ k-slab partials, A in LDS
+// Split reductions of at most 32 rows (bf16; the o and down projections of a round): grid
+// (G, 1, slabs).  Workgroup (g, z) copies the A rows of k slab z into LDS once and computes
+// the slab's partial tiles of column tiles g, g + G, g + 2G, ..: TP of them at a time, each
+// by KW waves over consecutive k ranges of the slab, summed in wave order through LDS.  So
+// A crosses from L2 into a compute unit once per slab instead of once per column tile.
+template <int MT, int KTSMAX, int U>
+__global__ __launch_bounds__(1024) void gemm16_slab_kernel(GemmArgs a, int tp_n, int kw_n) {
+  constexpr int ROWS = MT * 16;
+  __shared__ __attribute__((aligned(1024))) char sa[MT * KTSMAX * 1024];
+  __shared__ float red[16][ROWS][16];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nw = blockDim.x >> 6;
+  const int KT = a.Kp / kTileK;
+  const int z = blockIdx.z, S = gridDim.z;
+  const int kb = KT * z / S, ke = KT * (z + 1) / S, kts = ke - kb;
+  // the slab's A fragments (16-row group mt, k tile kb + j at sa + (mt * KTSMAX + j) KiB)
+  const int max_group = (a.a_rows - 1) >> 4;
+  for (int c = w; c < MT * kts; c += nw) {
+    const int mt = c / kts, j = c % kts;
+    const int grp = mt < max_group ? mt : max_group;
+    const char* src = (const char*)a.A + ((size_t)grp * a.lda + (size_t)(kb + j) * 512) * 2 + lane * 16;
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void_t*)(sa + (mt * KTSMAX + j) * 1024), 16, 0, 0);
+  }
+  const int tp = w / kw_n, kw = w % kw_n;
+  const int n_tiles = (a.e.N + 15) / 16, n_valid = a.e.N / kTileN;
+  const int k0 = kb + kts * kw / kw_n, k1 = kb + kts * (kw + 1) / kw_n;
+  bool first = true;
+  for (int base = blockIdx.x; base < n_tiles; base += gridDim.x * tp_n) {
+    const int t = base + tp * gridDim.x;            // this wave's column tile
+    f32x4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (tp < tp_n && t < n_tiles && k0 < k1) {
+      const bf16_t* bptr = (const bf16_t*)a.B + ((size_t)(t < n_valid ? t : 0) * KT) * 512 + lane * 8;
+      for (int kt = k0; kt < k1; kt += U) {
+        Frag<bf16_t> bf[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) bf[u].load(bptr + (size_t)(kt + u < k1 ? kt + u : k1 - 1) * 512);
+        __builtin_amdgcn_sched_barrier(0);   // all U weight tiles in flight before the MFMAs
+        if (first) {   // the A copies have landed once at most the U weight loads remain
+          wait_vm<U>();
+          lds_barrier();
+          first = false;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (kt + u < k1) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+              Frag<bf16_t> af;
+              af.v = *reinterpret_cast<const bf16x8*>(sa + (mt * KTSMAX + kt + u - kb) * 1024 + lane * 16);
+              mma(acc[mt], af, bf[u]);
+            }
+          }
+      }
+    }
+    if (first) {       // waves without work still wait for the shared copies
+      wait_vm<0>();
+      lds_barrier();
+      first = false;
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * (lane / 16) + i][lane % 16] = acc[mt][i];
+    __syncthreads();
+    // tile group g2 sums its KW k ranges in order
+    for (int idx = threadIdx.x; idx < tp_n * ROWS * 16; idx += blockDim.x) {
+      const int g2 = idx / (ROWS * 16), r = idx / 16 % ROWS, c = idx % 16;
+      const int tt = base + g2 * gridDim.x, m = r, n = tt * 16 + c;
+      if (tt >= n_tiles || m >= a.e.M || n >= a.e.N) continue;
+      float sum = 0.f;
+      for (int v = 0; v < kw_n; ++v) sum += red[g2 * kw_n + v][r][c];
+      a.e.out_f32[(size_t)z * a.e.part_stride + (size_t)m * a.e.ldo + n] = sum;
+    }
+    __syncthreads();
+  }
+  if (first) wait_vm<0>();   // no tile at all: leave no copy in flight
+}
+
+// Launch parameters of gemm16_slab_kernel for M rows, N columns and a padded K with `slabs`
+// k slabs: workgroups per slab (so that about 256 run), column tiles in flight per
+// workgroup and waves per tile (16 at most in all); false if the slab's A rows do not fit.
+struct SlabPlan { int G, tp, kw; };
+static bool slab_plan(int M, int N, int Kp, int slabs, SlabPlan* sp) {
+  const int MT = M > 16 ? 2 : 1, KT = Kp / kTileK, n_tiles = (N + 15) / 16;
+  const int kts = (KT + slabs - 1) / slabs;
+  if (M > 32 || kts > (MT == 1 ? 80 : 48) || slabs < 1 || KT < slabs) return false;
+  int G = 256 / slabs;
+  if (G > n_tiles) G = n_tiles;
+  if (G < 1) G = 1;
+  const int per = (n_tiles + G - 1) / G;          // column tiles of the busiest workgroup
+  int tp = per < 16 ? per : 16;
+  int kw = 16 / tp;                                 // waves per tile: enough for ~8 k tiles each
+  const int want = (kts + 7) / 8;
+  if (kw > want) kw = want;
+  if (kw < 1) kw = 1;
+  sp->G = G; sp->tp = tp; sp->kw = kw;
+  return true;
+}
+
 // ------------------------------------------------------------------ wide GEMM (large M)
 
 template <typename T, bool AF32, int MT, int NT, int WM, int WN, int U>
@@ -385,8 +488,17 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
       if (M > 16) RT_LAUNCH((gemm16_kernel<T, true, 2, 1, 4, 8>), grid, dim3(256), 0, s, a);
       else RT_LAUNCH((gemm16_kernel<T, true, 1, 1, 4, 8>), grid, dim3(256), 0, s, a);
     } else if (a.ksplit > 1) {
-      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
-      else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 4, 4>), grid, dim3(256), 0, s, a);
+      SlabPlan sp;
+      if (sizeof(T) == 2 && slab_plan(M, N, a.Kp, a.ksplit, &sp)) {
+        // A rows of each slab staged once per workgroup
+        const dim3 g3(sp.G, 1, a.ksplit), blk(64 * sp.tp * sp.kw);
+        if (M > 16) RT_LAUNCH((gemm16_slab_kernel<2, 48, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
+        else RT_LAUNCH((gemm16_slab_kernel<1, 80, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
+      } else if (M > 16) {
+        RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
+      } else {
+        RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 4, 4>), grid, dim3(256), 0, s, a);
+      }
     } else if (N >= 16384) {
       // 16 rows: two waves of 8 loads in flight, so that all 1216 workgroups of the
       // Qwen3-4B gate|up are resident at once (5% faster than eight waves of four)
