@@ -19,7 +19,9 @@ struct AttnArgs {
   int splits;                    // key-range splits per (seq, kv head, row block)
   int row_blocks;                // row blocks of rb_rows (token, head) rows per sequence
   int rb_rows;                   // rows per block: 64, or 96 (bf16) when a sequence has 65..96 rows
-  float* opart; float* mlpart;   // split partials
+  // split partials: per (split, row) the running max and sum (fp32 mlpart) and the
+  // split's own normalised output O / sum (opart: fp16 for bf16 models, fp32 otherwise)
+  float* opart; float* mlpart;
   int32_t* plan;                 // [2][64] balanced split plan: first slot, split count per unit
   void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)

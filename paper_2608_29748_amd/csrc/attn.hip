@@ -23,6 +23,37 @@ namespace rt {
 constexpr int kChunk = 64;      // keys per LDS chunk (four pages)
 constexpr int kMaxSplitPages = 1024;   // fp32 path: page ids of one split held in LDS (16384 keys)
 
+// Storage of the split partials' normalised output rows: fp16 for bf16 models (the
+// output is rounded to bf16 anyway; fp16 keeps 3 more significand bits), fp32 otherwise.
+template <typename T> struct PartOf;
+template <> struct PartOf<bf16_t> {
+  using P = _Float16;
+  // (values are weighted means of V entries; beyond the fp16 range they are clamped)
+  __device__ static __forceinline__ _Float16 h(float v) { return (_Float16)fminf(fmaxf(v, -65504.f), 65504.f); }
+  __device__ static __forceinline__ void store4(P* p, float a, float b, float c, float d) {
+    typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 h4;
+    *reinterpret_cast<h4*>(p) = h4{h(a), h(b), h(c), h(d)};
+  }
+  template <int N>
+  __device__ static __forceinline__ void load(const P* p, float (&v)[N]) {
+    typedef __attribute__((__vector_size__(N * sizeof(_Float16)))) _Float16 hN;
+    const hN x = *reinterpret_cast<const hN*>(p);
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = (float)x[e];
+  }
+};
+template <> struct PartOf<float> {
+  using P = float;
+  __device__ static __forceinline__ void store4(P* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+  }
+  template <int N>
+  __device__ static __forceinline__ void load(const P* p, float (&v)[N]) {
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = p[e];
+  }
+};
+
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim, int rb_rows) {
   return (size_t)n_seqs * n_kv_heads * row_blocks * splits * rb_rows * head_dim;
 }
@@ -319,12 +350,13 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
     }
   } else {
     const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
-    float* op = a.opart + blk * kAttnRows * HD;
+    typename PartOf<T>::P* op = reinterpret_cast<typename PartOf<T>::P*>(a.opart) + blk * kAttnRows * HD;
     float* ml = a.mlpart + blk * kAttnRows * 2;
     const int rl = w * 16 + c16;
+    const float inv = lrun > 0.f ? 1.f / lrun : 0.f;
 #pragma unroll
     for (int t = 0; t < NHT; ++t)
-      *reinterpret_cast<float4*>(op + (size_t)rl * HD + t * 16 + 4 * g4) = make_float4(o[t][0], o[t][1], o[t][2], o[t][3]);
+      PartOf<T>::store4(op + (size_t)rl * HD + t * 16 + 4 * g4, o[t][0] * inv, o[t][1] * inv, o[t][2] * inv, o[t][3] * inv);
     if (g4 == 0) { ml[rl * 2] = mrun; ml[rl * 2 + 1] = lrun; }
   }
 }
@@ -964,25 +996,27 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
       }
     } else {
       const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
-      float* op = a.opart + blk * RBR * HD;
+      _Float16* op = reinterpret_cast<_Float16*>(a.opart) + blk * RBR * HD;
       float* ml = a.mlpart + blk * RBR * 2;
       const int rw = rh * RH + rl;
+      const float inv = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
       for (int t = 0; t < NHT; ++t)
-        *reinterpret_cast<float4*>(op + (size_t)rw * HD + t * 16 + 4 * g4) =
-            make_float4(o[t2][t][0], o[t2][t][1], o[t2][t][2], o[t2][t][3]);
+        PartOf<bf16_t>::store4(op + (size_t)rw * HD + t * 16 + 4 * g4, o[t2][t][0] * inv, o[t2][t][1] * inv,
+                               o[t2][t][2] * inv, o[t2][t][3] * inv);
       if (g4 == 0) { ml[rw * 2] = M; ml[rw * 2 + 1] = L; }
     }
   }
 }
 
 // One wave per (sequence, kv head, row).  Lane j holds split j's running max and sum;
-// the partial O rows are loaded in batches of 32 splits (lane l keeps hd l, l+64, ...),
-// issued before the split weights exp2(m_j - M) are known, and summed with the weights
-// read from lane j.
+// lane l keeps hd elements l*PL .. l*PL+PL-1 of every split's normalised partial row,
+// loaded in batches of 32 splits before the split weights are known, then summed with
+// the weights exp2(m_j - M) * sum_j read from lane j.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int PL = HD / 64;                 // hd elements per lane
+  using P = typename PartOf<T>::P;
+  constexpr int PL = HD / 64;                 // hd elements per lane (1 or 2)
   constexpr int NB = 32;                      // splits per batch of loads
   const int lane = threadIdx.x & 63;
   const int rl = blockIdx.x * 4 + (threadIdx.x >> 6);        // row within the row block
@@ -995,14 +1029,22 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int r = rb * RBR + rl;
   if (r >= nq * G) return;
+  const int tok = r / G, h = kvh * G + r % G;
+  T* out = (T*)a.out;
+  const int orow = s * a.rows_per_seq + tok;
+  if (S <= 0) {   // no split holds keys of this unit (not produced by the plans)
+#pragma unroll
+    for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane * PL + e, a.ldo)] = Elem<T>::from_f32(0.f);
+    return;
+  }
   const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
-  const float* opp = a.opart + (blk0 * RBR + rl) * HD + lane;   // split j: + j * RBR * HD
+  const P* opp = reinterpret_cast<const P*>(a.opart) + (blk0 * RBR + rl) * HD + lane * PL;   // split j: + j * RBR * HD
   const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;          // split j: + j * RBR * 2
+  // loads past the last split read split S-1 again (no branch, so all stay in flight);
+  // their weights are zero
   float ob[NB][PL];
 #pragma unroll
-  for (int j = 0; j < NB; ++j)
-#pragma unroll
-    for (int e = 0; e < PL; ++e) ob[j][e] = j < S ? opp[(size_t)j * RBR * HD + 64 * e] : 0.f;
+  for (int j = 0; j < NB; ++j) PartOf<T>::template load<PL>(opp + (size_t)(j < S ? j : S - 1) * RBR * HD, ob[j]);
   float mj = -INFINITY, lj = 0.f;
   if (lane < S) {
     const float2 v = *reinterpret_cast<const float2*>(mlp + (size_t)lane * RBR * 2);
@@ -1010,8 +1052,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     lj = v.y;
   }
   const float M = warp_max(mj);
-  const float f = (M == -INFINITY || mj == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj - M);
-  const float den = warp_sum(f * lj);
+  const float f = (M == -INFINITY || mj == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj - M) * lj;
+  const float den = warp_sum(f);
   float num[PL];
 #pragma unroll
   for (int e = 0; e < PL; ++e) num[e] = 0.f;
@@ -1024,8 +1066,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int j0 = NB; j0 < S; j0 += NB) {
 #pragma unroll
     for (int j = 0; j < NB; ++j)
-#pragma unroll
-      for (int e = 0; e < PL; ++e) ob[j][e] = j0 + j < S ? opp[(size_t)(j0 + j) * RBR * HD + 64 * e] : 0.f;
+      PartOf<T>::template load<PL>(opp + (size_t)(j0 + j < S ? j0 + j : S - 1) * RBR * HD, ob[j]);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j0 + j));
@@ -1033,12 +1074,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       for (int e = 0; e < PL; ++e) num[e] += (j0 + j < S ? fj : 0.f) * ob[j][e];
     }
   }
-  const int tok = r / G, h = kvh * G + r % G;
-  T* out = (T*)a.out;
-  const int orow = s * a.rows_per_seq + tok;
   const float inv = den > 0.f ? 1.f / den : 0.f;
 #pragma unroll
-  for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane + 64 * e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
+  for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane * PL + e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
 // One query tile per wave: 64-row blocks 8 waves, two LDS stages (64 KB at hd 128);
@@ -1095,8 +1133,16 @@ __global__ __launch_bounds__(256) void attn_merge16_kernel(AttnArgs a) {
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int r = rb * RBR + rl;
   if (r >= nq * G) return;
+  if (S <= 0) {   // no split holds keys of this unit (not produced by the plans)
+    const int tok = r / G, h = kvh * G + r % G;
+#pragma unroll
+    for (int e = 0; e < PL; ++e)
+      ((T*)a.out)[pa_index(s * a.rows_per_seq + tok, h * HD + c * PL + e, a.ldo)] = Elem<T>::from_f32(0.f);
+    return;
+  }
   const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
-  const float* opp = a.opart + (blk0 * RBR + rl) * HD + c * PL;   // split j: + j * RBR * HD
+  using P = typename PartOf<T>::P;
+  const P* opp = reinterpret_cast<const P*>(a.opart) + (blk0 * RBR + rl) * HD + c * PL;   // split j: + j * RBR * HD
   const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;            // split j: + j * RBR * 2
   float mj[4], lj[4];
   float M = -INFINITY;
@@ -1122,30 +1168,24 @@ __global__ __launch_bounds__(256) void attn_merge16_kernel(AttnArgs a) {
 #pragma unroll
   for (int e = 0; e < PL; ++e) num[e] = 0.f;
   for (int j0 = 0; j0 < S; j0 += NB) {
-    float4 ob[NB][PL / 4];
-    float mb[NB];
+    // loads past the last split read split S-1 again (all in flight); their weights are zero
+    float ob[NB][PL];
+    float2 mb[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      mb[j] = -INFINITY;
-#pragma unroll
-      for (int q = 0; q < PL / 4; ++q) ob[j][q] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (j0 + j < S) {
-        const float* op = opp + (size_t)(j0 + j) * RBR * HD;
-#pragma unroll
-        for (int q = 0; q < PL / 4; ++q) ob[j][q] = *reinterpret_cast<const float4*>(op + 4 * q);
-        mb[j] = mlp[(size_t)(j0 + j) * RBR * 2];
-      }
+      const int jj = j0 + j < S ? j0 + j : S - 1;
+      PartOf<T>::template load<PL>(opp + (size_t)jj * RBR * HD, ob[j]);
+      mb[j] = *reinterpret_cast<const float2*>(mlp + (size_t)jj * RBR * 2);
     }
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const float f = (M == -INFINITY || mb[j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mb[j] - M);
+    for (int j = 0; j < NB; ++j)
+      if (j0 + j >= S) mb[j].x = -INFINITY;
 #pragma unroll
-      for (int q = 0; q < PL / 4; ++q) {
-        num[4 * q] += f * ob[j][q].x;
-        num[4 * q + 1] += f * ob[j][q].y;
-        num[4 * q + 2] += f * ob[j][q].z;
-        num[4 * q + 3] += f * ob[j][q].w;
-      }
+    for (int j = 0; j < NB; ++j) {
+      // weight of split j: its share exp2(m_j - M) * sum_j of the denominator
+      const float f = (M == -INFINITY || mb[j].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mb[j].x - M) * mb[j].y;
+#pragma unroll
+      for (int e = 0; e < PL; ++e) num[e] += f * ob[j][e];
     }
   }
   const int tok = r / G, h = kvh * G + r % G;
