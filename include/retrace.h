@@ -269,7 +269,9 @@ int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t gr
  * (10 hidden + 4 Hq*hd + 2 ffn) bytes for bf16.  Returns RT_ERR_HIP if that
  * allocation fails.  16 = apply the q / k-norm and RoPE and write the block's K / V
  * rows with the separate post-processing kernel in rounds and target-only steps too
- * (by default the bf16 attention kernel does it there; both round identically). */
+ * (by default the bf16 attention kernel does it there; both round identically).
+ * 64 = batches whose attention does not take the q / k work use the spanning key-split
+ * plan whenever it is valid (by default only where it shortens the longest split). */
 int rt_set_debug(rt_model* m, int32_t flags);
 
 /* Like rt_spec_round, but the verify pass uses drafts[n_seqs][block_size-1] (host)

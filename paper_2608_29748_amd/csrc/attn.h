@@ -22,7 +22,10 @@ struct AttnArgs {
   // split partials: per (split, row) the running max and sum (fp32 mlpart) and the
   // split's own normalised output O / sum (opart: fp16 for bf16 models, fp32 otherwise)
   float* opart; float* mlpart;
-  int32_t* plan;                 // [2][64] balanced split plan: first slot, split count per unit
+  int32_t* plan;                 // [2][64] balanced split plan: first partial block, split count per unit
+  int span;                      // bf16 kernel without the fused q / k work: balanced launches may
+                                 // use the spanning plan (slots cross unit boundaries) when it
+                                 // shortens the longest split; 2: whenever it is valid (test hook)
   void* out; int ldo;            // packed GEMM-operand layout of [row][n_q_heads * head_dim]; ldo = group stride
   float scale;                   // 1/sqrt(head_dim)
   // Rounds (at most 16 rows per sequence, one q|k|v slab): the q / k per-head RMSNorm,

@@ -55,7 +55,7 @@ template <> struct PartOf<float> {
 };
 
 size_t attn_partial_floats(int n_seqs, int n_kv_heads, int row_blocks, int splits, int head_dim, int rb_rows) {
-  return (size_t)n_seqs * n_kv_heads * row_blocks * splits * rb_rows * head_dim;
+  return (size_t)n_kv_heads * ((size_t)n_seqs * row_blocks * (splits + 1) - 1) * rb_rows * head_dim;
 }
 
 // wave-wide integer reductions and scan of the ROCm device library (DPP based)
@@ -92,6 +92,7 @@ __device__ __forceinline__ int attn_unit_chunks(const AttnArgs& a, int u, int rb
 struct SplitPlan {
   int count;   // lane u: s_u (0 past the units)
   int end;     // lane u: s_0 + .. + s_u
+  int q;       // the chunk bound per split
 };
 // Balanced plan; all 64 lanes of the wave must be active.
 __device__ __forceinline__ SplitPlan attn_balanced_plan(const AttnArgs& a, int rbr) {
@@ -107,7 +108,7 @@ __device__ __forceinline__ SplitPlan attn_balanced_plan(const AttnArgs& a, int r
     else lo = mid + 1;
   }
   const int cnt = (n + lo - 1) / lo;
-  return SplitPlan{cnt, __ockl_wfscan_add_i32(cnt, true)};
+  return SplitPlan{cnt, __ockl_wfscan_add_i32(cnt, true), lo};
 }
 // Work of the workgroup at (blockIdx.x, blockIdx.z): unit, split index within the unit
 // and the unit's split count; false for a slot the balanced plan leaves idle.
@@ -129,14 +130,50 @@ __device__ __forceinline__ bool attn_slot_work(const AttnArgs& a, int rbr, int& 
   split = slot - (__builtin_amdgcn_readlane(p.end, unit) - nsplit);
   return true;
 }
-// First slot (x) and split count (y) of unit u (merge side): the balanced plan as the
-// partial kernel's first workgroup stored it, clamped to this launch's slots (a merge
-// replayed on its own, for timing, may find another launch's plan there).
+// Partial blocks per KV head: one per slot, plus one per unit boundary under the
+// balanced plans (a spanning slot writes one block per unit it meets).
+__device__ __forceinline__ int attn_head_blocks(const AttnArgs& a) {
+  const int nu = a.n_seqs * a.row_blocks, slots = nu * a.splits;
+  return attn_balanced(a) ? slots + nu - 1 : slots;
+}
+// First partial block (x) and split count (y) of unit u (merge side): the balanced plan
+// as the partial kernel's first workgroup stored it, clamped to this launch's blocks (a
+// merge replayed on its own, for timing, may find another launch's plan there).
 __device__ __forceinline__ int2 attn_unit_slots(const AttnArgs& a, int u) {
   if (!attn_balanced(a)) return make_int2(u * a.splits, a.splits);
-  const int slots = a.n_seqs * a.row_blocks * a.splits;
-  const int first = min(max(a.plan[u], 0), slots);
-  return make_int2(first, min(max(a.plan[64 + u], 0), min(slots - first, 64)));
+  const int nb = attn_head_blocks(a);
+  const int first = min(max(a.plan[u], 0), nb);
+  return make_int2(first, min(max(a.plan[64 + u], 0), min(nb - first, 64)));
+}
+// Spanning plan (bf16 kernel without the fused q / k work; balanced launches): the units'
+// chunks are laid end to end, C in all, and slot x takes chunks [b(x), b(x+1)) of that
+// sequence, b(x) = floor(x C / S), so every slot gets floor or ceil of C / S chunks.  A
+// slot may meet the end of one unit and the start of the next; it then runs one segment
+// per unit.  The j-th slot meeting unit u writes partial block seg_first(u) + j.  Usable
+// when no unit meets more than 64 slots (one merge lane per split); else the kernel keeps
+// the balanced plan.  All 64 lanes of the wave must be active; lane u describes unit u.
+struct SpanPlan {
+  int start, n;        // unit u's first chunk in the concatenation, its chunk count
+  int first, count;    // its first slot, the number of slots meeting it
+  int seg_end;         // inclusive prefix sum of count (its blocks end there)
+  int total;           // C
+  bool ok;             // every count <= 64
+};
+__device__ __forceinline__ SpanPlan attn_span_plan(const AttnArgs& a, int rbr) {
+  const int lane = threadIdx.x & 63;
+  const int nu = a.n_seqs * a.row_blocks, S = nu * a.splits;
+  SpanPlan p;
+  p.n = lane < nu ? attn_unit_chunks(a, lane, rbr) : 0;
+  p.start = __ockl_wfscan_add_i32(p.n, true) - p.n;
+  p.total = __ockl_wfred_add_i32(p.n);
+  const int C = max(p.total, 1);
+  // slot holding chunk t: the largest x with floor(x C / S) <= t
+  auto slot_of = [&](int t) { return (int)(((long)(t + 1) * S + C - 1) / C) - 1; };
+  p.first = p.n > 0 ? slot_of(p.start) : 0;
+  p.count = p.n > 0 ? slot_of(p.start + p.n - 1) - p.first + 1 : 0;
+  p.seg_end = __ockl_wfscan_add_i32(p.count, true);
+  p.ok = __ockl_wfred_max_i32(p.count) <= 64;
+  return p;
 }
 
 // Scores are computed transposed, S^T = K Q^T: in the accumulator layout a lane holds
@@ -349,7 +386,7 @@ __global__ __launch_bounds__(256) void attn_staged_kernel(AttnArgs a) {
           op[pa_index(orow, h * HD + t * 16 + 4 * g4 + i, a.ldo)] = Elem<T>::from_f32(o[t][i] * inv);
     }
   } else {
-    const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
+    const size_t blk = (size_t)kvh * attn_head_blocks(a) + blockIdx.z * a.splits + blockIdx.x;
     typename PartOf<T>::P* op = reinterpret_cast<typename PartOf<T>::P*>(a.opart) + blk * kAttnRows * HD;
     float* ml = a.mlpart + blk * kAttnRows * 2;
     const int rl = w * 16 + c16;
@@ -518,15 +555,58 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rh = w >> 1, kh = w & 1;
   const int kvh = blockIdx.y;
-  int unit, split, nsplit;
-  if (!attn_slot_work(a, RBR, unit, split, nsplit)) return;
+  // This workgroup's segments: one (unit, chunk range, partial block) under the uniform
+  // and balanced plans; under the spanning plan (batches without the fused q / k work)
+  // one per unit its slot meets, run one after the other.
+  int unit = 0, split = 0, nsplit = 1;
+  bool span = false;
+  SpanPlan sp{};
+  unsigned long long seg_units = 0;   // spanning: units still to run
+  const int slot = blockIdx.z * a.splits + blockIdx.x;
+  if constexpr (!FUSED) {
+    if (a.span && attn_balanced(a)) {
+      // span when its slots are shorter than the balanced plan's longest split by more
+      // than the pipeline fill of a second segment (about three chunks, measured)
+      sp = attn_span_plan(a, RBR);
+      const int S = a.n_seqs * a.row_blocks * a.splits;
+      span = sp.ok && (a.span == 2 || (sp.total + S - 1) / S + 3 < attn_balanced_plan(a, RBR).q);
+    }
+  }
+  if (span) {
+    if (slot == 0 && blockIdx.y == 0 && threadIdx.x < 64) {   // hand the plan to the merge
+      a.plan[threadIdx.x] = sp.seg_end - sp.count;
+      a.plan[64 + threadIdx.x] = sp.count;
+    }
+    seg_units = __ballot(sp.count > 0 && slot >= sp.first && slot < sp.first + sp.count);
+    if (seg_units == 0) return;
+  } else if (!attn_slot_work(a, RBR, unit, split, nsplit)) {
+    return;
+  }
+  for (;;) {
+  int seg_c0 = 0, seg_c1 = 0;
+  size_t part_blk = (size_t)kvh * attn_head_blocks(a) + slot;
+  if (span) {
+    unit = __builtin_ctzll(seg_units);
+    seg_units &= seg_units - 1;
+    const int S = a.n_seqs * a.row_blocks * a.splits;
+    const long b0 = (long)slot * sp.total / S, b1 = (long)(slot + 1) * sp.total / S;
+    const int ustart = __builtin_amdgcn_readlane(sp.start, unit), un = __builtin_amdgcn_readlane(sp.n, unit);
+    const int ufirst = __builtin_amdgcn_readlane(sp.first, unit);
+    seg_c0 = (int)max(b0, (long)ustart) - ustart;
+    seg_c1 = (int)min(b1, (long)(ustart + un)) - ustart;
+    split = slot - ufirst;
+    nsplit = __builtin_amdgcn_readlane(sp.count, unit);
+    part_blk = (size_t)kvh * attn_head_blocks(a) + (__builtin_amdgcn_readlane(sp.seg_end, unit) - nsplit) + split;
+  }
+  {
   const int s = unit / a.row_blocks, rb = unit % a.row_blocks;
   const int G = a.n_q_heads / a.n_kv_heads;
   const int nq = a.nq ? a.nq[s * a.seq_stride] : a.rows_per_seq;
   const int P = a.pos0[s * a.seq_stride];
   const int nrows = nq * G;
   const int row0 = rb * RBR;
-  if (row0 >= nrows) return;
+  if (row0 >= nrows) goto seg_done;
+  {
   const int last_tok = min(nrows, row0 + RBR) - 1;
   const int kv_end = a.causal ? P + last_tok / G + 1 : P + nq;   // keys [0, kv_end), kv_end >= 1
   const int nchunks = (kv_end + kChunk - 1) / kChunk;
@@ -534,7 +614,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   // take the extra chunks, so the last one, which holds the newest keys (in rounds the
   // block's, whose K / V it may also write), is never the longest
   const int cq = nchunks / nsplit, cr = nchunks % nsplit;
-  const int c_beg = split * cq + min(split, cr), c_end = c_beg + cq + (split < cr ? 1 : 0);
+  const int c_beg = span ? seg_c0 : split * cq + min(split, cr);
+  const int c_end = span ? seg_c1 : c_beg + cq + (split < cr ? 1 : 0);
   const int last_page = (kv_end - 1) / kPage;
   const_i32_t* pt = (const_i32_t*)(a.page_table + (size_t)s * a.max_pages);
   // page w of chunk c (pages past kv_end are replaced by the last valid one, so every
@@ -962,7 +1043,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     }
   }
   lds_barrier();
-  if (kh == 1) return;
+  if (kh == 1) goto seg_done;
 #pragma unroll
   for (int t2 = 0; t2 < NRT; ++t2) {
     const int rl = t2 * 16 + c16;
@@ -995,7 +1076,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
             op[pa_index(orow, h * HD + t * 16 + 4 * g4 + e, a.ldo)] = f32_to_bf16(o[t2][t][e] * inv);
       }
     } else {
-      const size_t blk = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + blockIdx.z * a.splits + blockIdx.x;
+      const size_t blk = part_blk;
       _Float16* op = reinterpret_cast<_Float16*>(a.opart) + blk * RBR * HD;
       float* ml = a.mlpart + blk * RBR * 2;
       const int rw = rh * RH + rl;
@@ -1006,6 +1087,12 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
                                o[t2][t][2] * inv, o[t2][t][3] * inv);
       if (g4 == 0) { ml[rw * 2] = M; ml[rw * 2 + 1] = L; }
     }
+  }
+  }
+  }
+seg_done:
+  if (!span || seg_units == 0) break;
+  lds_barrier();   // the key-half merge buffer is read before the next segment's copies land
   }
 }
 
@@ -1037,7 +1124,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane * PL + e, a.ldo)] = Elem<T>::from_f32(0.f);
     return;
   }
-  const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
+  const size_t blk0 = (size_t)kvh * attn_head_blocks(a) + us.x;
   const P* opp = reinterpret_cast<const P*>(a.opart) + (blk0 * RBR + rl) * HD + lane * PL;   // split j: + j * RBR * HD
   const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;          // split j: + j * RBR * 2
   // loads past the last split read split S-1 again (no branch, so all stay in flight);
@@ -1140,7 +1227,7 @@ __global__ __launch_bounds__(256) void attn_merge16_kernel(AttnArgs a) {
       ((T*)a.out)[pa_index(s * a.rows_per_seq + tok, h * HD + c * PL + e, a.ldo)] = Elem<T>::from_f32(0.f);
     return;
   }
-  const size_t blk0 = (size_t)kvh * a.n_seqs * a.row_blocks * a.splits + us.x;
+  const size_t blk0 = (size_t)kvh * attn_head_blocks(a) + us.x;
   using P = typename PartOf<T>::P;
   const P* opp = reinterpret_cast<const P*>(a.opart) + (blk0 * RBR + rl) * HD + c * PL;   // split j: + j * RBR * HD
   const float* mlp = a.mlpart + (blk0 * RBR + rl) * 2;            // split j: + j * RBR * 2

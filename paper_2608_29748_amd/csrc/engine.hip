@@ -355,8 +355,9 @@ struct Engine : EngineBase {
     // Rounds and target-only steps (at most 16 rows per sequence, bf16, one q|k|v slab):
     // the attention kernel does the q / k-norm, the rotation and the block's K / V cache
     // write itself (debug flag 16 keeps the separate kernel)
-    const bool fuse = sizeof(T) == 2 && qks == 1 && c.nq == nullptr && c.rows_per_seq <= 16 && !(flags & 16) &&
-                      (q.hd == 64 || q.hd == 128);
+    const bool fusable = sizeof(T) == 2 && qks == 1 && c.nq == nullptr && c.rows_per_seq <= 16 &&
+                         (q.hd == 64 || q.hd == 128);
+    const bool fuse = fusable && !(flags & 16);
     if (!fuse) {
       QkvPostArgs qp{};
       qp.src = qks > 1 ? pat<float>(q.partial, q.s_partial) : at<float>(q.qkvf); qp.lds = q.qkvN; qp.M = c.M;
@@ -378,6 +379,9 @@ struct Engine : EngineBase {
     a.pos0 = c.pos0; a.nq = c.nq; a.seq_stride = c.stride; a.rows_per_seq = c.rows_per_seq;
     a.n_seqs = c.n_seqs; a.causal = c.causal; a.n_q_heads = q.Hq; a.n_kv_heads = q.Hkv; a.head_dim = q.hd;
     a.splits = c.splits; a.row_blocks = c.rb; a.rb_rows = c.rb_rows;
+    // batches whose attention never takes the q / k work (so the fused and separate forms,
+    // compared by a test hook, share one plan) may span unit boundaries
+    a.span = fusable ? 0 : (flags & 64) ? 2 : 1;
     a.opart = pat<float>(q.opart, q.s_opart); a.mlpart = pat<float>(q.mlpart, q.s_mlpart);
     a.plan = pat<int32_t>(q.attn_plan, q.s_attn_plan);
     a.out = at<T>(q.attn); a.ldo = 16 * q.Kp_q; a.scale = 1.0f / sqrtf((float)q.hd);
@@ -1411,7 +1415,7 @@ int rt_stream_read(const void* d_buf, size_t buf_bytes, size_t bytes, int32_t gr
 
 int rt_set_debug(rt_model* m, int32_t flags) {
   if (!m || !m->e) return fail(RT_ERR_INVALID, "null model");
-  if (flags < 0 || flags > 31) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
+  if (flags < 0 || flags > 127) return fail(RT_ERR_INVALID, "unknown debug flags %d", flags);
   if (flags & 8) {
     const int st = m->e->alloc_trace();
     if (st) return st;

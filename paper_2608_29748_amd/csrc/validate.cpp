@@ -191,8 +191,10 @@ int make_plan(const rt_config* c, Plan* p) {
   {
     size_t rb = q.attn_rb > q.pf_rb ? q.attn_rb : q.pf_rb;
     (void)rb;
-    size_t rows = (size_t)q.bmax * q.Hkv * q.attn_rb * q.attn_splits * q.attn_rows;
-    const size_t ar_rows = (size_t)q.bmax * q.Hkv * q.ar_rb * q.ar_splits * kAttnRowsAr;
+    // per KV head one partial block per slot, plus one per unit boundary (a slot of the
+    // spanning plan writes one block per unit it meets)
+    size_t rows = (size_t)q.Hkv * ((size_t)q.bmax * q.attn_rb * (q.attn_splits + 1) - 1) * q.attn_rows;
+    const size_t ar_rows = (size_t)q.Hkv * ((size_t)q.bmax * q.ar_rb * (q.ar_splits + 1) - 1) * kAttnRowsAr;
     if (ar_rows > rows) rows = ar_rows;
     q.opart = take(rows * q.hd * 4);
     q.mlpart = take(rows * 2 * 4);

@@ -54,14 +54,21 @@ def test_prefill_and_rounds_match_oracle(name):
     eng.close()
 
 
-@pytest.mark.parametrize("name,lens", [("tiny-f32", (20, 600)), ("mini-bf16-ragged", (20, 900))])
-def test_ragged_batch_key_splits_match_oracle(name, lens):
+@pytest.mark.parametrize("name,lens,batch", [("tiny-f32", (20, 600), 4), ("mini-bf16-ragged", (20, 900), 4),
+                                             ("mini-bf16-b6", (20, 900), 7)])
+def test_ragged_batch_key_splits_match_oracle(name, lens, batch):
     """A batch of very unequal contexts: the attention's key-split workgroups are shared
     out by context length (one split for the short sequences, several for the long
-    ones, some workgroups idle), in the fp32 and the bf16 kernels."""
-    wl, W, prompts = _setup(name, norm_init="perturbed", batch=4, prompt_len=lens)
+    ones, some workgroups idle), in the fp32 and the bf16 kernels; at seven sequences
+    (112 rows, no fused q / k work) the slots split the concatenated chunks evenly and
+    one slot may cover the end of a context and the start of the next ones."""
+    wl, W, prompts = _setup(name, norm_init="perturbed", batch=batch, prompt_len=lens)
     log(f"[{name} ragged] prompts {[len(p) for p in prompts]}")
     eng = engine_for(wl, W)
+    if batch > 4:   # the spanning plan wherever it is valid (debug flag 64)
+        orig = eng.set_debug
+        eng.set_debug = lambda f: orig(f | 64)
+        eng.set_debug(0)
     R = OracleRunner(OracleModel(wl, W))
     first = eng.prefill(prompts, wl.new_tokens)
     states = [R.prefill(p, wl.new_tokens) for p in prompts]
