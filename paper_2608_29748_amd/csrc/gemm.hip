@@ -318,13 +318,29 @@ __global__ __launch_bounds__(1024) void gemm16_slab_kernel(GemmArgs a, int tp_n,
       for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * (lane / 16) + i][lane % 16] = acc[mt][i];
     __syncthreads();
     // tile group g2 sums its KW k ranges in order
-    for (int idx = threadIdx.x; idx < tp_n * ROWS * 16; idx += blockDim.x) {
-      const int g2 = idx / (ROWS * 16), r = idx / 16 % ROWS, c = idx % 16;
-      const int tt = base + g2 * gridDim.x, m = r, n = tt * 16 + c;
-      if (tt >= n_tiles || m >= a.e.M || n >= a.e.N) continue;
-      float sum = 0.f;
-      for (int v = 0; v < kw_n; ++v) sum += red[g2 * kw_n + v][r][c];
-      a.e.out_f32[(size_t)z * a.e.part_stride + (size_t)m * a.e.ldo + n] = sum;
+    if (a.e.kind == EPI_SWIGLU) {
+      // 8 gate and the matching 8 up columns per 16-column tile: out[m][n/2 + j]
+      for (int idx = threadIdx.x; idx < tp_n * ROWS * 8; idx += blockDim.x) {
+        const int g2 = idx / (ROWS * 8), r = idx / 8 % ROWS, j = idx % 8;
+        const int tt = base + g2 * gridDim.x, m = r;
+        if (tt >= n_tiles || m >= a.e.M || tt * 16 + j >= a.e.N) continue;
+        float g = 0.f, u = 0.f;
+        for (int v = 0; v < kw_n; ++v) {
+          g += red[g2 * kw_n + v][r][j];
+          u += red[g2 * kw_n + v][r][j + 8];
+        }
+        const float act = g / (1.0f + expf(-g)) * u;
+        ((bf16_t*)a.e.out_act)[pa_index(m, tt * 8 + j, a.e.ldo)] = f32_to_bf16(act);
+      }
+    } else {
+      for (int idx = threadIdx.x; idx < tp_n * ROWS * 16; idx += blockDim.x) {
+        const int g2 = idx / (ROWS * 16), r = idx / 16 % ROWS, c = idx % 16;
+        const int tt = base + g2 * gridDim.x, m = r, n = tt * 16 + c;
+        if (tt >= n_tiles || m >= a.e.M || n >= a.e.N) continue;
+        float sum = 0.f;
+        for (int v = 0; v < kw_n; ++v) sum += red[g2 * kw_n + v][r][c];
+        a.e.out_f32[(size_t)z * a.e.part_stride + (size_t)m * a.e.ldo + n] = sum;
+      }
     }
     __syncthreads();
   }
@@ -334,7 +350,7 @@ __global__ __launch_bounds__(1024) void gemm16_slab_kernel(GemmArgs a, int tp_n,
 // Launch parameters of gemm16_slab_kernel for M rows, N columns and a padded K with `slabs`
 // k slabs: workgroups per slab (so that about 256 run), column tiles in flight per
 // workgroup and waves per tile (16 at most in all); false if the slab's A rows do not fit.
-struct SlabPlan { int G, tp, kw; };
+struct SlabPlan { int G, tp, kw, kpw; };
 static bool slab_plan(int M, int N, int Kp, int slabs, SlabPlan* sp) {
   const int MT = M > 16 ? 2 : 1, KT = Kp / kTileK, n_tiles = (N + 15) / 16;
   const int kts = (KT + slabs - 1) / slabs;
@@ -349,7 +365,17 @@ static bool slab_plan(int M, int N, int Kp, int slabs, SlabPlan* sp) {
   if (kw > want) kw = want;
   if (kw < 1) kw = 1;
   sp->G = G; sp->tp = tp; sp->kw = kw;
+  sp->kpw = (kts + kw - 1) / kw;
   return true;
+}
+// Weight tiles in flight per wave: batches of 8 up to 16 k tiles per wave, else of 14
+// (measured at the Qwen3-4B shape: down, 16 tiles per wave, 11.8 us with two batches of
+// 8 against 12.6 with one of 16; gate|up, 27 tiles, 19.4 us with 14 against 19.9 with 8)
+static void slab_launch(const GemmArgs& a, const SlabPlan& sp, int M, int slabs, hipStream_t s) {
+  const dim3 g3(sp.G, 1, slabs), blk(64 * sp.tp * sp.kw);
+  if (M > 16) RT_LAUNCH((gemm16_slab_kernel<2, 48, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
+  else if (sp.kpw <= 16) RT_LAUNCH((gemm16_slab_kernel<1, 80, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
+  else RT_LAUNCH((gemm16_slab_kernel<1, 80, 14>), g3, blk, 0, s, a, sp.tp, sp.kw);
 }
 
 // ------------------------------------------------------------------ wide GEMM (large M)
@@ -478,10 +504,11 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
       return hipGetLastError();
     }
     // tile width, waves and loads in flight per shape class (measured on the Qwen3 layer
-    // shapes): split reductions 16 columns x 4 waves per slab; N >= 16384 (gate|up) 16
-    // columns (2 waves x 8 loads at 16 rows); N >= 5120 32 columns (two loads in flight
-    // per wave at 16 rows: 5% faster than four at the 4B q|k|v); otherwise 16 columns
-    // with 8 loads in flight
+    // shapes): split reductions (bf16) on the slab kernel, A staged once per slab and
+    // workgroup; N >= 16384 (gate|up, SwiGLU) on the slab kernel with one slab (4B shape
+    // 20.3 -> 19.4 us; the 16-column kernel with 2 waves x 8 loads at 32 rows); N >= 5120
+    // 32 columns (two loads in flight per wave at 16 rows: 5% faster than four at the 4B
+    // q|k|v); otherwise 16 columns with 8 loads in flight
     if ((a.e.kind == EPI_PARTIAL) != (a.ksplit > 1) || a.ksplit < 1) return hipErrorInvalidValue;
     dim3 grid((N + 15) / 16, 1, a.ksplit);
     if (a_f32) {
@@ -491,18 +518,18 @@ hipError_t gemm(const GemmArgs& a, int shape, bool a_f32, hipStream_t s) {
       SlabPlan sp;
       if (sizeof(T) == 2 && slab_plan(M, N, a.Kp, a.ksplit, &sp)) {
         // A rows of each slab staged once per workgroup
-        const dim3 g3(sp.G, 1, a.ksplit), blk(64 * sp.tp * sp.kw);
-        if (M > 16) RT_LAUNCH((gemm16_slab_kernel<2, 48, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
-        else RT_LAUNCH((gemm16_slab_kernel<1, 80, 8>), g3, blk, 0, s, a, sp.tp, sp.kw);
+        slab_launch(a, sp, M, a.ksplit, s);
       } else if (M > 16) {
         RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 4, 4>), grid, dim3(256), 0, s, a);
       } else {
         RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 4, 4>), grid, dim3(256), 0, s, a);
       }
     } else if (N >= 16384) {
-      // 16 rows: two waves of 8 loads in flight, so that all 1216 workgroups of the
-      // Qwen3-4B gate|up are resident at once (5% faster than eight waves of four)
-      if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 4>), grid, dim3(512), 0, s, a);
+      SlabPlan sp;
+      if (sizeof(T) == 2 && a.e.kind == EPI_SWIGLU && slab_plan(M, N, a.Kp, 1, &sp)) {
+        slab_launch(a, sp, M, 1, s);
+      }
+      else if (M > 16) RT_LAUNCH((gemm16_kernel<T, false, 2, 1, 8, 4>), grid, dim3(512), 0, s, a);
       else RT_LAUNCH((gemm16_kernel<T, false, 1, 1, 2, 8>), grid, dim3(128), 0, s, a);
     } else if (N >= 5120) {
       dim3 g2((N + 31) / 32, 1, 1);
