@@ -59,7 +59,11 @@ def dominant_desc(wl):
     """The dominant kernel's launch class at this workload's verify shape."""
     rows = wl.batch * wl.block_size
     kern = "gemm16_kernel" if rows <= 64 else "gemm_mid_kernel"
-    return (f"gemm_gate_up: fused gate|up projection GEMM with SwiGLU epilogue ({kern}, bf16 MFMA, "
+    # at most 16 bf16 rows, K <= 2560 and at least 16384 columns: the k-slab kernel with
+    # the activation block staged in LDS (one slab)
+    if rows <= 16 and wl.dtype == "bf16" and wl.target.hidden <= 2560 and 2 * wl.target.ffn >= 16384:
+        kern = "gemm16_slab_kernel"
+    return (f"gemm_gate_up: fused gate|up projection GEMM with SwiGLU epilogue ({kern}, {wl.dtype} MFMA, "
             f"{rows} rows x {2 * wl.target.ffn} columns x K {wl.target.hidden})")
 
 

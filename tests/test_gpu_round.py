@@ -136,3 +136,19 @@ def test_long_prompt_chunked_prefill():
     rep = run_teacher_forced(eng, R, wl, states, 3, TOL[wl.dtype])
     log(f"[long prompt] rounds max err {rep.max_err}")
     eng.close()
+
+
+def test_two_sequence_slab_kernel_matches_oracle():
+    """Two sequences (32 round rows) of the 4096-wide mini model: the o and down k-slab
+    partials run on the slab kernel with two 16-row groups of each slab's activations
+    staged in LDS (one sequence runs one group); per stage and end to end."""
+    wl, W, prompts = _setup("mini-bf16-w4096", norm_init="perturbed", batch=2, prompt_len=(40, 70))
+    eng = engine_for(wl, W)
+    R = OracleRunner(OracleModel(wl, W))
+    first = eng.prefill(prompts, wl.new_tokens)
+    states = [R.prefill(p, wl.new_tokens) for p in prompts]
+    assert list(first) == [st.anchor for st in states]
+    rep = run_teacher_forced(eng, R, wl, states, 4, TOL[wl.dtype], exact=_exact(wl, W, R), stages={})
+    log(f"[w4096 batch 2] rounds {rep.rounds} max err {rep.max_err}")
+    assert rep.conditioned > 0
+    eng.close()
