@@ -35,6 +35,36 @@ def _compile(src: str) -> str:
     return obj
 
 
+# sources whose kernels hold LDS reads in inline assembly that the compiler's wait
+# insertion does not see: their gfx950 assembly is checked (isa_check) on every build
+ASM_CHECKED = ["attn.hip"]
+
+
+def _assembly(src: str) -> str:
+    out = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
+    cmd = [_hipcc(), *[f for f in FLAGS if f != "-fPIC"], *EXTRA.get(src, []), "--cuda-device-only", "-S",
+           os.path.join(CSRC, src), "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    return out
+
+
+def _check_assembly(path: str) -> None:
+    try:
+        from . import isa_check
+    except ImportError:       # run as a script
+        import isa_check
+    with open(path) as fh:
+        asm = fh.read()
+    if not isa_check.checked_kernels(asm):
+        raise RuntimeError(f"{path}: no kernel with inline-asm LDS reads found (check out of date)")
+    bad = isa_check.check(asm)
+    if bad:
+        raise RuntimeError(f"{path}: registers of untracked LDS reads touched before their wait:\n  "
+                           + "\n  ".join(bad[:20]))
+
+
 STAMP = OUT + ".sha256"
 
 
@@ -53,8 +83,11 @@ def source_hash() -> str:
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     digest = source_hash()
-    with cf.ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(8) as ex:
+        asms = [ex.submit(_assembly, src) for src in ASM_CHECKED]
         objs = list(ex.map(_compile, SOURCES))
+        for f in asms:
+            _check_assembly(f.result())
     tmp = OUT + ".tmp"
     cmd = [_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
