@@ -175,6 +175,8 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
+// s_waitcnt lgkmcnt(0) leaving the other counters alone: this wave's LDS accesses are done.
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xc07f); }
 // s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vm() {

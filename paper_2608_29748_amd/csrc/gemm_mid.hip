@@ -1,14 +1,16 @@
 // Weight-streaming bf16 MFMA GEMM for 33..512 rows (batched verify / draft blocks and
 // prefill chunks): Y = X * W^T with the packed operands of gemm.h.
 //
-// A workgroup (4 or 8 waves) owns MB rows x NB columns of the output and one k slab.  Per
+// A workgroup (4, 8 or 16 waves) owns MB rows x NB columns of the output and one k slab.  Per
 // 32-wide k tile it copies the MB/16 packed A fragments and NB/16 packed weight tiles
 // (1 KiB each, already in MFMA lane order) straight from memory into a ring of LDS
 // stages (16-byte direct-to-LDS loads, NSTAGE-1 k tiles in flight), so every weight
 // byte is read from HBM once per workgroup and every A byte once per workgroup.  Waves
 // split the tile (NW/2) x 2: wave (wm, wn) accumulates MB/(NW/2) rows x NB/2 columns,
-// reading its fragments from LDS at consecutive 16-byte lane offsets (conflict free).  The
-// epilogue runs on the accumulators in registers.
+// reading its fragments from LDS at consecutive 16-byte lane offsets (conflict free); with
+// DB the fragments of k tile kt+1 are read while the MFMAs of tile kt run (a register
+// double buffer, one k tile of the ring less in flight).  The epilogue runs on the
+// accumulators in registers.
 //
 // An fp32 A operand (AF32) is copied as 2 KiB fragments and split in registers into a
 // bf16 high part and a bf16 remainder, each multiplied by the weight tile (two MFMAs),
@@ -102,7 +104,7 @@ __device__ __forceinline__ void wait_tiles(int r) {
   }
 }
 
-template <int MB, int NB, int NSTAGE, bool AF32, int NW>
+template <int MB, int NB, int NSTAGE, bool AF32, int NW, bool DB = false>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_mid_kernel(GemmArgs a) {
   constexpr int WM = NW / 2;            // wave rows (two wave columns)
   constexpr int MT = MB / (16 * WM);    // 16-row tiles per wave
@@ -158,44 +160,87 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 #pragma unroll
   for (int i = 0; i < NSTAGE - 1; ++i)
     if (kb + i < ke) issue(kb + i, i);
-  for (int kt = kb; kt < ke; ++kt) {
-    const int i = kt - kb;
-    // this wave's copies of k tile kt have landed once at most the later tiles' remain
-    wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kt);
-    lds_barrier();   // every wave's copies of tile kt are visible; tile kt-1's stage is free
-    if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
-    const char* st = smem + (i % NSTAGE) * STG;
-    Frag<bf16_t> bf[NT];
-#pragma unroll
-    for (int n = 0; n < NT; ++n)
-      bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AI + wn * NT + n) * 1024 + lane * 16);
-    if constexpr (AF32) {
-#pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        const float4* pa = reinterpret_cast<const float4*>(st + (wm * MT + m) * 2048 + lane * 32);
-        const float4 x0 = pa[0], x1 = pa[1];
-        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-        Frag<bf16_t> hi, lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const bf16_t h = f32_to_bf16(xs[e]);
-          hi.v[e] = (short)h;
-          lo.v[e] = (short)f32_to_bf16(xs[e] - bf16_to_f32(h));
-        }
-#pragma unroll
-        for (int n = 0; n < NT; ++n) {
-          mma(acc[m][n], hi, bf[n]);
-          mma(acc[m][n], lo, bf[n]);
-        }
-      }
-    } else {
-      Frag<bf16_t> af[MT];
+  if constexpr (DB) {
+    static_assert(!AF32 && NSTAGE >= 3, "fragment double buffer: bf16 operands");
+    // The fragments of tile kt+1 are read from LDS while the MFMAs of tile kt run.  Step
+    // kt: wait for this wave's copies of tile kt+1 (the later tiles' stay in flight) and
+    // for its own LDS reads, barrier (all copies of kt+1 visible, every wave done reading
+    // tile kt-1, whose stage the step's copies then refill), read tile kt+1's fragments,
+    // multiply tile kt's.  The last step reads a stale stage into registers nobody uses, so
+    // that every step has one shape and the compiler's wait before the MFMAs covers only
+    // the previous step's reads.
+    auto read = [&](int stg, Frag<bf16_t>(&af)[MT], Frag<bf16_t>(&bf)[NT]) {
+      const char* st = smem + stg * STG;
 #pragma unroll
       for (int m = 0; m < MT; ++m) af[m].v = *reinterpret_cast<const bf16x8*>(st + (wm * MT + m) * 1024 + lane * 16);
 #pragma unroll
+      for (int n = 0; n < NT; ++n) bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AI + wn * NT + n) * 1024 + lane * 16);
+    };
+    auto step = [&](int kt, Frag<bf16_t>(&ca)[MT], Frag<bf16_t>(&cb)[NT], Frag<bf16_t>(&na)[MT],
+                    Frag<bf16_t>(&nb)[NT]) {
+      const int i = kt - kb;
+      wait_tiles<NSTAGE - 3, LPW>(ke - 2 - kt);
+      wait_lds();
+      lds_barrier();
+      if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
+      read((i + 1) % NSTAGE, na, nb);
+#pragma unroll
       for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int n = 0; n < NT; ++n) mma(acc[m][n], af[m], bf[n]);
+        for (int n = 0; n < NT; ++n) mma(acc[m][n], ca[m], cb[n]);
+    };
+    Frag<bf16_t> a0[MT], b0[NT], a1[MT], b1[NT];
+    if (kb < ke) {
+      wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kb);
+      lds_barrier();
+      read(0, a0, b0);
+    }
+    int kt = kb;
+    for (; kt + 1 < ke; kt += 2) {
+      step(kt, a0, b0, a1, b1);
+      step(kt + 1, a1, b1, a0, b0);
+    }
+    if (kt < ke) step(kt, a0, b0, a1, b1);
+  } else {
+    for (int kt = kb; kt < ke; ++kt) {
+      const int i = kt - kb;
+      // this wave's copies of k tile kt have landed once at most the later tiles' remain
+      wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kt);
+      lds_barrier();   // every wave's copies of tile kt are visible; tile kt-1's stage is free
+      if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
+      const char* st = smem + (i % NSTAGE) * STG;
+      Frag<bf16_t> bf[NT];
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+        bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AI + wn * NT + n) * 1024 + lane * 16);
+      if constexpr (AF32) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const float4* pa = reinterpret_cast<const float4*>(st + (wm * MT + m) * 2048 + lane * 32);
+          const float4 x0 = pa[0], x1 = pa[1];
+          const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+          Frag<bf16_t> hi, lo;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bf16_t h = f32_to_bf16(xs[e]);
+            hi.v[e] = (short)h;
+            lo.v[e] = (short)f32_to_bf16(xs[e] - bf16_to_f32(h));
+          }
+#pragma unroll
+          for (int n = 0; n < NT; ++n) {
+            mma(acc[m][n], hi, bf[n]);
+            mma(acc[m][n], lo, bf[n]);
+          }
+        }
+      } else {
+        Frag<bf16_t> af[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) af[m].v = *reinterpret_cast<const bf16x8*>(st + (wm * MT + m) * 1024 + lane * 16);
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int n = 0; n < NT; ++n) mma(acc[m][n], af[m], bf[n]);
+      }
     }
   }
 
@@ -243,7 +288,12 @@ static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t
   // makes 182 on 256 CUs: 3-5% faster there and 6% at a 512-row 4B-shape gate|up;
   // deeper LDS rings (5, 6 stages) measured no faster at any of these shapes.  Likewise
   // 128 x 96 makes 256 workgroups of the 8B gate|up at 128 rows (192 of 128 x 128):
-  // 50.6 -> 49.0 us.
+  // 50.6 -> 49.0 us.  The bf16 256-row tiles below the LM head's read each k tile's
+  // fragments during the previous tile's MFMAs (five LDS stages): 14B gate|up 112.6 ->
+  // 107.7 us, down 58.6 -> 54.4, q|k|v 29.3 -> 28.2 (round 21.10 -> 20.90 ms); at 128 rows
+  // (8B shape) the same change measured no faster, and staging the tiles through
+  // registers (16-byte loads two to four tiles ahead, written to LDS by the waves) instead
+  // of direct-to-LDS copies was slower (gate|up 119 us).
   // The output tile is split spatially, so every element is accumulated over k in the
   // same order either way.
   if (MB == 128) {
@@ -252,11 +302,14 @@ static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t
     else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<128, 128, 4, AF32, 8>), grid, dim3(512), 0, s, a);
     else if constexpr (!AF32) RT_LAUNCH((gemm_mid_kernel<128, 192, 4, false, 4>), grid, dim3(256), 0, s, a);
   } else {
-    if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, AF32, 8>), grid, dim3(512), 0, s, a);
-    else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, AF32 ? 3 : 4, AF32, 8>), grid, dim3(512), 0, s, a);
-    else if constexpr (!AF32) {
-      if (NB == 160) RT_LAUNCH((gemm_mid_kernel<256, 160, 4, false, 16>), grid, dim3(1024), 0, s, a);
-      else if (NB == 192) RT_LAUNCH((gemm_mid_kernel<256, 192, 4, false, 16>), grid, dim3(1024), 0, s, a);
+    if constexpr (AF32) {
+      if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, true, 8>), grid, dim3(512), 0, s, a);
+      else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, 3, true, 8>), grid, dim3(512), 0, s, a);
+    } else {
+      if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 5, false, 8, true>), grid, dim3(512), 0, s, a);
+      else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, 5, false, 8, true>), grid, dim3(512), 0, s, a);
+      else if (NB == 160) RT_LAUNCH((gemm_mid_kernel<256, 160, 5, false, 16, true>), grid, dim3(1024), 0, s, a);
+      else if (NB == 192) RT_LAUNCH((gemm_mid_kernel<256, 192, 5, false, 16, true>), grid, dim3(1024), 0, s, a);
       else RT_LAUNCH((gemm_mid_kernel<256, 256, 3, false, 16>), grid, dim3(1024), 0, s, a);
     }
   }
