@@ -32,7 +32,7 @@ def _exact(wl, W, R):
 
 
 @pytest.mark.parametrize("name", ["tiny-f32", "mini-bf16", "mini-bf16-ragged", "mini-bf16-gqa5", "mini-bf16-b4",
-                                  "mini-bf16-w4096", "mini-bf16-b6"])
+                                  "mini-bf16-w4096", "mini-bf16-b6", "mini-bf16-odd"])
 def test_prefill_and_rounds_match_oracle(name):
     """Prefill KV, then six rounds, each checked end to end and stage by stage (every
     layer from the GPU's own input, both LM heads from the GPU's own operands)."""

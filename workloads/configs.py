@@ -146,6 +146,15 @@ PRESETS = {
                           head_dim=64, ffn=1024),
         draft_layers=2, cond_layers=(0, 1), block_size=16, batch=6, prompt_len=(20, 200),
         new_tokens=40, seed=12),
+    # Ten sequences (160 round rows: 256-row tiles of the mid-size kernel with the fragment
+    # double buffer) at widths with odd k-tile counts (hidden 544 = 17 k tiles, FFN 1040
+    # padded to 33), so that k walks and k slabs of odd length end on the single step
+    "mini-bf16-odd": Workload(
+        name="mini-bf16-odd", dtype="bf16",
+        target=ModelShape(vocab=2048, hidden=544, n_layers=2, n_q_heads=4, n_kv_heads=2,
+                          head_dim=64, ffn=1040),
+        draft_layers=1, cond_layers=(0, 1), block_size=16, batch=10, prompt_len=(20, 80),
+        new_tokens=40, seed=13),
     # Width 4096 at batch 1 (as the Qwen3-8B shape): the LM head stages 128 KiB of
     # activations per workgroup; q and kv widths below the model width
     "mini-bf16-w4096": Workload(
