@@ -634,6 +634,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     const int h = sl >> 1, vp = sl & 1;
     voff[j] = h * 32 + (vp ^ ((h >> 3) & 1)) * 16;
   }
+  // with one row block per sequence every K / V chunk is read by one workgroup:
+  // non-temporal copies (several row blocks, as in prefill, share the chunks through cache)
+  const bool stream_kv = a.row_blocks == 1;
   auto issue = [&](int pg, int stg) {
     const char* kb = (const char*)a.kcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
     const char* vb = (const char*)a.vcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
@@ -642,12 +645,14 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     if (copies_k) {
 #pragma unroll
       for (int j = 0; j < NLD; ++j)
-        __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
+        if (stream_kv) __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, RT_NT_AUX);
+        else __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
     }
     if (copies_v) {
 #pragma unroll
       for (int j = 0; j < NLD; ++j)
-        __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
+        if (stream_kv) __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, RT_NT_AUX);
+        else __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, 0);
     }
   };
 

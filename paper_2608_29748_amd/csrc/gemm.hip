@@ -216,7 +216,7 @@ __global__ __launch_bounds__(NW * 64) void gemm16_kernel(GemmArgs a) {
     for (int u = 0; u < U; ++u) {
       const int k = kt + u < ke ? kt + u : ke - 1;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);
+      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load_stream(bptr[nt] + (size_t)k * 512);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * 512 * AB);
     }
@@ -288,7 +288,7 @@ __global__ __launch_bounds__(1024) void gemm16_slab_kernel(GemmArgs a, int tp_n,
       for (int kt = k0; kt < k1; kt += U) {
         Frag<bf16_t> bf[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) bf[u].load(bptr + (size_t)(kt + u < k1 ? kt + u : k1 - 1) * 512);
+        for (int u = 0; u < U; ++u) bf[u].load_stream(bptr + (size_t)(kt + u < k1 ? kt + u : k1 - 1) * 512);
         __builtin_amdgcn_sched_barrier(0);   // all U weight tiles in flight before the MFMAs
         if (first) {   // the A copies have landed once at most the U weight loads remain
           wait_vm<U>();
@@ -424,7 +424,7 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(GemmArgs a) {
     for (int u = 0; u < U; ++u) {
       const int k = kt + u < ke ? kt + u : ke - 1;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);
+      for (int nt = 0; nt < NT; ++nt) bf[u][nt].load(bptr[nt] + (size_t)k * 512);   // re-read by every row tile
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)k * 512 * AB);
     }
@@ -673,8 +673,8 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
       Frag<T> af[U][MT];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        bf[u][0].load(bptr[0] + (size_t)(kt + u) * 512);
-        bf[u][1].load(bptr[1] + (size_t)(kt + u) * 512);
+        bf[u][0].load_stream(bptr[0] + (size_t)(kt + u) * 512);
+        bf[u][1].load_stream(bptr[1] + (size_t)(kt + u) * 512);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) af[u][mt].load(aptr[mt] + (size_t)(kt + u) * 512);
       }
@@ -689,8 +689,8 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmHeadArgs a) {
     }
     for (; kt < KT; ++kt) {
       Frag<T> b0, b1, af[MT];
-      b0.load(bptr[0] + (size_t)kt * 512);
-      b1.load(bptr[1] + (size_t)kt * 512);
+      b0.load_stream(bptr[0] + (size_t)kt * 512);
+      b1.load_stream(bptr[1] + (size_t)kt * 512);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) af[mt].load(aptr[mt] + (size_t)kt * 512);
 #pragma unroll
@@ -768,7 +768,7 @@ __global__ __launch_bounds__(kLmWaves * 64) void lmhead_lds_kernel(LmHeadArgs a)
     for (int kt = 0; kt < KT; kt += U) {
       Frag<bf16_t> bf[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) bf[u].load(bptr + (size_t)(kt + u < KT ? kt + u : KT - 1) * 512);
+      for (int u = 0; u < U; ++u) bf[u].load_stream(bptr + (size_t)(kt + u < KT ? kt + u : KT - 1) * 512);
       __builtin_amdgcn_sched_barrier(0);   // all U weight tiles in flight before the MFMAs
 #pragma unroll
       for (int u = 0; u < U; ++u)

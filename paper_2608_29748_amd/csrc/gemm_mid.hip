@@ -144,11 +144,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     if (nt >= n_tiles_valid) nt = n_tiles_valid - 1;
     return (const char*)a.B + ((size_t)nt * KT + kt) * 1024;
   };
+  // With one row tile every weight tile is read by one workgroup: non-temporal copies.
+  // The A fragments, which every workgroup reads, and weights that several row tiles
+  // read stay cached.
+  const bool stream_b = gridDim.y == 1;
   auto issue = [&](int kt, int stg) {
 #pragma unroll
-    for (int j = 0; j < LPW; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(item_src(j, kt) + lane * 16),
-                                       (lds_void_t*)(smem + stg * STG + item_of(j) * 1024), 16, 0, 0);
+    for (int j = 0; j < LPW; ++j) {
+      const void* src = item_src(j, kt) + lane * 16;
+      lds_void_t* dst = (lds_void_t*)(smem + stg * STG + item_of(j) * 1024);
+      if (item_of(j) >= AI && stream_b) __builtin_amdgcn_global_load_lds(src, dst, 16, 0, RT_NT_AUX);
+      else __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+    }
   };
 
   f32x4 acc[MT][NT];
