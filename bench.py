@@ -189,12 +189,12 @@ def target_only(eng, wl, prompts, steps: int, spec_value: float, warmup: int = 4
 
 
 def stream_ceiling(nbytes: int, buf) -> dict:
-    """Best plain-read time of nbytes (one kernel, 1024 or 2048 workgroups, 20 launches
-    each, every launch on data the memory-side cache does not hold) on this GPU: the
-    streaming ceiling of a single kernel of that size."""
+    """Best plain-read time of nbytes (one kernel of non-temporal loads, 512, 1024 or 2048
+    workgroups, 20 launches each, every launch on data the memory-side cache does not
+    hold) on this GPU: the streaming ceiling of a single kernel of that size."""
     from paper_2608_29748_amd import binding as B
     n = max(16, int(nbytes) // 16 * 16)
-    us = min(B.rt_stream_read(buf.data_ptr(), buf.numel(), n, g, 20) for g in (1024, 2048))
+    us = min(B.rt_stream_read(buf.data_ptr(), buf.numel(), n, g, 20) for g in (512, 1024, 2048))
     return {"bytes": n, "us": us, "GBs": n / (us * 1e-6) / 1e9}
 
 

@@ -246,7 +246,8 @@ int rt_time_kernel(rt_model* m, int32_t kind, int32_t reps, rt_kernel_stat* stat
 /* The plain-read ceiling against which the round's weight-streaming kernels are
  * compared: `reps` (1..1000) back-to-back launches of a kernel that reads `bytes` (a
  * positive multiple of 16, at most buf_bytes) of the device buffer d_buf (256-byte
- * aligned, buf_bytes long) once, with `grid` (1..65536) workgroups of 256 threads,
+ * aligned, buf_bytes long) once with non-temporal 16-byte loads, each of `grid`
+ * (1..65536) workgroups of 256 threads reading one contiguous share,
  * between two HIP events on hip_stream (a hipStream_t; NULL = default stream).
  * Launch r reads the window starting at ((r + 1) * bytes) mod (buf_bytes - bytes + 1)
  * rounded down to 256 bytes, so that with buf_bytes well above the 256 MB memory-side

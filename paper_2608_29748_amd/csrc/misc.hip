@@ -418,21 +418,26 @@ void fill_zero(void* p, size_t bytes, hipStream_t s) {
   RT_LAUNCH(fill_zero_kernel, dim3((unsigned)g), dim3(256), 0, s, (uint4*)p, n16);
 }
 
-// Plain read of a buffer: every byte loaded once with 16-byte loads, four in flight per
-// lane, grid-strided; the values feed a store guarded by a runtime flag (passed as 0), so
-// no load can be dropped and nothing is written.
+// Plain read of a buffer: every byte loaded once with non-temporal 16-byte loads (as the
+// weight streams), workgroup b reading the b-th contiguous share, eight loads in flight
+// per lane; the values feed a store guarded by a runtime flag (passed as 0), so no load
+// can be dropped and nothing is written.
 __global__ __launch_bounds__(256) void stream_read_kernel(const uint4* __restrict__ p, size_t n16, uint32_t* sink,
                                                           int store) {
+  typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+  const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const size_t b0 = blockIdx.x * per, b1 = b0 + per < n16 ? b0 + per : n16;
+  const v4u* q = reinterpret_cast<const v4u*>(p);
   uint32_t acc = 0;
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const uint4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
-    acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^ (d.x ^ d.y ^ d.z ^ d.w);
-  }
-  for (; i < n16; i += stride) {
-    const uint4 a = p[i];
-    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  for (size_t i = b0 + threadIdx.x; i < b1; i += 8 * (size_t)blockDim.x) {
+    v4u v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const size_t j = i + (size_t)u * blockDim.x;
+      v[u] = __builtin_nontemporal_load(q + (j < b1 ? j : i));
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
   if (store) sink[blockIdx.x * blockDim.x + threadIdx.x] = acc;
 }
