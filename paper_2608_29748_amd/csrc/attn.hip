@@ -414,6 +414,17 @@ __device__ __forceinline__ float xor16_sum(float v) {
   return __uint_as_float(p[0]) + __uint_as_float(p[1]);
 }
 
+// Wait until at most min(N, r) chunks of LPC copies each (this wave's) are in flight.
+template <int N, int LPC>
+__device__ __forceinline__ void wait_chunks(int r) {
+  if constexpr (N <= 0) {
+    wait_vm<0>();
+  } else {
+    if (r >= N) wait_vm<N * LPC>();
+    else wait_chunks<N - 1, LPC>(r);
+  }
+}
+
 // LDS accesses hidden from the compiler's wait insertion, which would otherwise wait
 // for every direct-to-LDS copy in flight before them (the next chunk's copies
 // included).  lds_wait() waits for them; a value read is used only after lds_wait() and
@@ -894,11 +905,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   for (int c = c_beg; c < c_end; ++c) {
     const int i = c - c_beg;
     // this wave's copies of chunk c have landed once at most the later chunks' remain
-    if constexpr (NSTAGE >= 3) {
-      if (c + 1 < c_end) wait_vm<LPC>(); else wait_vm<0>();
-    } else {
-      wait_vm<0>();
-    }
+    wait_chunks<NSTAGE - 2, LPC>(c_end - 1 - c);
     lds_barrier();   // every wave's copies of chunk c are visible; chunk c-1's stage is free
     if (STAGED && !q_wave && c == c_beg) {   // the pair's normalised q from key half 0
       u32x4 qr[NKS];
@@ -1171,9 +1178,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane * PL + e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
-// One query tile per wave: 64-row blocks 8 waves, two LDS stages (64 KB at hd 128);
-// 96-row blocks 12 waves, three stages (96 KB; 15% faster than 4 waves of three tiles
-// at the 14B verify shape).  Results do not depend on the wave layout (the key-half
+// One query tile per wave: 64-row blocks 8 waves with three LDS stages (96 KB at hd 128;
+// 8B batch-8 rounds 34.2 -> 32.6 us per layer against two stages, four 33.3), two where
+// the kernel stages the q / k work's inputs (they take the third stage's room); 96-row
+// blocks 12 waves, three stages (96 KB; 15% faster than 4 waves of three tiles at the 14B
+// verify shape, where four stages measured no faster).  Results do not depend on the wave layout (the key-half
 // merge is written in explicit fused form).
 template <typename T>
 hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
@@ -1190,9 +1199,9 @@ hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
       else return hipErrorInvalidValue;
     } else if (a.rb_rows == 64) {
       if (a.head_dim == 128 && f) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
-      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
       else if (a.head_dim == 64 && f) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
       else return hipErrorInvalidValue;
     } else {
       return hipErrorInvalidValue;
