@@ -1178,9 +1178,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int e = 0; e < PL; ++e) out[pa_index(orow, h * HD + lane * PL + e, a.ldo)] = Elem<T>::from_f32(num[e] * inv);
 }
 
-// One query tile per wave: 64-row blocks 8 waves with three LDS stages (96 KB at hd 128;
-// 8B batch-8 rounds 34.2 -> 32.6 us per layer against two stages, four 33.3), two where
-// the kernel stages the q / k work's inputs (they take the third stage's room); 96-row
+// One query tile per wave: 64-row blocks 8 waves with two LDS stages (64 KB at hd 128,
+// two workgroups per compute unit), or three (96 KB) where every split holds long key
+// ranges: 8B batch-8 rounds 34.2 -> 32.6 us per layer (four stages 33.3), while the
+// short contexts of a 16-sequence serving batch ran 0.6 us slower with three; the kernel
+// that stages the q / k work's inputs keeps two (they take the third stage's room); 96-row
 // blocks 12 waves, three stages (96 KB; 15% faster than 4 waves of three tiles at the 14B
 // verify shape, where four stages measured no faster).  Results do not depend on the wave layout (the key-half
 // merge is written in explicit fused form).
@@ -1198,10 +1200,16 @@ hipError_t attention_partials(const AttnArgs& a, hipStream_t s) {
       else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 12, false>), grid, dim3(768), 0, s, a);
       else return hipErrorInvalidValue;
     } else if (a.rb_rows == 64) {
+      // a third stage where each split holds long key ranges (16 or more chunks at the
+      // longest context, one row block per sequence); otherwise two stages keep two
+      // workgroups per compute unit
+      const bool deep = a.row_blocks == 1 && a.max_pages / 4 >= 16 * a.splits;
       if (a.head_dim == 128 && f) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
-      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 128 && deep) RT_LAUNCH((attn_bf16_kernel<128, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 128) RT_LAUNCH((attn_bf16_kernel<128, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
       else if (a.head_dim == 64 && f) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, true>), grid, dim3(512), 0, s, a);
-      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64 && deep) RT_LAUNCH((attn_bf16_kernel<64, 3, 1, 8, false>), grid, dim3(512), 0, s, a);
+      else if (a.head_dim == 64) RT_LAUNCH((attn_bf16_kernel<64, 2, 1, 8, false>), grid, dim3(512), 0, s, a);
       else return hipErrorInvalidValue;
     } else {
       return hipErrorInvalidValue;
