@@ -178,3 +178,24 @@ def test_weight_elements_follow_the_canonical_order(B, name, mode):
     for i, (_, shape, _) in enumerate(specs):
         assert B.rt_weight_elements(c, i) == int(np.prod(shape)), (i, specs[i])
     assert B.rt_weight_elements(c, len(specs)) == 0 and B.rt_weight_elements(c, -1) == 0
+
+
+def test_stream_read_argument_checks(B):
+    """rt_stream_read rejects its documented invalid arguments before any device work."""
+    us = C.c_double()
+    buf = 1 << 20   # a 256-byte-aligned stand-in address: never dereferenced on these paths
+
+    def call(ptr=buf, buf_bytes=1 << 20, nbytes=4096, grid=64, reps=1, out=True):
+        return B._lib.rt_stream_read(C.c_void_p(ptr), buf_bytes, nbytes, grid, reps, None,
+                                     C.byref(us) if out else None)
+
+    assert call(ptr=0) == B.RT_ERR_INVALID and "null" in B.rt_last_error()
+    assert call(out=False) == B.RT_ERR_INVALID
+    assert call(nbytes=0) == B.RT_ERR_INVALID and "multiple of 16" in B.rt_last_error()
+    assert call(nbytes=4100) == B.RT_ERR_INVALID
+    assert call(ptr=buf + 16) == B.RT_ERR_INVALID and "aligned" in B.rt_last_error()
+    assert call(nbytes=2 << 20) == B.RT_ERR_INVALID and "exceed" in B.rt_last_error()
+    assert call(grid=0) == B.RT_ERR_INVALID and "grid" in B.rt_last_error()
+    assert call(grid=65537) == B.RT_ERR_INVALID
+    assert call(reps=0) == B.RT_ERR_INVALID and "reps" in B.rt_last_error()
+    assert call(reps=1001) == B.RT_ERR_INVALID

@@ -185,3 +185,18 @@ def test_measurement_calls_leave_the_rounds_unchanged():
         np.testing.assert_array_equal(t0, t1)
         np.testing.assert_array_equal(n0, n1)
         np.testing.assert_array_equal(h0, h1)
+
+
+def test_stream_read_probe():
+    """The plain-read ceiling probe (non-temporal contiguous reads) runs on a device buffer,
+    stays within it for every window and reports longer times for larger reads."""
+    import torch
+    buf = torch.zeros(128 << 20, dtype=torch.uint8, device="cuda")
+    assert buf.data_ptr() % 256 == 0
+    small = B.rt_stream_read(buf.data_ptr(), buf.numel(), 4 << 20, 512, 5)
+    large = B.rt_stream_read(buf.data_ptr(), buf.numel(), 64 << 20, 512, 5)
+    whole = B.rt_stream_read(buf.data_ptr(), buf.numel(), buf.numel(), 2048, 3)   # one window only
+    torch.cuda.synchronize()
+    log(f"stream probe: 4 MiB {small:.2f} us, 64 MiB {large:.2f} us, 128 MiB {whole:.2f} us")
+    assert 0 < small < large < whole
+    assert float(buf.sum()) == 0.0   # nothing was written
