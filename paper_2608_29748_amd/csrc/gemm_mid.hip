@@ -20,6 +20,8 @@
 // running the epilogue.
 #include "gemm.h"
 
+#include <type_traits>
+
 namespace rt {
 
 // Epilogue of one wave's accumulators: tile (m, n) covers rows rbase + 16 m + 0..3
@@ -104,7 +106,7 @@ __device__ __forceinline__ void wait_tiles(int r) {
   }
 }
 
-template <int MB, int NB, int NSTAGE, bool AF32, int NW, bool DB = false>
+template <int MB, int NB, int NSTAGE, bool AF32, int NW, bool DB = false, bool NTB = false>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_mid_kernel(GemmArgs a) {
   constexpr int WM = NW / 2;            // wave rows (two wave columns)
   constexpr int MT = MB / (16 * WM);    // 16-row tiles per wave
@@ -176,21 +178,52 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // multiply tile kt's.  The last step reads a stale stage into registers nobody uses, so
     // that every step has one shape and the compiler's wait before the MFMAs covers only
     // the previous step's reads.
-    auto read = [&](int stg, Frag<bf16_t>(&af)[MT], Frag<bf16_t>(&bf)[NT]) {
-      const char* st = smem + stg * STG;
+    //
+    // Per step the scalar work is kept small: every copy's source advances by one 1 KiB k
+    // tile per step from a pointer set up once, and the stages to fill and to read are
+    // byte offsets that advance by one stage with a wrap (no products or divisions).
+    auto read = [&](int off, Frag<bf16_t>(&af)[MT], Frag<bf16_t>(&bf)[NT]) {
+      const char* st = smem + off;
 #pragma unroll
       for (int m = 0; m < MT; ++m) af[m].v = *reinterpret_cast<const bf16x8*>(st + (wm * MT + m) * 1024 + lane * 16);
 #pragma unroll
       for (int n = 0; n < NT; ++n) bf[n].v = *reinterpret_cast<const bf16x8*>(st + (AI + wn * NT + n) * 1024 + lane * 16);
     };
-    auto step = [&](int kt, Frag<bf16_t>(&ca)[MT], Frag<bf16_t>(&cb)[NT], Frag<bf16_t>(&na)[MT],
+    // (NTB: the weight copies are non-temporal, chosen by the launch: one row tile)
+    const char* csrc[LPW];   // this wave's copy j of the next tile to issue (kb + NSTAGE - 1)
+    int cdst[LPW];
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      csrc[j] = item_src(j, kb) + (size_t)(NSTAGE - 1) * 1024 + lane * 16;
+      cdst[j] = item_of(j) * 1024;
+    }
+    // copies j < AI / NW of every wave are A items, the later ones weight tiles, except
+    // past the last item, where a wave repeats A item 0 (kept cached)
+    static_assert(!NTB || AI % NW == 0, "non-temporal copies: A items fill whole rounds of the waves");
+    const bool last_is_b = w + NW * (LPW - 1) < IT;
+    constexpr int RING = NSTAGE * STG;
+    int off_is = (NSTAGE - 1) * STG, off_rd = STG;   // step 0 fills stage NSTAGE-1 and reads stage 1
+    // STEADY: the step and the next both issue a tile, so NSTAGE - 3 later tiles are in
+    // flight whatever the slab's length
+    auto step = [&](int kt, auto steady, Frag<bf16_t>(&ca)[MT], Frag<bf16_t>(&cb)[NT], Frag<bf16_t>(&na)[MT],
                     Frag<bf16_t>(&nb)[NT]) {
-      const int i = kt - kb;
-      wait_tiles<NSTAGE - 3, LPW>(ke - 2 - kt);
+      if constexpr (decltype(steady)::value) wait_vm<(NSTAGE - 3) * LPW>();
+      else wait_tiles<NSTAGE - 3, LPW>(ke - 2 - kt);
       wait_lds();
       lds_barrier();
-      if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
-      read((i + 1) % NSTAGE, na, nb);
+      if (decltype(steady)::value || kt + NSTAGE - 1 < ke) {
+#pragma unroll
+        for (int j = 0; j < LPW; ++j) {
+          lds_void_t* dst = (lds_void_t*)(smem + off_is + cdst[j]);
+          if (NTB && j >= AI / NW && (j < LPW - 1 || IT % NW == 0 || last_is_b))
+            __builtin_amdgcn_global_load_lds((const void*)csrc[j], dst, 16, 0, RT_NT_AUX);
+          else __builtin_amdgcn_global_load_lds((const void*)csrc[j], dst, 16, 0, 0);
+          csrc[j] += 1024;
+        }
+      }
+      read(off_rd, na, nb);
+      off_is = off_is + STG == RING ? 0 : off_is + STG;
+      off_rd = off_rd + STG == RING ? 0 : off_rd + STG;
 #pragma unroll
       for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -200,14 +233,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     if (kb < ke) {
       wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kb);
       lds_barrier();
-      read(0, a0, b0);
+      read(0, a0, b0);   // stage 0
     }
     int kt = kb;
-    for (; kt + 1 < ke; kt += 2) {
-      step(kt, a0, b0, a1, b1);
-      step(kt + 1, a1, b1, a0, b0);
+    for (; kt + NSTAGE < ke; kt += 2) {
+      step(kt, std::true_type{}, a0, b0, a1, b1);
+      step(kt + 1, std::true_type{}, a1, b1, a0, b0);
     }
-    if (kt < ke) step(kt, a0, b0, a1, b1);
+    for (; kt + 1 < ke; kt += 2) {
+      step(kt, std::false_type{}, a0, b0, a1, b1);
+      step(kt + 1, std::false_type{}, a1, b1, a0, b0);
+    }
+    if (kt < ke) step(kt, std::false_type{}, a0, b0, a1, b1);
   } else {
     for (int kt = kb; kt < ke; ++kt) {
       const int i = kt - kb;
@@ -313,9 +350,15 @@ static void mid_launch(const GemmArgs& a, int MB, int NB, dim3 grid, hipStream_t
       if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 3, true, 8>), grid, dim3(512), 0, s, a);
       else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, 3, true, 8>), grid, dim3(512), 0, s, a);
     } else {
-      if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 5, false, 8, true>), grid, dim3(512), 0, s, a);
+      // one row tile: every weight tile is read by one workgroup (non-temporal copies)
+      const bool one = grid.y == 1;
+      if (NB == 64 && one) RT_LAUNCH((gemm_mid_kernel<256, 64, 5, false, 8, true, true>), grid, dim3(512), 0, s, a);
+      else if (NB == 64) RT_LAUNCH((gemm_mid_kernel<256, 64, 5, false, 8, true>), grid, dim3(512), 0, s, a);
+      else if (NB == 128 && one) RT_LAUNCH((gemm_mid_kernel<256, 128, 5, false, 8, true, true>), grid, dim3(512), 0, s, a);
       else if (NB == 128) RT_LAUNCH((gemm_mid_kernel<256, 128, 5, false, 8, true>), grid, dim3(512), 0, s, a);
+      else if (NB == 160 && one) RT_LAUNCH((gemm_mid_kernel<256, 160, 5, false, 16, true, true>), grid, dim3(1024), 0, s, a);
       else if (NB == 160) RT_LAUNCH((gemm_mid_kernel<256, 160, 5, false, 16, true>), grid, dim3(1024), 0, s, a);
+      else if (NB == 192 && one) RT_LAUNCH((gemm_mid_kernel<256, 192, 5, false, 16, true, true>), grid, dim3(1024), 0, s, a);
       else if (NB == 192) RT_LAUNCH((gemm_mid_kernel<256, 192, 5, false, 16, true>), grid, dim3(1024), 0, s, a);
       else RT_LAUNCH((gemm_mid_kernel<256, 256, 3, false, 16>), grid, dim3(1024), 0, s, a);
     }
