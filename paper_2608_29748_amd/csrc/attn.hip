@@ -648,18 +648,37 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   // with one row block per sequence every K / V chunk is read by one workgroup:
   // non-temporal copies (several row blocks, as in prefill, share the chunks through cache)
   const bool stream_kv = a.row_blocks == 1;
-  auto issue = [&](int pg, int stg) {
-    const char* kb = (const char*)a.kcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
-    const char* vb = (const char*)a.vcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
-    char* lk = smem + stg * STG + cw * PGB;
-    char* lv = smem + stg * STG + PAGES * PGB + cw * PGB;
-    if (copies_k) {
+  // With SPREAD a copying wave copies one page of K or one of V: its cache, per-lane
+  // offsets and LDS slice are chosen once here, so that a chunk's copies cost one branch
+  // and one page address.  stg_off: the byte offset of the stage.
+  const char* const kvsrc = copies_k ? (const char*)a.kcache : (const char*)a.vcache;
+  int coff[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) coff[j] = copies_k ? koff[j] : voff[j];
+  const int lslice = (copies_k ? 0 : PAGES * PGB) + cw * PGB;
+  auto issue = [&](int pg, int stg_off) {
+    if constexpr (SPREAD) {
+      if (!copies_k && !copies_v) return;
+      const char* b = kvsrc + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
+      char* l = smem + stg_off + lslice;
+      if (stream_kv) {
+#pragma unroll
+        for (int j = 0; j < NLD; ++j)
+          __builtin_amdgcn_global_load_lds((const void*)(b + coff[j]), (lds_void_t*)(l + j * 1024), 16, 0, RT_NT_AUX);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NLD; ++j)
+          __builtin_amdgcn_global_load_lds((const void*)(b + coff[j]), (lds_void_t*)(l + j * 1024), 16, 0, 0);
+      }
+    } else {
+      const char* kb = (const char*)a.kcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
+      const char* vb = (const char*)a.vcache + ((size_t)pg * a.n_kv_heads + kvh) * PGB;
+      char* lk = smem + stg_off + cw * PGB;
+      char* lv = smem + stg_off + PAGES * PGB + cw * PGB;
 #pragma unroll
       for (int j = 0; j < NLD; ++j)
         if (stream_kv) __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, RT_NT_AUX);
         else __builtin_amdgcn_global_load_lds((const void*)(kb + koff[j]), (lds_void_t*)(lk + j * 1024), 16, 0, 0);
-    }
-    if (copies_v) {
 #pragma unroll
       for (int j = 0; j < NLD; ++j)
         if (stream_kv) __builtin_amdgcn_global_load_lds((const void*)(vb + voff[j]), (lds_void_t*)(lv + j * 1024), 16, 0, RT_NT_AUX);
@@ -775,7 +794,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   // prologue: chunks c_beg .. c_beg+NSTAGE-2 in flight
 #pragma unroll
   for (int i = 0; i < NSTAGE - 1; ++i)
-    if (c_beg + i < c_end) issue(page_of(c_beg + i), i);
+    if (c_beg + i < c_end) issue(page_of(c_beg + i), i * STG);
   int pg_next = page_of(c_beg + NSTAGE - 1);
 
   if constexpr (STAGED) {
@@ -902,8 +921,13 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   const bool b_mine = fused && b_any && P + bi >= kb_lo && P + bi < kb_hi;   // a row this workgroup caches
   const int b_page = b_mine ? pt[(P + bi) / kPage] : 0;
 
+  // byte offsets of chunk c's stage and of the stage its step fills (chunk c+NSTAGE-1),
+  // advanced by one stage per chunk with a wrap
+  int off_c = 0, off_n = (NSTAGE - 1) * STG;
   for (int c = c_beg; c < c_end; ++c) {
-    const int i = c - c_beg;
+    const int cur = off_c, nxt = off_n;
+    off_c = off_c + STG == NSTAGE * STG ? 0 : off_c + STG;
+    off_n = off_n + STG == NSTAGE * STG ? 0 : off_n + STG;
     // this wave's copies of chunk c have landed once at most the later chunks' remain
     wait_chunks<NSTAGE - 2, LPC>(c_end - 1 - c);
     lds_barrier();   // every wave's copies of chunk c are visible; chunk c-1's stage is free
@@ -925,7 +949,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
       const int pos = P + bi;
       if (b_any && pos >= max(kb_lo, c * kChunk) && pos < min(kb_hi, (c + 1) * kChunk)) {
         const int pg = pos / kPage - c * PAGES, r = pos % kPage;
-        char* st = smem + (i % NSTAGE) * STG + (b_v ? PAGES * PGB : 0) + pg * PGB;
+        char* st = smem + cur + (b_v ? PAGES * PGB : 0) + pg * PGB;
         u32x4 v = lds_ld16(bside);
         lds_wait();
         lds_hold(v);
@@ -941,11 +965,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
       lds_barrier();
     }
     if (c + NSTAGE - 1 < c_end) {
-      issue(pg_next, (i + NSTAGE - 1) % NSTAGE);
+      issue(pg_next, nxt);
       pg_next = page_of(c + NSTAGE);
     }
     if (nrt == 0) continue;
-    const char* sk = smem + (i % NSTAGE) * STG;
+    const char* sk = smem + cur;
     const char* sv = sk + PAGES * PGB;
     const int kbase = c * kChunk + kh * 32;
     // fragments of this wave's 32 keys: K (2 score tiles x NKS), V^T (NHT)
