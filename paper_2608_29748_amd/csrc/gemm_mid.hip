@@ -246,13 +246,42 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     }
     if (kt < ke) step(kt, std::false_type{}, a0, b0, a1, b1);
   } else {
-    for (int kt = kb; kt < ke; ++kt) {
-      const int i = kt - kb;
+    // As in the double-buffered loop, little scalar work per k tile: every copy's source
+    // advances by one k tile (2 KiB for fp32 A fragments, 1 KiB otherwise) from a pointer
+    // set up once, stage offsets are counters, and one constant wait serves every step
+    // that still issues a tile.
+    const char* csrc[LPW];
+    int cdst[LPW], cstep[LPW];
+    bool cnt[LPW];
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      const int it = item_of(j);
+      cstep[j] = it < AI ? AB : 1024;
+      csrc[j] = item_src(j, kb) + (size_t)(NSTAGE - 1) * cstep[j] + lane * 16;
+      cdst[j] = it * 1024;
+      cnt[j] = it >= AI && stream_b;
+    }
+    constexpr int RING = NSTAGE * STG;
+    int off_is = (NSTAGE - 1) * STG, off_rd = 0;   // tile kb + NSTAGE - 1 fills the last stage
+    // STEADY: tile kt + NSTAGE - 1 exists, so NSTAGE - 2 later tiles are in flight
+    auto step1 = [&](int kt, auto steady) {
       // this wave's copies of k tile kt have landed once at most the later tiles' remain
-      wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kt);
+      if constexpr (decltype(steady)::value) wait_vm<(NSTAGE - 2) * LPW>();
+      else wait_tiles<NSTAGE - 2, LPW>(ke - 1 - kt);
+      wait_lds();      // this wave's LDS reads of tile kt-1 are done
       lds_barrier();   // every wave's copies of tile kt are visible; tile kt-1's stage is free
-      if (kt + NSTAGE - 1 < ke) issue(kt + NSTAGE - 1, (i + NSTAGE - 1) % NSTAGE);
-      const char* st = smem + (i % NSTAGE) * STG;
+      if (decltype(steady)::value || kt + NSTAGE - 1 < ke) {
+#pragma unroll
+        for (int j = 0; j < LPW; ++j) {
+          lds_void_t* dst = (lds_void_t*)(smem + off_is + cdst[j]);
+          if (cnt[j]) __builtin_amdgcn_global_load_lds((const void*)csrc[j], dst, 16, 0, RT_NT_AUX);
+          else __builtin_amdgcn_global_load_lds((const void*)csrc[j], dst, 16, 0, 0);
+          csrc[j] += cstep[j];
+        }
+      }
+      const char* st = smem + off_rd;
+      off_is = off_is + STG == RING ? 0 : off_is + STG;
+      off_rd = off_rd + STG == RING ? 0 : off_rd + STG;
       Frag<bf16_t> bf[NT];
 #pragma unroll
       for (int n = 0; n < NT; ++n)
@@ -285,7 +314,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 #pragma unroll
           for (int n = 0; n < NT; ++n) mma(acc[m][n], af[m], bf[n]);
       }
-    }
+    };
+    int kt = kb;
+    for (; kt + NSTAGE - 1 < ke; ++kt) step1(kt, std::true_type{});
+    for (; kt < ke; ++kt) step1(kt, std::false_type{});
   }
 
   // epilogue from the accumulators: lane (g4, c16) of tile (m, n) holds rows
