@@ -69,23 +69,30 @@ def dominant_desc(wl):
 
 GEMM_SOURCES = ("paper_2608_29748_amd/csrc/gemm.hip", "paper_2608_29748_amd/csrc/gemm.h",
                 "paper_2608_29748_amd/csrc/common.h")
+MID_SOURCES = GEMM_SOURCES + ("paper_2608_29748_amd/csrc/gemm_mid.hip",)
 
 
-def gemm_source_hash() -> str:
+def traffic_sources(wl):
+    """The sources a traffic record of the dominant GEMM depends on: the mid-size kernel
+    (more than 64 rows per round) adds its own file."""
+    return MID_SOURCES if wl.batch * wl.block_size > 64 else GEMM_SOURCES
+
+
+def gemm_source_hash(sources=GEMM_SOURCES) -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in GEMM_SOURCES:
+    for f in sources:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
+def measured_traffic(wl):
     """HBM bytes per launch of the dominant kernel from the committed counter summary
     (rocprofv3 FETCH_SIZE and WRITE_SIZE passes, each scaled by the same counter's
     reading for a plain copy of known size); None when that summary was taken on
     different kernel sources or is absent."""
-    path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{workload}_traffic.md")
+    path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{wl.name}_traffic.md")
     if not os.path.exists(path):
         return None
     rec = None
@@ -93,7 +100,7 @@ def measured_traffic(workload: str):
         for line in fh:
             if line.startswith("traffic-json:"):
                 rec = json.loads(line.split(":", 1)[1])
-    if not rec or rec.get("source_sha256") != gemm_source_hash():
+    if not rec or rec.get("source_sha256") != gemm_source_hash(traffic_sources(wl)):
         return None
     return rec["bytes_per_launch"]
 
@@ -354,7 +361,7 @@ def main():
                    "top_k": wl.top_k, "top_p": wl.top_p, "parallelism": "single GPU"},
         "roofline": {"bound": bound, "kernel": dominant_desc(wl),
                      "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-                     "traffic": measured_traffic(wl.name), "traffic_unit": "bytes per launch (HBM fetch + write)",
+                     "traffic": measured_traffic(wl), "traffic_unit": "bytes per launch (HBM fetch + write)",
                      "algorithmic_bytes_per_launch": per_launch_bytes, "algorithmic_flops_per_launch": per_launch_flops,
                      "us_per_launch": per_launch_us,
                      "hbm_frac": per_launch_bytes / (per_launch_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
